@@ -1,0 +1,266 @@
+"""Prof-K top-k selection on MI355X: Python binding of libprofk.so.
+
+This module only marshals arguments: every step of the selection runs in the
+HIP kernels of libprofk.so (built by paper_2608_12573_amd.build).  PyTorch
+provides device memory and the current stream.  If the library has not been
+built, every call raises instead of computing anything on the CPU.
+
+    vals, idx, info = topk(x, k)                  # x: 1-D fp32/bf16 CUDA tensor
+    vals, idx, info = topk_rows(x, k)             # x: [B, D]
+    vals, idx, info = batchtopk(x, k_row)         # global top-(B*k_row) of [B, D]
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libprofk.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "profk.h")
+
+F32 = 0
+BF16 = 1
+MODE_FILTER, MODE_DIRECT = 0, 1
+FORCE_AUTO, FORCE_FILTER, FORCE_DIRECT = 0, 1, 2
+STATUS_FILTERED, STATUS_UNDERFLOW, STATUS_OVERFLOW, STATUS_DIRECT = 0, 1, 2, 3
+OK, EINVAL, EDTYPE, EWORKSPACE, ENULL, EHIP = 0, -1, -2, -3, -4, -5
+
+
+class PlanOpts(ctypes.Structure):
+    _fields_ = [("S_min", ctypes.c_int32), ("S_max", ctypes.c_int32),
+                ("cost_ratio", ctypes.c_double), ("eps_split", ctypes.c_double),
+                ("paper_literal", ctypes.c_int32), ("force_mode", ctypes.c_int32)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("k", ctypes.c_int64),
+                ("eps", ctypes.c_double), ("recall", ctypes.c_double),
+                ("k_req", ctypes.c_int64), ("S", ctypes.c_int64), ("t", ctypes.c_int64),
+                ("M", ctypes.c_int64), ("mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("p_underflow", ctypes.c_double), ("p_overflow", ctypes.c_double)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+
+
+INFO_DTYPE = np.dtype([("count", "<u8"), ("tau_key", "<u4"), ("status", "<i4"), ("n_valid", "<i8")])
+INFO_BYTES = INFO_DTYPE.itemsize
+
+
+class ProfkError(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libprofk.so; raises when it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ProfkError(f"{LIB_PATH} is missing: run paper_2608_12573_amd.build.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, u32, u64, dbl = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                       ctypes.c_uint32, ctypes.c_uint64, ctypes.c_double)
+        P = ctypes.POINTER
+        L.profk_default_opts.argtypes = [P(PlanOpts)]
+        L.profk_default_row_opts.argtypes = [P(PlanOpts)]
+        L.profk_plan.argtypes = [i64, i64, dbl, dbl, P(PlanOpts), P(Plan)]
+        L.profk_plan_rows.argtypes = [i64, i64, dbl, dbl, P(PlanOpts), P(Plan)]
+        L.profk_workspace_size.argtypes = [P(Plan), i32, i64]
+        L.profk_workspace_size.restype = ctypes.c_size_t
+        L.profk_topk.argtypes = [P(Plan), i32, vp, i64, i64, u64, vp, vp, vp, ctypes.c_size_t, vp, vp]
+        L.profk_topk_tau.argtypes = [P(Plan), i32, vp, i64, i64, u32, vp, vp, vp, ctypes.c_size_t, vp, vp]
+        L.profk_topk_simple.argtypes = [vp, i64, i64, u64, vp, vp]
+        L.profk_topk_rows.argtypes = [P(Plan), i32, vp, i64, i64, i64, i64, u64, vp, vp, vp,
+                                      ctypes.c_size_t, vp, vp]
+        L.profk_batchtopk.argtypes = [P(Plan), i32, vp, i64, i64, i64, u64, vp, vp, vp,
+                                      ctypes.c_size_t, vp, vp]
+        L.profk_debug_sample_indices.argtypes = [u64, i64, i64, i64, vp, vp]
+        L.profk_debug_filter.argtypes = [P(Plan), i32, vp, i64, u32, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.profk_status_string.argtypes = [ctypes.c_int]
+        L.profk_status_string.restype = ctypes.c_char_p
+        L.profk_last_hip_error.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def header_functions():
+    """Names of the functions include/profk.h declares."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(profk_\w+)\s*\(", text)))
+
+
+def _check(rc):
+    if rc != OK:
+        msg = lib().profk_status_string(rc).decode()
+        if rc == EHIP:
+            msg += f" (hipError {lib().profk_last_hip_error()})"
+        raise ProfkError(msg)
+
+
+def opts(flat=True, **kw):
+    o = PlanOpts()
+    (lib().profk_default_opts if flat else lib().profk_default_row_opts)(ctypes.byref(o))
+    for key, val in kw.items():
+        setattr(o, key, val)
+    return o
+
+
+def plan(N, k, eps=1e-6, recall=1.0, **kw):
+    """profk_plan: (S, t, M) for N values and top-k."""
+    p = Plan()
+    _check(lib().profk_plan(N, k, eps, recall, ctypes.byref(opts(True, **kw)), ctypes.byref(p)))
+    return p
+
+
+def plan_rows(D, k, eps=1e-6, recall=1.0, **kw):
+    """profk_plan_rows: the per-row plan for rows of D values."""
+    p = Plan()
+    _check(lib().profk_plan_rows(D, k, eps, recall, ctypes.byref(opts(False, **kw)), ctypes.byref(p)))
+    return p
+
+
+def workspace_size(p, dtype, batch=1):
+    return int(lib().profk_workspace_size(ctypes.byref(p), dtype, batch))
+
+
+# ----------------------------------------------------------- torch side ---
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise ProfkError(f"unsupported dtype {t.dtype}")
+
+
+def _stream():
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def workspace(p, dtype, batch=1, device="cuda"):
+    torch = _torch()
+    return torch.empty(max(workspace_size(p, dtype, batch), 1), dtype=torch.uint8, device=device)
+
+
+def read_info(info_tensor):
+    """Host copy of profk_info_t records (synchronises the tensor's stream)."""
+    raw = info_tensor.cpu().numpy().tobytes()
+    return np.frombuffer(raw, dtype=INFO_DTYPE)
+
+
+def topk(x, k, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None, info=None):
+    """Top-k of a 1-D fp32/bf16 CUDA tensor: (values, int64 indices, info)."""
+    torch = _torch()
+    if x.dim() != 1 or not x.is_cuda:
+        raise ProfkError("x must be a 1-D CUDA tensor")
+    dt = _dtype_code(x)
+    N = x.numel()
+    p = p if p is not None else plan(N, k, eps, recall)
+    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
+    if out is None:
+        out = (torch.empty(k, dtype=x.dtype, device=x.device),
+               torch.empty(k, dtype=torch.int64, device=x.device))
+    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    _check(lib().profk_topk(ctypes.byref(p), dt, _ptr(x), N, k, seed, _ptr(out[0]), _ptr(out[1]),
+                            _ptr(ws), ws.numel(), _stream(), _ptr(info)))
+    return out[0], out[1], info
+
+
+def topk_tau(x, k, tau_key, p, ws=None, eps=1e-6):
+    """profk_topk_tau: the pipeline with the threshold given (forces the
+    fallback paths on purpose)."""
+    torch = _torch()
+    dt = _dtype_code(x)
+    N = x.numel()
+    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
+    vals = torch.empty(k, dtype=x.dtype, device=x.device)
+    idx = torch.empty(k, dtype=torch.int64, device=x.device)
+    info = torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    _check(lib().profk_topk_tau(ctypes.byref(p), dt, _ptr(x), N, k, tau_key, _ptr(vals), _ptr(idx),
+                                _ptr(ws), ws.numel(), _stream(), _ptr(info)))
+    return vals, idx, info
+
+
+def topk_simple(x, k, seed=0):
+    torch = _torch()
+    vals = torch.empty(k, dtype=torch.float32, device=x.device)
+    idx = torch.empty(k, dtype=torch.int64, device=x.device)
+    _check(lib().profk_topk_simple(_ptr(x), x.numel(), k, seed, _ptr(vals), _ptr(idx)))
+    return vals, idx
+
+
+def topk_rows(x, k, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None, info=None):
+    """Per-row top-k of a [B, D] CUDA tensor (rows may be strided)."""
+    torch = _torch()
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise ProfkError("x must be [B, D] with unit column stride")
+    dt = _dtype_code(x)
+    B, D = x.shape
+    p = p if p is not None else plan_rows(D, k, eps, recall)
+    ws = ws if ws is not None else workspace(p, dt, B, x.device)
+    if out is None:
+        out = (torch.empty((B, k), dtype=x.dtype, device=x.device),
+               torch.empty((B, k), dtype=torch.int64, device=x.device))
+    info = info if info is not None else torch.empty(B * INFO_BYTES, dtype=torch.uint8, device=x.device)
+    _check(lib().profk_topk_rows(ctypes.byref(p), dt, _ptr(x), B, D, x.stride(0), k, seed,
+                                 _ptr(out[0]), _ptr(out[1]), _ptr(ws), ws.numel(), _stream(),
+                                 _ptr(info)))
+    return out[0], out[1], info
+
+
+def batchtopk(x, k_row, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None, info=None):
+    """BatchTopK: the B*k_row largest entries of a contiguous [B, D] tensor,
+    with flat indices row*D + col."""
+    torch = _torch()
+    if x.dim() != 2 or not x.is_contiguous():
+        raise ProfkError("x must be a contiguous [B, D] tensor")
+    dt = _dtype_code(x)
+    B, D = x.shape
+    K = B * k_row
+    p = p if p is not None else plan(B * D, K, eps, recall)
+    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
+    if out is None:
+        out = (torch.empty(K, dtype=x.dtype, device=x.device),
+               torch.empty(K, dtype=torch.int64, device=x.device))
+    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    _check(lib().profk_batchtopk(ctypes.byref(p), dt, _ptr(x), B, D, k_row, seed, _ptr(out[0]),
+                                 _ptr(out[1]), _ptr(ws), ws.numel(), _stream(), _ptr(info)))
+    return out[0], out[1], info
+
+
+def debug_sample_indices(seed, row, S, N, device="cuda"):
+    torch = _torch()
+    out = torch.empty(S, dtype=torch.int64, device=device)
+    _check(lib().profk_debug_sample_indices(seed, row, S, N, _ptr(out), _stream()))
+    return out
+
+
+def debug_filter(x, tau_key, p, ws=None):
+    """Stage 3 alone: (buffer keys, buffer indices, count) for a given tau."""
+    torch = _torch()
+    dt = _dtype_code(x)
+    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
+    bk = torch.empty(p.M, dtype=torch.int32, device=x.device)
+    bi = torch.empty(p.M, dtype=torch.int32, device=x.device)
+    cnt = torch.empty(1, dtype=torch.int32, device=x.device)
+    _check(lib().profk_debug_filter(ctypes.byref(p), dt, _ptr(x), x.numel(), tau_key, _ptr(bk), _ptr(bi),
+                                    _ptr(cnt), _ptr(ws), ws.numel(), _stream()))
+    return bk, bi, cnt

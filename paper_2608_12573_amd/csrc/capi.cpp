@@ -1,0 +1,202 @@
+// extern "C" entry points of libprofk.so: argument checks, workspace
+// carving and launches.  Declarations and contracts are in include/profk.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <mutex>
+
+#include "launch.h"
+#include "plan_internal.h"
+#include "profk.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+int hip_fail(hipError_t e) {
+  g_last_hip_error = static_cast<int>(e);
+  return PROFK_EHIP;
+}
+
+bool plan_consistent(const profk_plan_t* p) {
+  return p->N >= 1 && p->N <= static_cast<int64_t>(UINT32_MAX) && p->k >= 1 && p->k <= p->N &&
+         p->k_req >= 1 && p->k_req <= p->k && p->S >= 1 && p->t >= 1 && p->t <= p->S &&
+         p->S <= static_cast<int64_t>(UINT32_MAX) && p->M >= p->k && p->M <= p->N &&
+         (p->mode == PROFK_MODE_FILTER || p->mode == PROFK_MODE_DIRECT);
+}
+
+bool dtype_ok(int32_t dt) { return dt == PROFK_F32 || dt == PROFK_BF16; }
+
+size_t elem_size(int32_t dt) { return dt == PROFK_F32 ? 4 : 2; }
+
+// Shared checks of the flat entry points.  Returns PROFK_OK and fills the
+// layout when the call may proceed.
+int check_flat(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t N, int64_t k,
+               const void* out_vals, const int64_t* out_idx, const void* ws, size_t ws_bytes,
+               profk::FlatLayout* L) {
+  if (!plan || !values || !out_vals || !out_idx || !ws) return PROFK_ENULL;
+  if (!dtype_ok(dtype)) return PROFK_EDTYPE;
+  if (!plan_consistent(plan) || plan->N != N || plan->k != k) return PROFK_EINVAL;
+  if (k > profk::kFinMaxK) return PROFK_EINVAL;
+  if (reinterpret_cast<uintptr_t>(values) % elem_size(dtype) != 0) return PROFK_EINVAL;
+  *L = profk::flat_layout(*plan, dtype, profk::device_cu_count());
+  if (ws_bytes < L->bytes) return PROFK_EWORKSPACE;
+  return PROFK_OK;
+}
+
+int run_flat(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t N, int64_t k,
+             uint64_t seed, uint64_t row, void* out_vals, int64_t* out_idx, void* ws, size_t ws_bytes,
+             void* stream, profk_info_t* info, int use_tau, uint32_t tau_key) {
+  profk::FlatLayout L;
+  const int rc = check_flat(plan, dtype, values, N, k, out_vals, out_idx, ws, ws_bytes, &L);
+  if (rc != PROFK_OK) return rc;
+  profk::FlatCall c{plan, dtype, values, static_cast<uint32_t>(N), static_cast<uint32_t>(k), seed, row,
+                    out_vals, out_idx, static_cast<uint8_t*>(ws), L, static_cast<hipStream_t>(stream),
+                    info, use_tau, tau_key};
+  const hipError_t e = profk::launch_flat(c);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+void profk_default_opts(profk_plan_opts_t* o) {
+  if (!o) return;
+  o->S_min = 32768;
+  o->S_max = 131072;
+  o->cost_ratio = 1.0;
+  o->eps_split = 0.5;
+  o->paper_literal = 0;
+  o->force_mode = PROFK_FORCE_AUTO;
+}
+
+void profk_default_row_opts(profk_plan_opts_t* o) {
+  profk_default_opts(o);
+  if (o) o->S_min = 256;
+}
+
+int profk_plan(int64_t N, int64_t k, double eps, double recall, const profk_plan_opts_t* opts,
+               profk_plan_t* out) {
+  profk_plan_opts_t o;
+  if (opts) o = *opts; else profk_default_opts(&o);
+  return profk::make_plan(N, k, eps, recall, o, out);
+}
+
+int profk_plan_rows(int64_t D, int64_t k, double eps, double recall, const profk_plan_opts_t* opts,
+                    profk_plan_t* out) {
+  profk_plan_opts_t o;
+  if (opts) o = *opts; else profk_default_row_opts(&o);
+  return profk::make_plan(D, k, eps, recall, o, out);
+}
+
+size_t profk_workspace_size(const profk_plan_t* plan, int32_t dtype, int64_t batch) {
+  if (!plan || !dtype_ok(dtype) || !plan_consistent(plan) || batch != 1) return 0;
+  return profk::flat_layout(*plan, dtype, profk::device_cu_count()).bytes;
+}
+
+int profk_topk(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t N, int64_t k,
+               uint64_t seed, void* out_vals, int64_t* out_idx, void* ws, size_t ws_bytes,
+               void* stream, profk_info_t* info_dev) {
+  return run_flat(plan, dtype, values, N, k, seed, 0, out_vals, out_idx, ws, ws_bytes, stream,
+                  info_dev, 0, 0);
+}
+
+int profk_topk_tau(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t N, int64_t k,
+                   uint32_t tau_key, void* out_vals, int64_t* out_idx, void* ws, size_t ws_bytes,
+                   void* stream, profk_info_t* info_dev) {
+  return run_flat(plan, dtype, values, N, k, 0, 0, out_vals, out_idx, ws, ws_bytes, stream, info_dev,
+                  1, tau_key);
+}
+
+int profk_batchtopk(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t B, int64_t D,
+                    int64_t k_row, uint64_t seed, void* out_vals, int64_t* out_flat_idx, void* ws,
+                    size_t ws_bytes, void* stream, profk_info_t* info_dev) {
+  if (B < 1 || D < 1 || k_row < 1 || k_row > D) return PROFK_EINVAL;
+  if (B > static_cast<int64_t>(UINT32_MAX) / D) return PROFK_EINVAL;
+  return run_flat(plan, dtype, values, B * D, B * k_row, seed, 0, out_vals, out_flat_idx, ws, ws_bytes,
+                  stream, info_dev, 0, 0);
+}
+
+int profk_topk_rows(const profk_plan_t*, int32_t, const void*, int64_t, int64_t, int64_t, int64_t,
+                    uint64_t, void*, int64_t*, void*, size_t, void*, profk_info_t*) {
+  return PROFK_EINVAL;
+}
+
+int profk_debug_sample_indices(uint64_t seed, int64_t row, int64_t S, int64_t N, int64_t* out_dev,
+                               void* stream) {
+  if (!out_dev) return PROFK_ENULL;
+  if (S < 1 || S > static_cast<int64_t>(UINT32_MAX) || N < 1 || row < 0) return PROFK_EINVAL;
+  const hipError_t e = profk::launch_sample_indices(seed, static_cast<uint64_t>(row),
+                                                    static_cast<uint32_t>(S), static_cast<uint64_t>(N),
+                                                    out_dev, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
+int profk_debug_filter(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t N,
+                       uint32_t tau_key, uint32_t* buf_key, uint32_t* buf_idx, uint32_t* count_dev,
+                       void* ws, size_t ws_bytes, void* stream) {
+  if (!plan || !values || !buf_key || !buf_idx || !count_dev || !ws) return PROFK_ENULL;
+  if (!dtype_ok(dtype)) return PROFK_EDTYPE;
+  if (!plan_consistent(plan) || plan->N != N) return PROFK_EINVAL;
+  if (reinterpret_cast<uintptr_t>(values) % elem_size(dtype) != 0) return PROFK_EINVAL;
+  const profk::FlatLayout L = profk::flat_layout(*plan, dtype, profk::device_cu_count());
+  if (ws_bytes < L.bytes) return PROFK_EWORKSPACE;
+  profk::FlatCall c{plan, dtype, values, static_cast<uint32_t>(N), static_cast<uint32_t>(plan->k), 0, 0,
+                    nullptr, nullptr, static_cast<uint8_t*>(ws), L, static_cast<hipStream_t>(stream),
+                    nullptr, 1, tau_key};
+  const hipError_t e = profk::launch_debug_filter(c, buf_key, buf_idx, count_dev);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
+namespace {
+std::mutex g_simple_mu;
+void* g_simple_ws = nullptr;
+size_t g_simple_bytes = 0;
+}  // namespace
+
+int profk_topk_simple(const float* values, int64_t N, int64_t k, uint64_t seed, float* out_vals,
+                      int64_t* out_idx) {
+  profk_plan_t plan;
+  int rc = profk_plan(N, k, 1e-6, 1.0, nullptr, &plan);
+  if (rc != PROFK_OK) return rc;
+  std::lock_guard<std::mutex> lock(g_simple_mu);
+  const size_t need = profk_workspace_size(&plan, PROFK_F32, 1);
+  if (need == 0) return PROFK_EINVAL;
+  if (need > g_simple_bytes) {
+    if (g_simple_ws) (void)hipFree(g_simple_ws);
+    g_simple_ws = nullptr;
+    g_simple_bytes = 0;
+    hipError_t e = hipMalloc(&g_simple_ws, need);
+    if (e != hipSuccess) return hip_fail(e);
+    g_simple_bytes = need;
+  }
+  rc = profk_topk(&plan, PROFK_F32, values, N, k, seed, out_vals, out_idx, g_simple_ws, g_simple_bytes,
+                  nullptr, nullptr);
+  if (rc != PROFK_OK) return rc;
+  const hipError_t e = hipStreamSynchronize(nullptr);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
+void profk_release(void) {
+  std::lock_guard<std::mutex> lock(g_simple_mu);
+  if (g_simple_ws) (void)hipFree(g_simple_ws);
+  g_simple_ws = nullptr;
+  g_simple_bytes = 0;
+}
+
+const char* profk_status_string(int code) {
+  switch (code) {
+    case PROFK_OK: return "ok";
+    case PROFK_EINVAL: return "invalid argument";
+    case PROFK_EDTYPE: return "unsupported dtype";
+    case PROFK_EWORKSPACE: return "workspace too small";
+    case PROFK_ENULL: return "null pointer";
+    case PROFK_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int profk_last_hip_error(void) { return g_last_hip_error; }
+
+}  // extern "C"

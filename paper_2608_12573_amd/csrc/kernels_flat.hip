@@ -1,0 +1,687 @@
+// Prof-K on one vector: sampling (stage 1), threshold (stage 2), the
+// filter-and-compact pass (stage 3) and refinement with fallback (stage 4),
+// Sec. 3 "The Prof-K Algorithm".
+//
+// Kernel sequence of one call, all on the caller's stream:
+//   k_sample      ceil(S/4096) blocks: Philox draws, gathers, and each block's
+//                 local top-t sample keys (the t-th largest of the whole
+//                 sample is among the union of the blocks' top-t).
+//   k_select_tau  one block: tau = t-th largest key of that union.
+//   k_filter      persistent grid, one contiguous chunk per block, 16-byte
+//                 nontemporal loads; survivors go to the block's private
+//                 region of the candidate buffer through LDS-allocated
+//                 slots, so the pass issues no same-address global atomics
+//                 (those serialise across the chip).
+//   k_finish      reads the per-block counts; when k_req <= count <= M one
+//                 block refines the buffer exactly in LDS, otherwise every
+//                 block computes the exact top-k of its chunk of the input
+//                 and the last block to finish merges them.
+#include <climits>
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace profk {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+template <int DT> struct Elem;
+template <> struct Elem<0> { static constexpr int EPV = 4, ES = 4, KEYBITS = 32; };
+template <> struct Elem<1> { static constexpr int EPV = 8, ES = 2, KEYBITS = 16; };
+
+// ------------------------------------------------------------ stage 1 -----
+struct SampleArgs {
+  const void* values;
+  uint64_t n, seed, row;
+  uint32_t S, t, tcap;
+  uint32_t* union_keys;
+  CallState* st;
+};
+
+template <int DT>
+__global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
+  __shared__ uint32_t keys[kSampPerBlock];
+  __shared__ SelectShared sel;
+  __shared__ uint32_t emitted;
+  const uint32_t b = blockIdx.x, tid = threadIdx.x;
+  if (b == 0 && tid == 0) {
+    a.st->spill_cnt = 0;
+    a.st->ticket = 0;
+    a.st->status = 0;
+  }
+  const uint32_t j0 = b * kSampPerBlock;
+  const uint32_t nb = min(static_cast<uint32_t>(kSampPerBlock), a.S - j0);
+  {
+    // draw j = j0 + 4*tid + q is word q of Philox block (j0/4 + tid)
+    const U64x4 w = philox4x64_10(static_cast<uint64_t>(j0 / 4) + tid, a.row, 0, 0, a.seed, 0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t j = 4 * tid + q;
+      if (j < nb) keys[j] = key_of<DT>(load_raw<DT>(a.values, index_of_word(w.w[q], a.n)));
+    }
+  }
+  __syncthreads();
+  uint32_t* dst = a.union_keys + static_cast<size_t>(b) * a.tcap;
+  const uint32_t tl = min(a.t, nb);
+  if (tl == nb) {
+    for (uint32_t j = tid; j < nb; j += kSampBS) dst[j] = keys[j];
+    return;
+  }
+  auto visit = [&](auto f) {
+    for (uint32_t j = tid; j < nb; j += kSampBS) f(keys[j]);
+  };
+  const SelectResult r = block_select_kth<kSampBS>(visit, tl, Elem<DT>::KEYBITS, 0u, sel);
+  if (tid == 0) emitted = 0;
+  __syncthreads();
+  for (uint32_t j = tid; j < nb; j += kSampBS)
+    if (keys[j] > r.kth) dst[atomicAdd(&emitted, 1u)] = keys[j];
+  for (uint32_t j = r.above + tid; j < tl; j += kSampBS) dst[j] = r.kth;
+}
+
+// ------------------------------------------------------------ stage 2 -----
+constexpr uint32_t kTauCache = 16384;
+
+struct TauArgs {
+  const uint32_t* keys;
+  uint32_t n, t;
+  int keybits;
+  CallState* st;
+};
+
+__global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
+  __shared__ uint32_t cache[kTauCache];
+  __shared__ SelectShared sel;
+  const uint32_t tid = threadIdx.x;
+  auto gload = [&](uint32_t i) { return a.keys[i]; };
+  SelectResult r;
+  if (a.n <= kTauCache) {
+    for_items<kTauBS, 8>(a.n, gload, [&](uint32_t i, uint32_t v) { cache[i] = v; });
+    __syncthreads();
+    r = block_select_kth<kTauBS>(
+        [&](auto f) {
+          for (uint32_t i = tid; i < a.n; i += kTauBS) f(cache[i]);
+        },
+        a.t, a.keybits, 0u, sel);
+  } else {
+    r = block_select_kth<kTauBS>(
+        [&](auto f) { for_items<kTauBS, 8>(a.n, gload, [&](uint32_t, uint32_t v) { f(v); }); },
+        a.t, a.keybits, 0u, sel);
+  }
+  if (tid == 0) a.st->tau_key = r.kth;
+}
+
+__global__ void k_init_state(CallState* st, uint32_t tau_key) {
+  if (threadIdx.x == 0) {
+    st->tau_key = tau_key;
+    st->spill_cnt = 0;
+    st->ticket = 0;
+    st->status = 0;
+  }
+}
+
+// ------------------------------------------------------------ stage 3 -----
+struct FilterArgs {
+  const void* values;
+  uint32_t n, head, nvec, vpb;
+  uint32_t C, spill_cap;
+  CallState* st;
+  uint32_t *reg_key, *reg_idx, *blk_cnt, *blk_max, *spill_key, *spill_idx;
+};
+
+// Survival test on a transformed word: for a threshold whose pattern is
+// non-negative, key(x) >= key(tau) iff bits(x) >= bits(tau) as signed
+// integers; for a negative one, iff bits(x) <= bits(tau) as unsigned, which
+// is the signed test on bits ^ 0x7FFFFFFF.  So every element costs one XOR
+// and one signed compare (bf16: the same per 16-bit half).
+template <int DT>
+__global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
+  constexpr int EPV = Elem<DT>::EPV;
+  constexpr int ES = Elem<DT>::ES;
+  __shared__ uint32_t s_cnt;
+  __shared__ uint32_t s_wmax[kFiltBS / kWave];
+  const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), b = blockIdx.x;
+  if (tid == 0) s_cnt = 0;
+  const uint32_t tau = a.st->tau_key;
+  uint32_t flip;
+  int thr;
+  if (DT == 0) {
+    const uint32_t tb = bits_from_key_f32(tau);
+    flip = (tb >> 31) ? 0x7FFFFFFFu : 0u;
+    thr = static_cast<int>(tb ^ flip);
+  } else {
+    const uint32_t tb = bits_from_key_bf16(tau);
+    const uint32_t f16 = (tb & 0x8000u) ? 0x7FFFu : 0u;
+    flip = f16 | (f16 << 16);
+    thr = static_cast<int>(static_cast<int16_t>(static_cast<uint16_t>(tb ^ f16)));
+  }
+  // a vector that can never pass the fast test unless every element survives
+  const uint32_t neutral = DT == 0 ? (0x80000000u ^ flip) : ((0x8000u * 0x10001u) ^ flip);
+  __syncthreads();
+
+  uint32_t my_max = 0;
+  // Reserve `total` consecutive slots of this block's region for one wave;
+  // slots past the region capacity go to the shared spill list.
+  auto reserve = [&](uint32_t cnt, uint32_t& slot, uint32_t& first_spill, uint32_t& sbase) {
+    const uint32_t incl = wave_incl_sum(cnt);
+    const uint32_t total = __shfl(incl, kWave - 1, kWave);
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(&s_cnt, total);
+    base = __shfl(base, 0, kWave);
+    const uint32_t n_in = base < a.C ? min(total, a.C - base) : 0u;
+    const uint32_t n_spill = total - n_in;
+    sbase = 0;
+    if (n_spill) {
+      if (lane == 0) sbase = atomicAdd(&a.st->spill_cnt, n_spill);
+      sbase = __shfl(sbase, 0, kWave);
+    }
+    first_spill = base + n_in;
+    slot = base + incl - cnt;
+  };
+  auto store = [&](uint32_t slot, uint32_t first_spill, uint32_t sbase, uint32_t key, uint32_t idx) {
+    my_max = max(my_max, key);
+    if (slot < a.C) {
+      const size_t g = static_cast<size_t>(b) * a.C + slot;
+      a.reg_key[g] = key;
+      a.reg_idx[g] = idx;
+    } else {
+      const uint32_t sp = sbase + (slot - first_spill);
+      if (sp < a.spill_cap) {
+        a.spill_key[sp] = key;
+        a.spill_idx[sp] = idx;
+      }
+    }
+  };
+
+  const u32x4* vec = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.values) +
+                                                    static_cast<size_t>(a.head) * ES);
+  const uint32_t vbeg = b * a.vpb;
+  const uint32_t vend = min(vbeg + a.vpb, a.nvec);
+  for (uint32_t vb = vbeg; vb < vend; vb += kFiltBS * kFiltU) {
+    u32x4 v[kFiltU];
+#pragma unroll
+    for (int u = 0; u < kFiltU; ++u) {
+      const uint32_t vi = vb + u * kFiltBS + tid;
+      if (vi < vend) v[u] = __builtin_nontemporal_load(vec + vi);
+      else v[u] = u32x4{neutral, neutral, neutral, neutral};
+    }
+    int mx;
+    if (DT == 0) {
+      mx = INT_MIN;
+#pragma unroll
+      for (int u = 0; u < kFiltU; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = max(mx, static_cast<int>(v[u][e] ^ flip));
+    } else {
+      s16x2 m2 = s16x2{SHRT_MIN, SHRT_MIN};
+#pragma unroll
+      for (int u = 0; u < kFiltU; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(s16x2, v[u][e] ^ flip));
+      mx = max(static_cast<int>(m2.x), static_cast<int>(m2.y));
+    }
+    if (__ballot(mx >= thr) == 0) continue;
+
+    // Rare path: exact per-element test, one slot reservation per wave.
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int u = 0; u < kFiltU; ++u) {
+      const bool valid = vb + u * kFiltBS + tid < vend;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t w = v[u][e] ^ flip;
+        if (DT == 0) {
+          cnt += (valid && static_cast<int>(w) >= thr) ? 1u : 0u;
+        } else {
+          cnt += (valid && (static_cast<int>(w << 16) >> 16) >= thr) ? 1u : 0u;
+          cnt += (valid && (static_cast<int>(w) >> 16) >= thr) ? 1u : 0u;
+        }
+      }
+    }
+    uint32_t slot, first_spill, sbase;
+    reserve(cnt, slot, first_spill, sbase);
+#pragma unroll
+    for (int u = 0; u < kFiltU; ++u) {
+      const uint32_t vi = vb + u * kFiltBS + tid;
+      const bool valid = vi < vend;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t raw = v[u][e];
+        const uint32_t w = raw ^ flip;
+        if (DT == 0) {
+          if (valid && static_cast<int>(w) >= thr) {
+            store(slot, first_spill, sbase, key_f32(raw), a.head + vi * EPV + e);
+            ++slot;
+          }
+        } else {
+          if (valid && (static_cast<int>(w << 16) >> 16) >= thr) {
+            store(slot, first_spill, sbase, key_bf16(raw & 0xFFFFu), a.head + vi * EPV + 2 * e);
+            ++slot;
+          }
+          if (valid && (static_cast<int>(w) >> 16) >= thr) {
+            store(slot, first_spill, sbase, key_bf16(raw >> 16), a.head + vi * EPV + 2 * e + 1);
+            ++slot;
+          }
+        }
+      }
+    }
+  }
+
+  // Elements before the first aligned vector and after the last one.
+  if (b == gridDim.x - 1 && tid < kWave) {
+    const uint32_t tail0 = a.head + a.nvec * EPV;
+    const uint32_t ns = a.head + (a.n - tail0);
+    uint32_t idx = 0, key = 0;
+    bool ok = false;
+    if (lane < ns) {
+      idx = lane < a.head ? lane : tail0 + (lane - a.head);
+      key = key_of<DT>(load_raw<DT>(a.values, idx));
+      ok = key >= tau;
+    }
+    if (__ballot(ok)) {
+      uint32_t slot, first_spill, sbase;
+      reserve(ok ? 1u : 0u, slot, first_spill, sbase);
+      if (ok) store(slot, first_spill, sbase, key, idx);
+    }
+  }
+
+  const uint32_t wm = wave_max_u32(my_max);
+  if (lane == 0) s_wmax[tid / kWave] = wm;
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < kFiltBS / kWave; ++i) m = max(m, s_wmax[i]);
+    a.blk_cnt[b] = s_cnt;
+    a.blk_max[b] = m;
+  }
+}
+
+// ------------------------------------------------------------ stage 4 -----
+constexpr uint32_t kFinCache = 28672;
+
+struct FinShared {
+  uint32_t cache[kFinCache];
+  uint64_t sortbuf[kFinMaxK];
+  uint32_t pre[1024];
+  SelectShared sel;
+  uint32_t misc[8];
+};
+
+// Last index b with pre[b] <= i (pre non-decreasing, pre[0] = 0).
+__device__ __forceinline__ uint32_t region_of(const uint32_t* pre, uint32_t G, uint32_t i) {
+  uint32_t lo = 0, hi = G;
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (pre[mid] <= i) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// Candidates stored in G regions of capacity C (the first `stored` entries
+// of each, exclusive prefix in `pre`) followed by a plain list.
+struct RegionSrc {
+  const uint32_t *key, *idx;
+  uint32_t C, G, R;
+  const uint32_t* pre;
+  const uint32_t *skey, *sidx;
+  __device__ size_t where(uint32_t i, bool& in_list) const {
+    if (i >= R) { in_list = true; return i - R; }
+    in_list = false;
+    const uint32_t r = region_of(pre, G, i);
+    return static_cast<size_t>(r) * C + (i - pre[r]);
+  }
+  __device__ uint32_t get_key(uint32_t i) const {
+    bool l;
+    const size_t p = where(i, l);
+    return l ? skey[p] : key[p];
+  }
+  __device__ uint32_t get_idx(uint32_t i) const {
+    bool l;
+    const size_t p = where(i, l);
+    return l ? sidx[p] : idx[p];
+  }
+};
+
+// A contiguous range of the input, keys computed on the fly.
+template <int DT>
+struct InputSrc {
+  const void* values;
+  uint32_t lo;
+  __device__ uint32_t get_key(uint32_t i) const { return key_of<DT>(load_raw<DT>(values, lo + i)); }
+  __device__ uint32_t get_idx(uint32_t i) const { return lo + i; }
+};
+
+// Exact top-kk (kk <= kFinMaxK, kk <= n) of a candidate set under the total
+// order, collected into sh.sortbuf (unsorted) and returned count kk.  Keys of
+// all candidates lie in [lo_key, hi_key].
+template <class Src>
+__device__ void select_topk(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
+                            uint32_t hi_key, int keybits, FinShared& sh) {
+  const uint32_t tid = threadIdx.x;
+  const bool cached = n <= kFinCache;
+  auto gkey = [&](uint32_t i) { return src.get_key(i); };
+  if (cached) {
+    for_items<kFinBS, 8>(n, gkey, [&](uint32_t i, uint32_t v) { sh.cache[i] = v; });
+    __syncthreads();
+  }
+  auto visit_i = [&](auto f) {
+    if (cached) {
+      for (uint32_t i = tid; i < n; i += kFinBS) f(i, sh.cache[i]);
+    } else {
+      for_items<kFinBS, 8>(n, gkey, f);
+    }
+  };
+  const int shared = shared_prefix_bits(lo_key, hi_key, keybits);
+  const SelectResult r = block_select_kth<kFinBS>(
+      [&](auto f) { visit_i([&](uint32_t, uint32_t key) { f(key); }); }, kk, keybits - shared,
+      lo_key, sh.sel);
+  const uint32_t kstar = r.kth;
+  const uint32_t krem = kk - r.above;
+  const bool cut = krem < r.equal;
+  uint32_t istar = 0xFFFFFFFFu;
+  if (cut) {
+    // the krem smallest indices among the ties at kstar
+    const SelectResult ri = block_select_kth<kFinBS>(
+        [&](auto f) {
+          visit_i([&](uint32_t i, uint32_t key) {
+            if (key == kstar) f(~src.get_idx(i));
+          });
+        },
+        krem, 32, 0u, sh.sel);
+    istar = ~ri.kth;
+  }
+  if (tid == 0) sh.misc[0] = 0;
+  __syncthreads();
+  visit_i([&](uint32_t i, uint32_t key) {
+    if (key >= kstar) {
+      const uint32_t id = src.get_idx(i);
+      if (key > kstar || !cut || id <= istar) {
+        const uint32_t p = atomicAdd(&sh.misc[0], 1u);
+        if (p < kFinMaxK) sh.sortbuf[p] = composite(key, id);
+      }
+    }
+  });
+  __syncthreads();
+}
+
+template <int DT>
+__device__ void write_sorted(FinShared& sh, uint32_t kk, uint32_t k, void* out_vals,
+                             int64_t* out_idx) {
+  const uint32_t tid = threadIdx.x;
+  const uint32_t P = next_pow2(kk);
+  for (uint32_t i = kk + tid; i < P; i += kFinBS) sh.sortbuf[i] = 0;
+  __syncthreads();
+  bitonic_sort_desc<kFinBS>(sh.sortbuf, P);
+  for (uint32_t i = tid; i < k; i += kFinBS) {
+    uint32_t bits;
+    int64_t id;
+    if (i < kk) {
+      const uint64_t c = sh.sortbuf[i];
+      bits = bits_of_key<DT>(comp_key(c));
+      id = comp_idx(c);
+    } else {
+      bits = DT == 0 ? 0xFF800000u : 0xFF80u;  // -inf padding (relaxed recall)
+      id = -1;
+    }
+    if (DT == 0) static_cast<uint32_t*>(out_vals)[i] = bits;
+    else static_cast<uint16_t*>(out_vals)[i] = static_cast<uint16_t>(bits);
+    out_idx[i] = id;
+  }
+}
+
+struct FinishArgs {
+  const void* values;
+  uint32_t n, k, k_req, M;
+  int direct;
+  uint32_t G_f, C;
+  const uint32_t *blk_cnt, *blk_max, *reg_key, *reg_idx, *spill_key, *spill_idx;
+  CallState* st;
+  uint32_t G_fb, chunk;
+  uint32_t *cand_key, *cand_idx, *cand_cnt;
+  void* out_vals;
+  int64_t* out_idx;
+  profk_info_t* info;
+};
+
+template <int DT>
+__global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
+  __shared__ FinShared sh;
+  constexpr int KB = Elem<DT>::KEYBITS;
+  const uint32_t key_max = KB == 32 ? 0xFFFFFFFFu : 0xFFFFu;
+  const uint32_t tid = threadIdx.x, b = blockIdx.x;
+  uint32_t total = 0, status = PROFK_STATUS_DIRECT;
+  if (!a.direct) {
+    const uint32_t cnt = tid < a.G_f ? a.blk_cnt[tid] : 0u;
+    const uint32_t stored = min(cnt, a.C);
+    uint32_t R;
+    const uint32_t pre = block_excl_sum<kFinBS>(stored, sh.sel.wsum, &R);
+    if (tid < a.G_f) sh.pre[tid] = pre;
+    total = block_sum<kFinBS>(cnt, sh.sel.wsum);
+    status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
+                             : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
+    if (status == PROFK_STATUS_FILTERED) {
+      if (b != 0) return;
+      const uint32_t gmax = block_max<kFinBS>(cnt ? a.blk_max[tid] : 0u, sh.sel.wsum);
+      const uint32_t tau = a.st->tau_key;
+      RegionSrc src{a.reg_key, a.reg_idx, a.C, a.G_f, R, sh.pre, a.spill_key, a.spill_idx};
+      const uint32_t kk = min(a.k, total);
+      select_topk(src, total, kk, tau, max(gmax, tau), KB, sh);
+      write_sorted<DT>(sh, kk, a.k, a.out_vals, a.out_idx);
+      if (tid == 0) {
+        a.st->status = status;
+        if (a.info) {
+          a.info->count = total;
+          a.info->tau_key = tau;
+          a.info->status = static_cast<int32_t>(status);
+          a.info->n_valid = kk;
+        }
+      }
+      return;
+    }
+  }
+  // Exact fallback: each block takes the exact top-k of its chunk ...
+  const uint32_t lo = static_cast<uint32_t>(min<uint64_t>(a.n, static_cast<uint64_t>(b) * a.chunk));
+  const uint32_t hi = static_cast<uint32_t>(min<uint64_t>(a.n, static_cast<uint64_t>(lo) + a.chunk));
+  const uint32_t nb = hi - lo;
+  const uint32_t kb = min(a.k, nb);
+  if (kb) {
+    InputSrc<DT> src{a.values, lo};
+    select_topk(src, nb, kb, 0u, key_max, KB, sh);
+    for (uint32_t i = tid; i < kb; i += kFinBS) {
+      const uint64_t c = sh.sortbuf[i];
+      a.cand_key[static_cast<size_t>(b) * a.k + i] = comp_key(c);
+      a.cand_idx[static_cast<size_t>(b) * a.k + i] = comp_idx(c);
+    }
+  }
+  if (tid == 0) a.cand_cnt[b] = kb;
+  // ... and the last block to finish merges the per-chunk results.
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) sh.misc[1] = (atomicAdd(&a.st->ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
+  __syncthreads();
+  if (!sh.misc[1]) return;
+  __threadfence();
+  const uint32_t cc = tid < gridDim.x ? a.cand_cnt[tid] : 0u;
+  uint32_t R;
+  const uint32_t pre = block_excl_sum<kFinBS>(cc, sh.sel.wsum, &R);
+  if (tid < gridDim.x) sh.pre[tid] = pre;
+  __syncthreads();
+  RegionSrc src{a.cand_key, a.cand_idx, a.k, gridDim.x, R, sh.pre, nullptr, nullptr};
+  select_topk(src, R, a.k, 0u, key_max, KB, sh);
+  write_sorted<DT>(sh, a.k, a.k, a.out_vals, a.out_idx);
+  if (tid == 0) {
+    a.st->status = status;
+    if (a.info) {
+      a.info->count = a.direct ? 0u : total;
+      a.info->tau_key = a.direct ? 0u : a.st->tau_key;
+      a.info->status = static_cast<int32_t>(status);
+      a.info->n_valid = a.k;
+    }
+  }
+}
+
+// ------------------------------------------------------ inspection ---------
+__global__ void k_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t n, int64_t* out) {
+  const uint32_t blk = blockIdx.x * blockDim.x + threadIdx.x;
+  if (static_cast<uint64_t>(blk) * 4 >= S) return;
+  const U64x4 w = philox4x64_10(blk, row, 0, 0, seed, 0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint64_t j = static_cast<uint64_t>(blk) * 4 + q;
+    if (j < S) out[j] = index_of_word(w.w[q], n);
+  }
+}
+
+// Gathers the regions and the spill list into one contiguous buffer.
+__global__ __launch_bounds__(1024) void k_gather_buffer(uint32_t G, uint32_t C, uint32_t cap,
+                                                        const uint32_t* blk_cnt,
+                                                        const uint32_t* reg_key, const uint32_t* reg_idx,
+                                                        const uint32_t* spill_key, const uint32_t* spill_idx,
+                                                        const CallState* st, uint32_t* out_key,
+                                                        uint32_t* out_idx, uint32_t* count) {
+  __shared__ uint32_t pre[1024];
+  __shared__ uint32_t wsum[20];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t cnt = tid < G ? blk_cnt[tid] : 0u;
+  uint32_t R;
+  const uint32_t p = block_excl_sum<1024>(min(cnt, C), wsum, &R);
+  if (tid < G) pre[tid] = p;
+  const uint32_t total = block_sum<1024>(cnt, wsum);
+  __syncthreads();
+  RegionSrc src{reg_key, reg_idx, C, G, R, pre, spill_key, spill_idx};
+  const uint32_t stored = min(total, cap);
+  for (uint32_t i = tid; i < stored; i += 1024) {
+    out_key[i] = src.get_key(i);
+    out_idx[i] = src.get_idx(i);
+  }
+  if (tid == 0) *count = total;
+  (void)st;
+}
+
+// ------------------------------------------------------------- host -------
+static inline uint32_t cdiv(uint64_t a, uint64_t b) { return static_cast<uint32_t>((a + b - 1) / b); }
+static inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
+  FlatLayout L;
+  const uint64_t N = static_cast<uint64_t>(p.N);
+  const uint32_t epv = dtype == PROFK_F32 ? 4 : 8;
+  const uint32_t S = static_cast<uint32_t>(p.S), t = static_cast<uint32_t>(p.t);
+  const uint32_t M = static_cast<uint32_t>(p.M), k = static_cast<uint32_t>(p.k);
+  L.G_s = cdiv(S, kSampPerBlock);
+  L.tcap = t < static_cast<uint32_t>(kSampPerBlock) ? t : kSampPerBlock;
+  const uint32_t last_nb = S - (L.G_s - 1) * kSampPerBlock;
+  L.union_n = (L.G_s - 1) * L.tcap + (t < last_nb ? t : last_nb);
+  const uint32_t maxg = static_cast<uint32_t>(num_cus * 4 < kFiltMaxBlocks ? num_cus * 4 : kFiltMaxBlocks);
+  uint32_t g = cdiv(cdiv(N, epv), kFiltBS * kFiltU);
+  L.G_f = g < 1 ? 1 : (g > maxg ? maxg : g);
+  const uint64_t c = 64 + (2ull * M + L.G_f - 1) / L.G_f;
+  L.C = static_cast<uint32_t>(c < M ? c : M);
+  if (L.C < 1) L.C = 1;
+  const uint32_t fbmax = static_cast<uint32_t>(num_cus < kFbMaxBlocks ? num_cus : kFbMaxBlocks);
+  uint32_t gb = cdiv(N, kFbMinChunk);
+  L.G_fb = gb < 1 ? 1 : (gb > fbmax ? fbmax : gb);
+  L.chunk = cdiv(N, L.G_fb);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
+  L.off_state = take(sizeof(CallState));
+  L.off_union = take(static_cast<size_t>(L.G_s) * L.tcap * 4);
+  L.off_blk_cnt = take(static_cast<size_t>(L.G_f) * 4);
+  L.off_blk_max = take(static_cast<size_t>(L.G_f) * 4);
+  L.off_reg_key = take(static_cast<size_t>(L.G_f) * L.C * 4);
+  L.off_reg_idx = take(static_cast<size_t>(L.G_f) * L.C * 4);
+  L.off_spill_key = take(static_cast<size_t>(M) * 4);
+  L.off_spill_idx = take(static_cast<size_t>(M) * 4);
+  L.off_cand_key = take(static_cast<size_t>(L.G_fb) * k * 4);
+  L.off_cand_idx = take(static_cast<size_t>(L.G_fb) * k * 4);
+  L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
+  L.bytes = off;
+  return L;
+}
+
+template <class T> static T* at(uint8_t* ws, size_t off) { return reinterpret_cast<T*>(ws + off); }
+
+template <int DT>
+static hipError_t launch_filter(const FlatCall& c, CallState* st) {
+  const FlatLayout& L = c.L;
+  constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV;
+  const uintptr_t addr = reinterpret_cast<uintptr_t>(c.values);
+  uint32_t head = static_cast<uint32_t>(((16 - (addr & 15)) & 15) / ES);
+  if (head > c.n) head = c.n;
+  const uint32_t nvec = (c.n - head) / EPV;
+  uint32_t vpb = cdiv(nvec, L.G_f);
+  vpb = cdiv(vpb, kFiltBS) * kFiltBS;
+  FilterArgs fa{c.values, c.n, head, nvec, vpb, L.C, static_cast<uint32_t>(c.plan->M), st,
+                at<uint32_t>(c.ws, L.off_reg_key), at<uint32_t>(c.ws, L.off_reg_idx),
+                at<uint32_t>(c.ws, L.off_blk_cnt), at<uint32_t>(c.ws, L.off_blk_max),
+                at<uint32_t>(c.ws, L.off_spill_key), at<uint32_t>(c.ws, L.off_spill_idx)};
+  hipLaunchKernelGGL(k_filter<DT>, dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  return hipGetLastError();
+}
+
+template <int DT>
+static hipError_t launch_flat_t(const FlatCall& c) {
+  const FlatLayout& L = c.L;
+  const profk_plan_t& p = *c.plan;
+  CallState* st = at<CallState>(c.ws, L.off_state);
+  const bool direct = p.mode == PROFK_MODE_DIRECT && !c.use_tau;
+  hipError_t e;
+  if (direct || c.use_tau) {
+    hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, st, c.use_tau ? c.tau_key : 0u);
+  } else {
+    SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
+                  L.tcap, at<uint32_t>(c.ws, L.off_union), st};
+    hipLaunchKernelGGL(k_sample<DT>, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
+    TauArgs ta{at<uint32_t>(c.ws, L.off_union), L.union_n, static_cast<uint32_t>(p.t), Elem<DT>::KEYBITS, st};
+    hipLaunchKernelGGL(k_select_tau, dim3(1), dim3(kTauBS), 0, c.stream, ta);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (!direct && (e = launch_filter<DT>(c, st)) != hipSuccess) return e;
+  FinishArgs fa{c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
+                direct ? 1 : 0, L.G_f, L.C,
+                at<uint32_t>(c.ws, L.off_blk_cnt), at<uint32_t>(c.ws, L.off_blk_max),
+                at<uint32_t>(c.ws, L.off_reg_key), at<uint32_t>(c.ws, L.off_reg_idx),
+                at<uint32_t>(c.ws, L.off_spill_key), at<uint32_t>(c.ws, L.off_spill_idx), st,
+                L.G_fb, L.chunk, at<uint32_t>(c.ws, L.off_cand_key), at<uint32_t>(c.ws, L.off_cand_idx),
+                at<uint32_t>(c.ws, L.off_cand_cnt), c.out_vals, c.out_idx, c.info};
+  hipLaunchKernelGGL(k_finish<DT>, dim3(L.G_fb), dim3(kFinBS), 0, c.stream, fa);
+  return hipGetLastError();
+}
+
+hipError_t launch_flat(const FlatCall& c) {
+  return c.dtype == PROFK_F32 ? launch_flat_t<0>(c) : launch_flat_t<1>(c);
+}
+
+hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t N, int64_t* out,
+                                 hipStream_t s) {
+  const uint32_t nblk = cdiv(S, 4);
+  hipLaunchKernelGGL(k_sample_indices, dim3(cdiv(nblk, 256)), dim3(256), 0, s, seed, row, S, N, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* buf_idx,
+                               uint32_t* count_dev) {
+  const FlatLayout& L = c.L;
+  CallState* st = at<CallState>(c.ws, L.off_state);
+  hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, st, c.tau_key);
+  hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st) : launch_filter<1>(c, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gather_buffer, dim3(1), dim3(1024), 0, c.stream, L.G_f, L.C,
+                     static_cast<uint32_t>(c.plan->M), at<uint32_t>(c.ws, L.off_blk_cnt),
+                     at<uint32_t>(c.ws, L.off_reg_key), at<uint32_t>(c.ws, L.off_reg_idx),
+                     at<uint32_t>(c.ws, L.off_spill_key), at<uint32_t>(c.ws, L.off_spill_idx), st,
+                     buf_key, buf_idx, count_dev);
+  return hipGetLastError();
+}
+
+int device_cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
+}  // namespace profk

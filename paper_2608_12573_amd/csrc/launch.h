@@ -1,0 +1,74 @@
+// Host view of the kernels: workspace layout and launch entry points.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "profk.h"
+
+namespace profk {
+
+// Per-call device state at the start of a workspace (256 bytes).
+struct CallState {
+  uint32_t tau_key;    // threshold key (stage 2)
+  uint32_t spill_cnt;  // survivors that did not fit their block's region
+  uint32_t ticket;     // last-block-done counter of the fallback
+  uint32_t status;     // PROFK_STATUS_* of the call
+  uint32_t pad[60];
+};
+
+// Launch geometry.
+constexpr int kSampBS = 1024;                 // threads of a sample block
+constexpr int kSampPerBlock = 4 * kSampBS;    // draws per sample block
+constexpr int kTauBS = 1024;
+constexpr int kFiltBS = 256;                  // threads of a filter block
+constexpr int kFiltU = 8;                     // 16-byte loads in flight per lane
+constexpr int kFiltMaxBlocks = 1024;
+constexpr int kFinBS = 1024;
+constexpr int kFinMaxK = 4096;                // largest k of the one-block refinement
+constexpr int kFbMaxBlocks = 256;
+constexpr uint32_t kFbMinChunk = 8192;
+
+// Workspace layout of one flat (vector) call.
+struct FlatLayout {
+  uint32_t G_s = 0, tcap = 0, union_n = 0;    // sampling
+  uint32_t G_f = 0, C = 0;                    // filter blocks, region capacity
+  uint32_t G_fb = 0, chunk = 0;               // fallback blocks, elements each
+  size_t off_state = 0, off_union = 0, off_blk_cnt = 0, off_blk_max = 0;
+  size_t off_reg_key = 0, off_reg_idx = 0, off_spill_key = 0, off_spill_idx = 0;
+  size_t off_cand_key = 0, off_cand_idx = 0, off_cand_cnt = 0;
+  size_t bytes = 0;
+};
+
+FlatLayout flat_layout(const profk_plan_t& plan, int dtype, int num_cus);
+
+struct FlatCall {
+  const profk_plan_t* plan;
+  int dtype;
+  const void* values;
+  uint32_t n, k;
+  uint64_t seed;
+  uint64_t row;
+  void* out_vals;
+  int64_t* out_idx;
+  uint8_t* ws;
+  FlatLayout L;
+  hipStream_t stream;
+  profk_info_t* info;
+  int use_tau;          // 1: threshold given by the caller
+  uint32_t tau_key;
+};
+
+hipError_t launch_flat(const FlatCall& c);
+
+// Inspection helpers.
+hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t N,
+                                 int64_t* out, hipStream_t s);
+hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* buf_idx,
+                               uint32_t* count_dev);
+
+int device_cu_count();
+
+}  // namespace profk

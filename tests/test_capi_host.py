@@ -1,0 +1,126 @@
+"""Host-side checks of libprofk.so (no GPU needed): every symbol the header
+declares is exported, the C++ planner equals the oracle planner, and bad
+arguments are rejected with the documented codes."""
+
+import itertools
+import math
+
+import pytest
+
+import paper_2608_12573_amd as pk
+from oracle import plan as oplan
+
+
+def test_library_exports_every_header_symbol():
+    L = pk.lib()
+    names = pk.header_functions()
+    assert len(names) >= 15
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def _oracle_opts(o):
+    return oplan.PlanOpts(S_min=o.S_min, S_max=o.S_max, cost_ratio=o.cost_ratio,
+                          eps_split=o.eps_split, paper_literal=bool(o.paper_literal),
+                          force_mode=o.force_mode)
+
+
+def _same(p, q):
+    assert (p.N, p.k, p.k_req, p.S, p.t, p.M, p.mode) == (q.N, q.k, q.k_req, q.S, q.t, q.M, q.mode)
+    assert p.p_underflow == pytest.approx(q.p_underflow, rel=1e-9, abs=1e-300)
+    assert p.p_overflow == pytest.approx(q.p_overflow, rel=1e-9, abs=1e-300)
+
+
+GRID_N = [1000, 4096, 65537, 2**20, 3 * 10**6, 2**24 + 3, 2**26, 2**28, 2**30, 2**32 - 1]
+GRID_K = [1, 2, 16, 64, 512, 1024, 4096, 65536, 262144]
+GRID_E = [1e-1, 1e-3, 1e-6, 1e-9]
+GRID_R = [1.0, 0.95, 0.5]
+
+
+@pytest.mark.parametrize("N", GRID_N)
+def test_planner_equals_oracle_grid(N):
+    for k, eps, rho in itertools.product(GRID_K, GRID_E, GRID_R):
+        if k > N:
+            continue
+        p = pk.plan(N, k, eps, rho)
+        q = oplan.plan(N, k, eps, rho)
+        _same(p, q)
+
+
+@pytest.mark.parametrize("D", [4096, 131072, 65536, 12288])
+def test_row_planner_equals_oracle(D):
+    for k in (1, 8, 32, 64, 256):
+        for eps in (1e-6, 1e-3):
+            p = pk.plan_rows(D, k, eps)
+            q = oplan.plan_rows(D, k, eps)
+            _same(p, q)
+
+
+def test_paper_literal_and_options_equal_oracle():
+    cases = [dict(paper_literal=1), dict(S_min=64, S_max=64, force_mode=pk.FORCE_FILTER),
+             dict(cost_ratio=0.1), dict(eps_split=0.3), dict(S_min=131072, S_max=131072)]
+    for kw, (N, k) in itertools.product(cases, [(2**20, 64), (2**28, 1024), (2**29, 64),
+                                                (10**6, 10), (2**28, 262144)]):
+        o = pk.opts(True, **kw)
+        p = pk.plan(N, k, 1e-6, 1.0, **kw)
+        q = oplan.plan(N, k, 1e-6, 1.0, _oracle_opts(o))
+        _same(p, q)
+
+
+def test_plan_rejects_bad_arguments():
+    bad = [(0, 1, 1e-6, 1.0), (10, 0, 1e-6, 1.0), (10, 11, 1e-6, 1.0), (10, 5, 0.0, 1.0),
+           (10, 5, 1.0, 1.0), (10, 5, 1e-3, 0.0), (10, 5, 1e-3, 1.5), (2**32, 5, 1e-3, 1.0)]
+    for N, k, e, r in bad:
+        with pytest.raises(pk.ProfkError, match="invalid argument"):
+            pk.plan(N, k, e, r)
+    with pytest.raises(pk.ProfkError):
+        pk.plan(100, 5, 1e-3, 1.0, S_min=0)
+
+
+def test_workspace_is_small_and_validates():
+    p = pk.plan(2**28, 1024)
+    ws = pk.workspace_size(p, pk.F32)
+    assert 0 < ws < 64 << 20          # O(S + M + k), far below the 1 GiB input
+    assert pk.workspace_size(p, 7) == 0
+    assert pk.workspace_size(p, pk.F32, 0) == 0
+
+
+def test_status_strings():
+    L = pk.lib()
+    for code in (pk.OK, pk.EINVAL, pk.EDTYPE, pk.EWORKSPACE, pk.ENULL, pk.EHIP, 12345):
+        assert L.profk_status_string(code)
+
+
+def test_null_and_dtype_errors_without_gpu():
+    L = pk.lib()
+    p = pk.plan(2**20, 64)
+    import ctypes
+    rc = L.profk_topk(ctypes.byref(p), pk.F32, None, 2**20, 64, 0, None, None, None, 0, None, None)
+    assert rc == pk.ENULL
+    rc = L.profk_topk(ctypes.byref(p), 9, ctypes.c_void_p(16), 2**20, 64, 0, ctypes.c_void_p(16),
+                      ctypes.c_void_p(16), ctypes.c_void_p(16), 1 << 30, None, None)
+    assert rc == pk.EDTYPE
+    rc = L.profk_topk(ctypes.byref(p), pk.F32, ctypes.c_void_p(16), 2**20, 65, 0, ctypes.c_void_p(16),
+                      ctypes.c_void_p(16), ctypes.c_void_p(16), 1 << 30, None, None)
+    assert rc == pk.EINVAL
+    rc = L.profk_topk(ctypes.byref(p), pk.F32, ctypes.c_void_p(16), 2**20, 64, 0, ctypes.c_void_p(16),
+                      ctypes.c_void_p(16), ctypes.c_void_p(16), 16, None, None)
+    assert rc == pk.EWORKSPACE
+    rc = L.profk_topk(ctypes.byref(p), pk.F32, ctypes.c_void_p(18), 2**20, 64, 0, ctypes.c_void_p(16),
+                      ctypes.c_void_p(16), ctypes.c_void_p(16), 1 << 30, None, None)
+    assert rc == pk.EINVAL
+
+
+def test_oracle_and_product_share_no_code():
+    import os
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    for d, needle in (("oracle", "paper_2608_12573_amd"), ("paper_2608_12573_amd", "oracle")):
+        for dirpath, _, files in os.walk(os.path.join(root, d)):
+            if "_build" in dirpath:
+                continue
+            for fn in files:
+                if fn.endswith((".py", ".hip", ".cpp", ".h")):
+                    with open(os.path.join(dirpath, fn)) as f:
+                        text = f.read()
+                    assert f"import {needle}" not in text and f"from {needle}" not in text, fn
+                    assert f"{needle}/" not in text, fn

@@ -1,0 +1,232 @@
+"""GPU parity of the flat (single-vector) path against the CPU oracle.
+
+Every comparison is bit-exact on values and indices (the method only
+compares and copies), and also checks the threshold key, the survivor count
+and the status the oracle's stage-by-stage run produces with the same seed.
+"""
+
+import numpy as np
+import pytest
+
+import paper_2608_12573_amd as pk
+import workloads
+from oracle import exact, keys as okeys, philox, plan as oplan, profk as oprofk
+from gpu_util import (compare, gpu_bf16, gpu_f32, host_bits, note, oracle_plan_of,
+                      plan_from_lib, torch)
+
+pytestmark = pytest.mark.gpu
+
+
+def _f32_case(x, k, seed, eps=1e-6, recall=1.0, offset=0, **kw):
+    p = pk.plan(x.size, k, eps, recall, **kw)
+    q = oracle_plan_of(p, **kw)
+    note(f"flat f32 N={x.size} k={k} seed={seed} off={offset} S={p.S} t={p.t} M={p.M} mode={p.mode}")
+    g = gpu_f32(x, offset)
+    vals, idx, info = pk.topk(g, k, seed=seed, p=p)
+    ref = oprofk.run(okeys.f32_bits(x), "f32", k, q, seed)
+    return compare(vals, idx, info, ref, "f32"), ref
+
+
+def _bf16_case(b, k, seed, eps=1e-6, recall=1.0, offset=0, **kw):
+    p = pk.plan(b.size, k, eps, recall, **kw)
+    q = oracle_plan_of(p, **kw)
+    note(f"flat bf16 N={b.size} k={k} seed={seed} off={offset} S={p.S} t={p.t} M={p.M}")
+    g = gpu_bf16(b, offset)
+    vals, idx, info = pk.topk(g, k, seed=seed, p=p)
+    ref = oprofk.run(b, "bf16", k, q, seed)
+    return compare(vals, idx, info, ref, "bf16"), ref
+
+
+# ----------------------------------------------------------- stage 1 ------
+@pytest.mark.parametrize("seed,row,S,N", [(0, 0, 32768, 2**20), (123, 7, 1359, 131072),
+                                          (2**63 + 5, 0, 131072, 2**28), (1, 0, 5, 3),
+                                          (99, 4095, 4097, 2**32 - 1)])
+def test_sample_indices_match_oracle(seed, row, S, N):
+    note(f"sample_indices seed={seed} row={row} S={S} N={N}")
+    got = pk.debug_sample_indices(seed, row, S, N).cpu().numpy()
+    assert np.array_equal(got, philox.sample_indices(seed, row, S, N))
+
+
+# ----------------------------------------------------------- stage 3 ------
+@pytest.mark.parametrize("offset", [0, 1, 2, 3])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_filter_survivor_set(dtype, offset):
+    N = 3 * 2**20 + 5
+    if dtype == "f32":
+        x = workloads.normal_f32(N, seed=11)
+        bits = okeys.f32_bits(x)
+        g = gpu_f32(x, offset)
+    else:
+        bits = workloads.relu_normal_bf16(N, seed=11)
+        g = gpu_bf16(bits, offset)
+    key = okeys.keys_of(bits, dtype)
+    tau = int(np.sort(key)[-5000])                         # about 5000 survivors
+    p = pk.plan(N, 64, 1e-6, 1.0, S_min=4096, S_max=4096, force_mode=pk.FORCE_FILTER)
+    p.M = 20000
+    surv = oprofk.survivors(key, tau)
+    for rep in range(3):
+        note(f"debug_filter {dtype} N={N} off={offset} rep={rep}")
+        bk, bi, cnt = pk.debug_filter(g, tau, p)
+        n = int(cnt.cpu().numpy()[0])
+        assert n == surv.size
+        gi = bi.cpu().numpy().view(np.uint32)[:n].astype(np.int64)
+        gk = bk.cpu().numpy().view(np.uint32)[:n].astype(np.int64)
+        order = np.argsort(gi)
+        assert np.array_equal(gi[order], surv)
+        assert np.array_equal(gk[order], key[surv])
+
+
+def test_filter_counts_past_capacity():
+    N = 2**20 + 3
+    x = workloads.uniform_f32(N, seed=12)
+    key = okeys.keys_of(okeys.f32_bits(x), "f32")
+    p = pk.plan(N, 64, 1e-6, 1.0, S_min=4096, S_max=4096, force_mode=pk.FORCE_FILTER)
+    p.M = 100
+    tau = int(np.sort(key)[-100000])
+    note("debug_filter past capacity")
+    bk, bi, cnt = pk.debug_filter(gpu_f32(x), tau, p)
+    assert int(cnt.cpu().numpy()[0]) == 100000
+    gi = bi.cpu().numpy().view(np.uint32)[:100].astype(np.int64)
+    assert np.all(key[gi] >= tau) and np.unique(gi).size == 100
+
+
+# ------------------------------------------------------------ end to end --
+@pytest.mark.parametrize("seed", range(10))
+def test_config1_uniform_2p20_k64(seed):
+    x = workloads.uniform_f32(2**20, seed=0)
+    rec, ref = _f32_case(x, 64, seed)
+    assert ref.status == oprofk.STATUS_FILTERED
+
+
+SMALL = dict(S_min=2048, S_max=2048, force_mode=pk.FORCE_FILTER)
+
+
+@pytest.mark.parametrize("N,k", [(5000, 1), (5000, 7), (65536 + 17, 64), (65536 + 17, 1000),
+                                 (300_001, 4096), (1 << 20, 333), (4099, 4096)])
+@pytest.mark.parametrize("dist", ["normal", "uniform", "ints"])
+def test_small_sizes_forced_filter(N, k, dist):
+    g = np.random.default_rng(N + k)
+    x = {"normal": lambda: g.standard_normal(N).astype(np.float32),
+         "uniform": lambda: g.random(N, dtype=np.float32),
+         "ints": lambda: g.integers(0, 300, N).astype(np.float32)}[dist]()
+    for seed in range(3):
+        _f32_case(x, k, seed, eps=1e-3, **SMALL)
+
+
+@pytest.mark.parametrize("offset", [1, 2, 3])
+def test_unaligned_base(offset):
+    x = workloads.normal_f32(2**20 + 9, seed=3)
+    _f32_case(x, 100, 5, offset=offset)
+
+
+def test_special_values_and_ties():
+    x = workloads.special_f32(200_000, seed=6)
+    for k in (1, 10, 500, 4096):
+        _f32_case(x, k, 1, eps=1e-3, **SMALL)
+
+
+@pytest.mark.parametrize("N,k", [(1, 1), (3, 2), (64, 64), (1000, 10), (1000, 1000), (70_000, 4096)])
+def test_direct_mode(N, k):
+    x = workloads.special_f32(N, seed=N)
+    rec, ref = _f32_case(x, k, 0)
+    assert ref.status == oprofk.STATUS_DIRECT
+
+
+@pytest.mark.parametrize("offset", [0, 1, 3])
+def test_bf16_flat(offset):
+    b = workloads.relu_normal_bf16(2**20 + 11, seed=3)
+    for k in (32, 100, 4096):
+        _bf16_case(b, k, 2, offset=offset)
+
+
+def test_relaxed_recall_flat():
+    x = workloads.normal_f32(2**20, seed=8)
+    for seed in range(5):
+        rec, ref = _f32_case(x, 2000, seed, recall=0.9)
+
+
+# ------------------------------------------------------- forced failures --
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forced_underflow_and_overflow(dtype):
+    N = 500_000
+    if dtype == "f32":
+        x = workloads.uniform_f32(N, seed=9)
+        x[[5, 77, 1234]] = 2.0
+        bits = okeys.f32_bits(x)
+        g = gpu_f32(x)
+    else:
+        bits = workloads.relu_normal_bf16(N, seed=9)
+        g = gpu_bf16(bits)
+    key = okeys.keys_of(bits, dtype)
+    k = 64
+    p = pk.plan(N, k, 1e-6, 1.0, S_min=4096, S_max=4096, force_mode=pk.FORCE_FILTER)
+    q = plan_from_lib(p)
+    for tau, want in ((int(key.max()), oprofk.STATUS_UNDERFLOW), (int(key.min()), oprofk.STATUS_OVERFLOW)):
+        note(f"topk_tau {dtype} tau={tau:#x}")
+        vals, idx, info = pk.topk_tau(g, k, tau, p)
+        ref = oprofk.run(bits, dtype, k, q, 0, tau_override=tau)
+        assert ref.status == want
+        compare(vals, idx, info, ref, dtype)
+
+
+def test_plan_override_small_buffer_overflows():
+    x = workloads.normal_f32(2**20, seed=10)
+    p = pk.plan(2**20, 64)
+    p.M = 64
+    q = plan_from_lib(p)
+    note("plan override M=k")
+    vals, idx, info = pk.topk(gpu_f32(x), 64, seed=0, p=p)
+    ref = oprofk.run(okeys.f32_bits(x), "f32", 64, q, 0)
+    assert ref.status == oprofk.STATUS_OVERFLOW
+    compare(vals, idx, info, ref, "f32")
+
+
+def test_repeat_is_deterministic():
+    x = workloads.normal_f32(2**22, seed=13)
+    g = gpu_f32(x)
+    p = pk.plan(x.size, 256)
+    note("determinism x20")
+    first = None
+    for _ in range(20):
+        vals, idx, info = pk.topk(g, 256, seed=4, p=p)
+        cur = (host_bits(vals).tobytes(), idx.cpu().numpy().tobytes(), info.cpu().numpy().tobytes())
+        if first is None:
+            first = cur
+        assert cur == first
+
+
+def test_simple_entry_point():
+    x = workloads.normal_f32(2**20, seed=14)
+    note("topk_simple")
+    vals, idx = pk.topk_simple(gpu_f32(x), 50, seed=3)
+    v, i = exact.topk(okeys.f32_bits(x), "f32", 50)
+    assert np.array_equal(idx.cpu().numpy(), i)
+    assert np.array_equal(host_bits(vals), v)
+    pk.lib().profk_release()
+
+
+# ------------------------------------------------------ full-size configs --
+@pytest.fixture(scope="module")
+def c2_input():
+    return workloads.normal_f32(2**28, seed=1)
+
+
+@pytest.mark.parametrize("k", [16, 256, 1024, 4096])
+def test_config2_normal_2p28(c2_input, k):
+    rec, ref = _f32_case(c2_input, k, 0)
+    assert ref.status == oprofk.STATUS_FILTERED
+
+
+C3 = {"pareto": lambda n: workloads.pareto_f32(n, seed=2),
+      "zeros90": lambda n: workloads.zeros90_f32(n, seed=2),
+      "ramp": lambda n: workloads.ramp_f32(n),
+      "plateau": lambda n: workloads.plateau_f32(n, seed=2, width=10_000),
+      "plateau_wide": lambda n: workloads.plateau_f32(n, seed=2, width=200_000)}
+
+
+@pytest.mark.parametrize("name", list(C3))
+def test_config3_adversarial_2p26(name):
+    x = C3[name](2**26)
+    rec, ref = _f32_case(x, 512, 0)
+    if name == "plateau_wide":
+        assert ref.status == oprofk.STATUS_OVERFLOW
