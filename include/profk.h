@@ -181,6 +181,12 @@ int profk_topk_tau(const profk_plan_t* plan, int32_t dtype, const void* values,
                    int64_t* out_idx, void* ws, size_t ws_bytes, void* stream,
                    profk_info_t* info_dev);
 
+/* Timing hook for measurement tools: while set, every flat call records
+ * `before` on its stream immediately before the filter-pass launch (stage 3)
+ * and `after` immediately after it.  Both are hipEvent_t passed as void*;
+ * NULL, NULL clears the hook.  The setting is per calling thread. */
+void profk_set_trace_events(void* before, void* after);
+
 /* ---- Status ------------------------------------------------------------- */
 
 const char* profk_status_string(int code);

@@ -84,6 +84,7 @@ def lib():
         L.profk_status_string.argtypes = [ctypes.c_int]
         L.profk_status_string.restype = ctypes.c_char_p
         L.profk_last_hip_error.restype = ctypes.c_int
+        L.profk_set_trace_events.argtypes = [vp, vp]
         _lib = L
     return _lib
 

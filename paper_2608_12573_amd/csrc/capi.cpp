@@ -12,6 +12,8 @@
 namespace {
 
 thread_local int g_last_hip_error = 0;
+thread_local hipEvent_t g_ev_before = nullptr;
+thread_local hipEvent_t g_ev_after = nullptr;
 
 int hip_fail(hipError_t e) {
   g_last_hip_error = static_cast<int>(e);
@@ -52,7 +54,7 @@ int run_flat(const profk_plan_t* plan, int32_t dtype, const void* values, int64_
   if (rc != PROFK_OK) return rc;
   profk::FlatCall c{plan, dtype, values, static_cast<uint32_t>(N), static_cast<uint32_t>(k), seed, row,
                     out_vals, out_idx, static_cast<uint8_t*>(ws), L, static_cast<hipStream_t>(stream),
-                    info, use_tau, tau_key};
+                    info, use_tau, tau_key, g_ev_before, g_ev_after};
   const hipError_t e = profk::launch_flat(c);
   return e == hipSuccess ? PROFK_OK : hip_fail(e);
 }
@@ -198,5 +200,10 @@ const char* profk_status_string(int code) {
 }
 
 int profk_last_hip_error(void) { return g_last_hip_error; }
+
+void profk_set_trace_events(void* before, void* after) {
+  g_ev_before = static_cast<hipEvent_t>(before);
+  g_ev_after = static_cast<hipEvent_t>(after);
+}
 
 }  // extern "C"

@@ -86,10 +86,19 @@ __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
   return x;
 }
 
+// Wave-wide maximum, uniform result: DPP exchanges inside each 16-lane row
+// (quad swaps, half-row and row mirrors), then the four row results are read
+// into scalars.
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) x = max(x, __shfl_xor(x, o, kWave));
-  return x;
+  x = max(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0xB1, 0xF, 0xF, false)));
+  x = max(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x4E, 0xF, 0xF, false)));
+  x = max(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x141, 0xF, 0xF, false)));
+  x = max(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x140, 0xF, 0xF, false)));
+  const uint32_t r0 = __builtin_amdgcn_readlane(static_cast<int>(x), 0);
+  const uint32_t r1 = __builtin_amdgcn_readlane(static_cast<int>(x), 16);
+  const uint32_t r2 = __builtin_amdgcn_readlane(static_cast<int>(x), 32);
+  const uint32_t r3 = __builtin_amdgcn_readlane(static_cast<int>(x), 48);
+  return max(max(r0, r1), max(r2, r3));
 }
 
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
@@ -168,7 +177,7 @@ __device__ __forceinline__ void for_items(uint32_t n, Load load, Body body) {
 constexpr int kSelBins = 2048;
 constexpr int kSelDigit = 11;
 
-struct SelectShared {
+struct alignas(16) SelectShared {
   uint32_t hist[kSelBins];
   uint32_t wsum[20];
   uint32_t found[4];
@@ -185,44 +194,88 @@ struct SelectResult {
 // the set, from any thread; every call site in the block calls it with the
 // same set.  Only the low `nbits` bits may differ between items: the bits
 // above are `prefix` for all of them.  Requires 1 <= kk <= |set|.
-template <int BS, class Visit>
-__device__ SelectResult block_select_kth(Visit visit, uint32_t kk, int nbits,
-                                         uint32_t prefix, SelectShared& sh) {
+// Digits are DIGIT bits wide; `hist` is LDS of 2^DIGIT words (16-byte
+// aligned).  Per digit pass: an LDS histogram, then wave 0 alone scans it
+// from the top with 16-byte reads and wave prefix sums, so a pass costs
+// three barriers.
+template <int BS, int DIGIT, class Visit>
+__device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t kk, int nbits,
+                                                         uint32_t prefix, uint32_t* hist,
+                                                         SelectShared& sh) {
+  static_assert(DIGIT >= 8 && DIGIT <= 13, "digit width");
+  const uint32_t tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
   uint32_t krem = kk, above_total = 0, eq = 0;
   int hi = nbits;
   if (hi == 0) {
-    // every item equals the prefix
     uint32_t cnt = 0;
     visit([&](uint32_t) { ++cnt; });
     eq = block_sum<BS>(cnt, sh.wsum);
   }
   while (hi > 0) {
-    const int bits = hi < kSelDigit ? hi : kSelDigit;
+    const int bits = hi < DIGIT ? hi : DIGIT;
     const int shift = hi - bits;
     const uint32_t nb = 1u << bits;
     const uint32_t hmask = (hi >= 32) ? 0u : ~((1u << hi) - 1u);
-    for (uint32_t b = threadIdx.x; b < nb; b += BS) sh.hist[b] = 0;
+    for (uint32_t b = tid; b < nb; b += BS) hist[b] = 0;
     __syncthreads();
     const uint32_t pre = prefix & hmask;
     visit([&](uint32_t s) {
-      if ((s & hmask) == pre) atomicAdd(&sh.hist[(s >> shift) & (nb - 1)], 1u);
+      if ((s & hmask) == pre) atomicAdd(&hist[(s >> shift) & (nb - 1)], 1u);
     });
     __syncthreads();
-    // Each thread owns a run of bins in descending order; an exclusive scan
-    // over threads gives the number of items in higher bins.
-    const uint32_t per = (nb + BS - 1) / BS;
-    const uint32_t r0 = threadIdx.x * per;   // descending rank of my first bin
-    uint32_t loc = 0;
-    for (uint32_t r = r0; r < r0 + per && r < nb; ++r) loc += sh.hist[nb - 1 - r];
-    uint32_t run = block_excl_sum<BS>(loc, sh.wsum, nullptr);
-    for (uint32_t r = r0; r < r0 + per && r < nb; ++r) {
-      const uint32_t h = sh.hist[nb - 1 - r];
-      if (run < krem && krem <= run + h) {
-        sh.found[0] = nb - 1 - r;
-        sh.found[1] = run;
-        sh.found[2] = h;
+    if (tid < kWave) {
+      if (nb >= static_cast<uint32_t>(4 * kWave)) {
+        // lane L owns bins [nb - (L+1)*per, nb - L*per); lane 0 the highest
+        const uint32_t per = nb / kWave;  // a multiple of 4
+        const uint32_t base = nb - (lane + 1) * per;
+        uint32_t loc = 0;
+        for (uint32_t q = 0; q < per; q += 4) {
+          const uint4 v4 = *reinterpret_cast<const uint4*>(&hist[base + q]);
+          loc += v4.x + v4.y + v4.z + v4.w;
+        }
+        uint32_t run = wave_incl_sum(loc) - loc;
+        if (run < krem && krem <= run + loc) {
+          // the rank falls in this lane's bins: walk them from the top
+          for (int q = static_cast<int>(per) - 4; q >= 0; q -= 4) {
+            const uint4 v4 = *reinterpret_cast<const uint4*>(&hist[base + q]);
+            const uint32_t c4[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+            for (int j = 3; j >= 0; --j) {
+              if (run < krem && krem <= run + c4[j]) {
+                sh.found[0] = base + q + j;
+                sh.found[1] = run;
+                sh.found[2] = c4[j];
+              }
+              run += c4[j];
+            }
+          }
+        }
+      } else {
+        // at most 128 bins: lane L owns descending ranks [L*per, (L+1)*per)
+        const uint32_t per = (nb + kWave - 1) / kWave;  // 1 or 2
+        uint32_t hv[2];
+        uint32_t loc = 0;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const uint32_t r = lane * per + q;
+          hv[q] = (static_cast<uint32_t>(q) < per && r < nb) ? hist[nb - 1 - r] : 0u;
+          loc += hv[q];
+        }
+        uint32_t run = wave_incl_sum(loc) - loc;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const uint32_t r = lane * per + q;
+          if (static_cast<uint32_t>(q) < per && r < nb) {
+            if (run < krem && krem <= run + hv[q]) {
+              sh.found[0] = nb - 1 - r;
+              sh.found[1] = run;
+              sh.found[2] = hv[q];
+            }
+            run += hv[q];
+          }
+        }
       }
-      run += h;
     }
     __syncthreads();
     const uint32_t d = sh.found[0], ab = sh.found[1];
@@ -231,13 +284,61 @@ __device__ SelectResult block_select_kth(Visit visit, uint32_t kk, int nbits,
     krem -= ab;
     above_total += ab;
     hi = shift;
-    __syncthreads();
   }
+  __syncthreads();
   SelectResult res;
   res.kth = prefix;
   res.above = above_total;
   res.equal = eq;
   return res;
+}
+
+// The common case: 11-bit digits in the SelectShared histogram.
+template <int BS, class Visit>
+__device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t kk, int nbits,
+                                                         uint32_t prefix, SelectShared& sh) {
+  return block_select_kth<BS, kSelDigit>(visit, kk, nbits, prefix, sh.hist, sh);
+}
+
+// Top-t of up to 64*E keys held by one wave (E per lane, `valid` bits mark
+// which of a lane's slots hold keys): t rounds of a wave-wide max; the lowest
+// lane holding the maximum gives up one copy and stores it to out[round]
+// (out may be null).  Returns got = min(t, number of keys); `last` receives
+// the got-th largest key in every lane.
+template <int E>
+__device__ __forceinline__ uint32_t wave_top_t(uint32_t (&v)[E], uint32_t valid, uint32_t t,
+                                               uint32_t* out, uint32_t& last) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint32_t got = 0;
+  for (; got < t; ++got) {
+    uint32_t m = 0;
+    bool have = false;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if ((valid >> e) & 1u) {
+        m = have ? max(m, v[e]) : v[e];
+        have = true;
+      }
+    const uint64_t any = __ballot(have);
+    if (any == 0) break;
+    uint32_t wm = have ? m : 0u;
+    wm = wave_max_u32(wm);
+    last = wm;
+    // lanes whose maximum equals the wave maximum; the lowest one gives it up
+    const uint64_t holders = __ballot(have && m == wm);
+    const int owner = __ffsll(static_cast<unsigned long long>(holders)) - 1;
+    if (lane == owner) {
+      bool done = false;
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (!done && ((valid >> e) & 1u) && v[e] == wm) {
+          valid &= ~(1u << e);
+          done = true;
+        }
+      if (out) out[got] = wm;
+    }
+  }
+  return got;
 }
 
 // Number of leading bits shared by every value in [lo, hi] (lo <= hi),
@@ -248,19 +349,60 @@ __device__ __forceinline__ int shared_prefix_bits(uint32_t lo, uint32_t hi, int 
 }
 
 // ----------------------------------------------------------- bitonic sort --
-// Sorts a[0..n) descending, n a power of two, in LDS.  Caller syncs before.
-template <int BS>
-__device__ void bitonic_sort_desc(uint64_t* a, uint32_t n) {
-  for (uint32_t size = 2; size <= n; size <<= 1) {
+// Sorts P = E*BS 64-bit values descending.  Thread t holds positions
+// e*BS + t (e < E) in v[e].  Compare-exchange partners at stride s are in the
+// same thread (s >= BS), in another wave (64 <= s < BS: through LDS, one
+// barrier per stage with two alternating buffers) or in the same wave
+// (s < 64: lane shuffles).  `lds` holds 2*P values.
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m) {
+  const uint32_t lo = __shfl_xor(static_cast<uint32_t>(x), m, kWave);
+  const uint32_t hi = __shfl_xor(static_cast<uint32_t>(x >> 32), m, kWave);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+template <int BS, int E>
+__device__ __forceinline__ void bitonic_sort_regs_desc(uint64_t (&v)[E], uint64_t* lds) {
+  constexpr uint32_t P = static_cast<uint32_t>(E) * BS;
+  const uint32_t t = threadIdx.x;
+  int buf = 0;
+  for (uint32_t size = 2; size <= P; size <<= 1) {
     for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
-      for (uint32_t i = threadIdx.x; i < n / 2; i += BS) {
-        const uint32_t lo = 2 * i - (i & (stride - 1));
-        const uint32_t hi = lo + stride;
-        const bool desc = (lo & size) == 0;
-        const uint64_t x = a[lo], y = a[hi];
-        if ((x < y) == desc) { a[lo] = y; a[hi] = x; }
+      if (stride >= static_cast<uint32_t>(BS)) {
+        const uint32_t es = stride / BS;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          if ((static_cast<uint32_t>(e) & es) == 0) {
+            const int f = e ^ static_cast<int>(es);
+            const uint32_t p = static_cast<uint32_t>(e) * BS + t;
+            const bool desc = (p & size) == 0;
+            const uint64_t a = v[e], b = v[f];
+            if ((a < b) == desc) { v[e] = b; v[f] = a; }
+          }
+        }
+      } else if (stride >= static_cast<uint32_t>(kWave)) {
+        uint64_t* cur = lds + (buf ? P : 0);
+        buf ^= 1;
+#pragma unroll
+        for (int e = 0; e < E; ++e) cur[static_cast<uint32_t>(e) * BS + t] = v[e];
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const uint32_t p = static_cast<uint32_t>(e) * BS + t;
+          const uint64_t o = cur[p ^ stride];
+          const bool desc = (p & size) == 0;
+          const bool lower = (p & stride) == 0;
+          v[e] = (lower == desc) ? max(v[e], o) : min(v[e], o);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const uint32_t p = static_cast<uint32_t>(e) * BS + t;
+          const uint64_t o = shfl_xor_u64(v[e], static_cast<int>(stride));
+          const bool desc = (p & size) == 0;
+          const bool lower = (p & stride) == 0;
+          v[e] = (lower == desc) ? max(v[e], o) : min(v[e], o);
+        }
       }
-      __syncthreads();
     }
   }
 }

@@ -3,17 +3,18 @@
 // Sec. 3 "The Prof-K Algorithm".
 //
 // Kernel sequence of one call, all on the caller's stream:
-//   k_sample      ceil(S/4096) blocks: Philox draws, gathers, and each block's
+//   k_sample      ceil(S/1024) blocks: Philox draws, gathers, and each block's
 //                 local top-t sample keys (the t-th largest of the whole
 //                 sample is among the union of the blocks' top-t).
-//   k_select_tau  one block: tau = t-th largest key of that union.
+//   k_select_tau  only when that union is large: one block picks tau.
 //   k_filter      persistent grid, one contiguous chunk per block, 16-byte
-//                 nontemporal loads; survivors go to the block's private
-//                 region of the candidate buffer through LDS-allocated
-//                 slots, so the pass issues no same-address global atomics
-//                 (those serialise across the chip).
-//   k_finish      reads the per-block counts; when k_req <= count <= M one
-//                 block refines the buffer exactly in LDS, otherwise every
+//                 nontemporal loads.  When the union is small each block
+//                 first selects tau from it itself.  Survivors are staged in
+//                 LDS and appended to one of eight candidate segments with
+//                 one atomic per block, because same-address global atomics
+//                 serialise across the chip.
+//   k_finish      reads the segment counts; when k_req <= count <= M one
+//                 block refines the candidates exactly, otherwise every
 //                 block computes the exact top-k of its chunk of the input
 //                 and the last block to finish merges them.
 #include <climits>
@@ -30,6 +31,14 @@ template <int DT> struct Elem;
 template <> struct Elem<0> { static constexpr int EPV = 4, ES = 4, KEYBITS = 32; };
 template <> struct Elem<1> { static constexpr int EPV = 8, ES = 2, KEYBITS = 16; };
 
+__device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt) {
+  if (threadIdx.x < kSegs) seg_cnt[threadIdx.x * kSegStride] = 0;
+  if (threadIdx.x == 0) {
+    st->ticket = 0;
+    st->status = 0;
+  }
+}
+
 // ------------------------------------------------------------ stage 1 -----
 struct SampleArgs {
   const void* values;
@@ -37,33 +46,66 @@ struct SampleArgs {
   uint32_t S, t, tcap;
   uint32_t* union_keys;
   CallState* st;
+  uint32_t* seg_cnt;
 };
 
 template <int DT>
 __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
+  constexpr int NW = kSampBS / kWave;
   __shared__ uint32_t keys[kSampPerBlock];
+  __shared__ uint32_t lists[NW][kWaveTopMax];
+  __shared__ uint32_t list_n[NW];
   __shared__ SelectShared sel;
   __shared__ uint32_t emitted;
-  const uint32_t b = blockIdx.x, tid = threadIdx.x;
-  if (b == 0 && tid == 0) {
-    a.st->spill_cnt = 0;
-    a.st->ticket = 0;
-    a.st->status = 0;
-  }
+  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  if (b == 0) reset_state(a.st, a.seg_cnt);
   const uint32_t j0 = b * kSampPerBlock;
   const uint32_t nb = min(static_cast<uint32_t>(kSampPerBlock), a.S - j0);
+  uint32_t kv[4];
+  uint32_t valid = 0;
   {
     // draw j = j0 + 4*tid + q is word q of Philox block (j0/4 + tid)
-    const U64x4 w = philox4x64_10(static_cast<uint64_t>(j0 / 4) + tid, a.row, 0, 0, a.seed, 0);
+    const U64x4 r = philox4x64_10(static_cast<uint64_t>(j0 / 4) + tid, a.row, 0, 0, a.seed, 0);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint32_t j = 4 * tid + q;
-      if (j < nb) keys[j] = key_of<DT>(load_raw<DT>(a.values, index_of_word(w.w[q], a.n)));
+      kv[q] = 0;
+      if (j < nb) {
+        kv[q] = key_of<DT>(load_raw<DT>(a.values, index_of_word(r.w[q], a.n)));
+        valid |= 1u << q;
+      }
     }
   }
-  __syncthreads();
   uint32_t* dst = a.union_keys + static_cast<size_t>(b) * a.tcap;
   const uint32_t tl = min(a.t, nb);
+  if (a.t <= kWaveTopMax) {
+    // each wave keeps its top-tl draws, then wave 0 merges the NW lists
+    uint32_t last;
+    const uint32_t got = wave_top_t<4>(kv, valid, tl, lists[w], last);
+    if (lane == 0) list_n[w] = got;
+    __syncthreads();
+    if (w == 0) {
+      constexpr int E2 = NW * kWaveTopMax / kWave;
+      uint32_t v2[E2];
+      uint32_t valid2 = 0;
+#pragma unroll
+      for (int e = 0; e < E2; ++e) {
+        // concatenated list position c = lane + 64*e
+        uint32_t c = lane + kWave * e, li = 0;
+        v2[e] = 0;
+#pragma unroll
+        for (int i = 0; i < NW; ++i)
+          if (li == static_cast<uint32_t>(i) && c >= list_n[i]) { c -= list_n[i]; li = i + 1; }
+        if (li < NW) { v2[e] = lists[li][c]; valid2 |= 1u << e; }
+      }
+      wave_top_t<E2>(v2, valid2, tl, dst, last);
+    }
+    return;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if ((valid >> q) & 1u) keys[4 * tid + q] = kv[q];
+  __syncthreads();
   if (tl == nb) {
     for (uint32_t j = tid; j < nb; j += kSampBS) dst[j] = keys[j];
     return;
@@ -80,6 +122,8 @@ __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
 }
 
 // ------------------------------------------------------------ stage 2 -----
+// tau = t-th largest key of the union.  Used when the union is too large
+// for the filter blocks to select from it themselves.
 constexpr uint32_t kTauCache = 16384;
 
 struct TauArgs {
@@ -111,22 +155,26 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
   if (tid == 0) a.st->tau_key = r.kth;
 }
 
-__global__ void k_init_state(CallState* st, uint32_t tau_key) {
-  if (threadIdx.x == 0) {
-    st->tau_key = tau_key;
-    st->spill_cnt = 0;
-    st->ticket = 0;
-    st->status = 0;
-  }
+struct InitArgs {
+  CallState* st;
+  uint32_t* seg_cnt;
+  uint32_t tau_key;
+};
+
+__global__ void k_init_state(InitArgs a) {
+  reset_state(a.st, a.seg_cnt);
+  if (threadIdx.x == 0) a.st->tau_key = a.tau_key;
 }
 
 // ------------------------------------------------------------ stage 3 -----
 struct FilterArgs {
   const void* values;
   uint32_t n, head, nvec, vpb;
-  uint32_t C, spill_cap;
+  uint32_t seg_cap;
   CallState* st;
-  uint32_t *reg_key, *reg_idx, *blk_cnt, *blk_max, *spill_key, *spill_idx;
+  const uint32_t* union_keys;  // sample union to select tau from, or null: tau in st
+  uint32_t union_n, t;
+  uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
 };
 
 // Survival test on a transformed word: for a threshold whose pattern is
@@ -138,11 +186,68 @@ template <int DT>
 __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   constexpr int EPV = Elem<DT>::EPV;
   constexpr int ES = Elem<DT>::ES;
-  __shared__ uint32_t s_cnt;
+  __shared__ uint32_t s_skey[kStage], s_sidx[kStage];
+  __shared__ uint32_t s_union[kFiltTauMax];
+  __shared__ SelectShared s_sel;
+  __shared__ uint32_t s_cnt, s_tau, s_base;
   __shared__ uint32_t s_wmax[kFiltBS / kWave];
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), b = blockIdx.x;
+  const uint32_t seg = b & (kSegs - 1);
   if (tid == 0) s_cnt = 0;
-  const uint32_t tau = a.st->tau_key;
+
+  // ---- threshold (stage 2) when the sample union is small
+  uint32_t tau;
+  if (a.union_n) {
+    for (uint32_t i = tid; i < a.union_n; i += kFiltBS) s_union[i] = a.union_keys[i];
+    __syncthreads();
+    if (a.t <= kWaveTopMax) {
+      // every wave keeps the top t of its share, wave 0 merges the lists
+      constexpr int NW = kFiltBS / kWave;
+      constexpr int E = kFiltTauMax / kFiltBS;
+      uint32_t uk[E];
+      uint32_t valid = 0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t i = tid + kFiltBS * e;
+        uk[e] = i < a.union_n ? s_union[i] : 0u;
+        if (i < a.union_n) valid |= 1u << e;
+      }
+      uint32_t last = 0;
+      const uint32_t w = tid / kWave;
+      const uint32_t got = wave_top_t<E>(uk, valid, a.t, s_sel.hist + w * kWaveTopMax, last);
+      if (lane == 0) s_sel.found[w] = got;
+      __syncthreads();
+      if (w == 0) {
+        constexpr int E2 = NW * kWaveTopMax / kWave;
+        uint32_t v2[E2];
+        uint32_t valid2 = 0;
+#pragma unroll
+        for (int e = 0; e < E2; ++e) {
+          uint32_t c = lane + kWave * e, li = 0;
+          v2[e] = 0;
+#pragma unroll
+          for (int i = 0; i < NW; ++i)
+            if (li == static_cast<uint32_t>(i) && c >= s_sel.found[i]) { c -= s_sel.found[i]; li = i + 1; }
+          if (li < NW) { v2[e] = s_sel.hist[li * kWaveTopMax + c]; valid2 |= 1u << e; }
+        }
+        wave_top_t<E2>(v2, valid2, a.t, nullptr, last);
+        if (lane == 0) s_tau = last;
+      }
+    } else {
+      const SelectResult r = block_select_kth<kFiltBS>(
+          [&](auto f) {
+            for (uint32_t i = tid; i < a.union_n; i += kFiltBS) f(s_union[i]);
+          },
+          a.t, Elem<DT>::KEYBITS, 0u, s_sel);
+      if (tid == 0) s_tau = r.kth;
+    }
+    __syncthreads();
+    tau = s_tau;
+    if (b == 0 && tid == 0) a.st->tau_key = tau;
+  } else {
+    tau = a.st->tau_key;
+  }
+
   uint32_t flip;
   int thr;
   if (DT == 0) {
@@ -159,36 +264,38 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   const uint32_t neutral = DT == 0 ? (0x80000000u ^ flip) : ((0x8000u * 0x10001u) ^ flip);
   __syncthreads();
 
+  uint32_t* const seg_counter = a.seg_cnt + seg * kSegStride;
+  uint32_t* const seg_key = a.seg_key + static_cast<size_t>(seg) * a.seg_cap;
+  uint32_t* const seg_idx = a.seg_idx + static_cast<size_t>(seg) * a.seg_cap;
   uint32_t my_max = 0;
-  // Reserve `total` consecutive slots of this block's region for one wave;
-  // slots past the region capacity go to the shared spill list.
-  auto reserve = [&](uint32_t cnt, uint32_t& slot, uint32_t& first_spill, uint32_t& sbase) {
+  // Reserve consecutive staging slots for one wave; slots past the LDS
+  // stage go straight to the block's segment.
+  auto reserve = [&](uint32_t cnt, uint32_t& slot, uint32_t& first_over, uint32_t& gbase) {
     const uint32_t incl = wave_incl_sum(cnt);
     const uint32_t total = __shfl(incl, kWave - 1, kWave);
     uint32_t base = 0;
     if (lane == 0) base = atomicAdd(&s_cnt, total);
     base = __shfl(base, 0, kWave);
-    const uint32_t n_in = base < a.C ? min(total, a.C - base) : 0u;
-    const uint32_t n_spill = total - n_in;
-    sbase = 0;
-    if (n_spill) {
-      if (lane == 0) sbase = atomicAdd(&a.st->spill_cnt, n_spill);
-      sbase = __shfl(sbase, 0, kWave);
+    const uint32_t n_in = base < kStage ? min(total, kStage - base) : 0u;
+    const uint32_t n_over = total - n_in;
+    gbase = 0;
+    if (n_over) {
+      if (lane == 0) gbase = atomicAdd(seg_counter, n_over);
+      gbase = __shfl(gbase, 0, kWave);
     }
-    first_spill = base + n_in;
+    first_over = base + n_in;
     slot = base + incl - cnt;
   };
-  auto store = [&](uint32_t slot, uint32_t first_spill, uint32_t sbase, uint32_t key, uint32_t idx) {
+  auto store = [&](uint32_t slot, uint32_t first_over, uint32_t gbase, uint32_t key, uint32_t idx) {
     my_max = max(my_max, key);
-    if (slot < a.C) {
-      const size_t g = static_cast<size_t>(b) * a.C + slot;
-      a.reg_key[g] = key;
-      a.reg_idx[g] = idx;
+    if (slot < kStage) {
+      s_skey[slot] = key;
+      s_sidx[slot] = idx;
     } else {
-      const uint32_t sp = sbase + (slot - first_spill);
-      if (sp < a.spill_cap) {
-        a.spill_key[sp] = key;
-        a.spill_idx[sp] = idx;
+      const uint32_t gp = gbase + (slot - first_over);
+      if (gp < a.seg_cap) {
+        seg_key[gp] = key;
+        seg_idx[gp] = idx;
       }
     }
   };
@@ -238,8 +345,8 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
         }
       }
     }
-    uint32_t slot, first_spill, sbase;
-    reserve(cnt, slot, first_spill, sbase);
+    uint32_t slot, first_over, gbase;
+    reserve(cnt, slot, first_over, gbase);
 #pragma unroll
     for (int u = 0; u < kFiltU; ++u) {
       const uint32_t vi = vb + u * kFiltBS + tid;
@@ -250,16 +357,16 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
         const uint32_t w = raw ^ flip;
         if (DT == 0) {
           if (valid && static_cast<int>(w) >= thr) {
-            store(slot, first_spill, sbase, key_f32(raw), a.head + vi * EPV + e);
+            store(slot, first_over, gbase, key_f32(raw), a.head + vi * EPV + e);
             ++slot;
           }
         } else {
           if (valid && (static_cast<int>(w << 16) >> 16) >= thr) {
-            store(slot, first_spill, sbase, key_bf16(raw & 0xFFFFu), a.head + vi * EPV + 2 * e);
+            store(slot, first_over, gbase, key_bf16(raw & 0xFFFFu), a.head + vi * EPV + 2 * e);
             ++slot;
           }
           if (valid && (static_cast<int>(w) >> 16) >= thr) {
-            store(slot, first_spill, sbase, key_bf16(raw >> 16), a.head + vi * EPV + 2 * e + 1);
+            store(slot, first_over, gbase, key_bf16(raw >> 16), a.head + vi * EPV + 2 * e + 1);
             ++slot;
           }
         }
@@ -279,21 +386,32 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
       ok = key >= tau;
     }
     if (__ballot(ok)) {
-      uint32_t slot, first_spill, sbase;
-      reserve(ok ? 1u : 0u, slot, first_spill, sbase);
-      if (ok) store(slot, first_spill, sbase, key, idx);
+      uint32_t slot, first_over, gbase;
+      reserve(ok ? 1u : 0u, slot, first_over, gbase);
+      if (ok) store(slot, first_over, gbase, key, idx);
     }
   }
 
+  // Append the staged survivors to the segment: one atomic per block.
   const uint32_t wm = wave_max_u32(my_max);
   if (lane == 0) s_wmax[tid / kWave] = wm;
   __syncthreads();
+  const uint32_t n_st = min(s_cnt, kStage);
   if (tid == 0) {
+    s_base = n_st ? atomicAdd(seg_counter, n_st) : 0u;
     uint32_t m = 0;
 #pragma unroll
     for (int i = 0; i < kFiltBS / kWave; ++i) m = max(m, s_wmax[i]);
-    a.blk_cnt[b] = s_cnt;
     a.blk_max[b] = m;
+  }
+  __syncthreads();
+  const uint32_t base = s_base;
+  for (uint32_t i = tid; i < n_st; i += kFiltBS) {
+    const uint32_t gp = base + i;
+    if (gp < a.seg_cap) {
+      seg_key[gp] = s_skey[i];
+      seg_idx[gp] = s_sidx[i];
+    }
   }
 }
 
@@ -301,45 +419,82 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
 constexpr uint32_t kFinCache = 28672;
 
 struct FinShared {
-  uint32_t cache[kFinCache];
+  uint32_t cache[kFinCache];       // candidate keys; later the sort's exchange buffers
   uint64_t sortbuf[kFinMaxK];
   uint32_t pre[1024];
   SelectShared sel;
+  uint32_t seg_n[kSegs], seg_pre[kSegs + 1];
   uint32_t misc[8];
 };
 
-// Last index b with pre[b] <= i (pre non-decreasing, pre[0] = 0).
-__device__ __forceinline__ uint32_t region_of(const uint32_t* pre, uint32_t G, uint32_t i) {
-  uint32_t lo = 0, hi = G;
-  while (hi - lo > 1) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (pre[mid] <= i) lo = mid; else hi = mid;
-  }
-  return lo;
-}
+// Index accessors handed to candidate visitors: an index is loaded only
+// when a visitor asks for it.
+struct LoadIdx {
+  const uint32_t* p;
+  __device__ __forceinline__ uint32_t operator()() const { return *p; }
+};
+struct PosIdx {
+  uint32_t v;
+  __device__ __forceinline__ uint32_t operator()() const { return v; }
+};
 
-// Candidates stored in G regions of capacity C (the first `stored` entries
-// of each, exclusive prefix in `pre`) followed by a plain list.
+// The filter's candidates: segment x holds n_x entries at x*cap; candidate i
+// is entry i - pre[x] of the segment with pre[x] <= i < pre[x+1].
+struct SegSrc {
+  const uint32_t *key, *idx;
+  uint32_t cap;
+  const uint32_t* pre;  // LDS, kSegs + 1 entries
+  __device__ __forceinline__ size_t pos(uint32_t i) const {
+    uint32_t x = 0;
+#pragma unroll
+    for (int j = 1; j < kSegs; ++j) x += (i >= pre[j]) ? 1u : 0u;
+    return static_cast<size_t>(x) * cap + (i - pre[x]);
+  }
+  template <int BS, class F>
+  __device__ __forceinline__ void visit(uint32_t n, const uint32_t* cache, F f) const {
+    for_items<BS, 8>(n, [&](uint32_t i) { return cache ? cache[i] : key[pos(i)]; },
+                     [&](uint32_t i, uint32_t v) { f(i, v, LoadIdx{idx + pos(i)}); });
+  }
+  __device__ __forceinline__ uint32_t idx_at(uint32_t i) const { return idx[pos(i)]; }
+};
+
+// Per-chunk exact results of the fallback: G regions of capacity C, region
+// r holding pre[r+1] - pre[r] entries (pre an LDS exclusive prefix, R the
+// total); one wave per region.
 struct RegionSrc {
   const uint32_t *key, *idx;
   uint32_t C, G, R;
   const uint32_t* pre;
-  const uint32_t *skey, *sidx;
-  __device__ size_t where(uint32_t i, bool& in_list) const {
-    if (i >= R) { in_list = true; return i - R; }
-    in_list = false;
-    const uint32_t r = region_of(pre, G, i);
-    return static_cast<size_t>(r) * C + (i - pre[r]);
+  template <int BS, class F>
+  __device__ __forceinline__ void visit(uint32_t, const uint32_t* cache, F f) const {
+    constexpr uint32_t groups = BS / kWave;
+    const uint32_t g = threadIdx.x / kWave, l = threadIdx.x % kWave;
+    for (uint32_t r = g; r < G; r += groups) {
+      const uint32_t bi = pre[r];
+      const uint32_t n = (r + 1 < G ? pre[r + 1] : R) - bi;
+      const size_t bg = static_cast<size_t>(r) * C;
+      for (uint32_t j0 = l; j0 < n; j0 += kWave * 8) {
+        uint32_t kv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint32_t j = j0 + u * kWave;
+          kv[u] = j < n ? (cache ? cache[bi + j] : key[bg + j]) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint32_t j = j0 + u * kWave;
+          if (j < n) f(bi + j, kv[u], LoadIdx{idx + bg + j});
+        }
+      }
+    }
   }
-  __device__ uint32_t get_key(uint32_t i) const {
-    bool l;
-    const size_t p = where(i, l);
-    return l ? skey[p] : key[p];
-  }
-  __device__ uint32_t get_idx(uint32_t i) const {
-    bool l;
-    const size_t p = where(i, l);
-    return l ? sidx[p] : idx[p];
+  __device__ __forceinline__ uint32_t idx_at(uint32_t i) const {
+    uint32_t lo = 0, hi = G;  // last region r with pre[r] <= i
+    while (hi - lo > 1) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (pre[mid] <= i) lo = mid; else hi = mid;
+    }
+    return idx[static_cast<size_t>(lo) * C + (i - pre[lo])];
   }
 };
 
@@ -348,94 +503,118 @@ template <int DT>
 struct InputSrc {
   const void* values;
   uint32_t lo;
-  __device__ uint32_t get_key(uint32_t i) const { return key_of<DT>(load_raw<DT>(values, lo + i)); }
-  __device__ uint32_t get_idx(uint32_t i) const { return lo + i; }
+  template <int BS, class F>
+  __device__ __forceinline__ void visit(uint32_t n, const uint32_t* cache, F f) const {
+    for_items<BS, 8>(n, [&](uint32_t i) { return cache ? cache[i] : key_of<DT>(load_raw<DT>(values, lo + i)); },
+                     [&](uint32_t i, uint32_t v) { f(i, v, PosIdx{lo + i}); });
+  }
+  __device__ __forceinline__ uint32_t idx_at(uint32_t i) const { return lo + i; }
 };
 
 // Exact top-kk (kk <= kFinMaxK, kk <= n) of a candidate set under the total
-// order, collected into sh.sortbuf (unsorted) and returned count kk.  Keys of
-// all candidates lie in [lo_key, hi_key].
+// order, collected unsorted into sh.sortbuf[0..kk).  Every candidate key lies
+// in [lo_key, hi_key].  The radix histogram (12-bit digits) borrows the sort
+// buffer; the collection first reserves slots for (key, candidate number)
+// and then loads all selected indices at once.
 template <class Src>
-__device__ void select_topk(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
-                            uint32_t hi_key, int keybits, FinShared& sh) {
+__device__ __forceinline__ void select_topk(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
+                                            uint32_t hi_key, int keybits, FinShared& sh) {
+  constexpr int kDigit = 12;
+  uint32_t* const hist = reinterpret_cast<uint32_t*>(sh.sortbuf);
   const uint32_t tid = threadIdx.x;
   const bool cached = n <= kFinCache;
-  auto gkey = [&](uint32_t i) { return src.get_key(i); };
   if (cached) {
-    for_items<kFinBS, 8>(n, gkey, [&](uint32_t i, uint32_t v) { sh.cache[i] = v; });
+    src.template visit<kFinBS>(n, nullptr, [&](uint32_t i, uint32_t key, auto) { sh.cache[i] = key; });
     __syncthreads();
   }
-  auto visit_i = [&](auto f) {
+  const uint32_t* cache = cached ? sh.cache : nullptr;
+  auto keys_only = [&](auto f) {
     if (cached) {
-      for (uint32_t i = tid; i < n; i += kFinBS) f(i, sh.cache[i]);
+      for (uint32_t i = tid; i < n; i += kFinBS) f(sh.cache[i]);
     } else {
-      for_items<kFinBS, 8>(n, gkey, f);
+      src.template visit<kFinBS>(n, nullptr, [&](uint32_t, uint32_t key, auto) { f(key); });
     }
   };
   const int shared = shared_prefix_bits(lo_key, hi_key, keybits);
-  const SelectResult r = block_select_kth<kFinBS>(
-      [&](auto f) { visit_i([&](uint32_t, uint32_t key) { f(key); }); }, kk, keybits - shared,
-      lo_key, sh.sel);
+  const SelectResult r =
+      block_select_kth<kFinBS, kDigit>(keys_only, kk, keybits - shared, lo_key, hist, sh.sel);
   const uint32_t kstar = r.kth;
   const uint32_t krem = kk - r.above;
   const bool cut = krem < r.equal;
   uint32_t istar = 0xFFFFFFFFu;
   if (cut) {
     // the krem smallest indices among the ties at kstar
-    const SelectResult ri = block_select_kth<kFinBS>(
+    const SelectResult ri = block_select_kth<kFinBS, kDigit>(
         [&](auto f) {
-          visit_i([&](uint32_t i, uint32_t key) {
-            if (key == kstar) f(~src.get_idx(i));
+          src.template visit<kFinBS>(n, cache, [&](uint32_t, uint32_t key, auto idx) {
+            if (key == kstar) f(~idx());
           });
         },
-        krem, 32, 0u, sh.sel);
+        krem, 32, 0u, hist, sh.sel);
     istar = ~ri.kth;
   }
   if (tid == 0) sh.misc[0] = 0;
   __syncthreads();
-  visit_i([&](uint32_t i, uint32_t key) {
-    if (key >= kstar) {
-      const uint32_t id = src.get_idx(i);
-      if (key > kstar || !cut || id <= istar) {
-        const uint32_t p = atomicAdd(&sh.misc[0], 1u);
-        if (p < kFinMaxK) sh.sortbuf[p] = composite(key, id);
-      }
+  src.template visit<kFinBS>(n, cache, [&](uint32_t i, uint32_t key, auto idx) {
+    if (key > kstar || (key == kstar && (!cut || idx() <= istar))) {
+      const uint32_t p = atomicAdd(&sh.misc[0], 1u);
+      if (p < kFinMaxK) sh.sortbuf[p] = (static_cast<uint64_t>(key) << 32) | i;
     }
   });
   __syncthreads();
+  for (uint32_t p = tid; p < kk; p += kFinBS) {
+    const uint64_t e = sh.sortbuf[p];
+    sh.sortbuf[p] = composite(static_cast<uint32_t>(e >> 32), src.idx_at(static_cast<uint32_t>(e)));
+  }
+  __syncthreads();
 }
 
-template <int DT>
-__device__ void write_sorted(FinShared& sh, uint32_t kk, uint32_t k, void* out_vals,
-                             int64_t* out_idx) {
+template <int DT, int E>
+__device__ __forceinline__ void sort_and_write(FinShared& sh, uint32_t kk, uint32_t k, void* out_vals,
+                                               int64_t* out_idx) {
   const uint32_t tid = threadIdx.x;
-  const uint32_t P = next_pow2(kk);
-  for (uint32_t i = kk + tid; i < P; i += kFinBS) sh.sortbuf[i] = 0;
-  __syncthreads();
-  bitonic_sort_desc<kFinBS>(sh.sortbuf, P);
-  for (uint32_t i = tid; i < k; i += kFinBS) {
+  uint64_t v[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const uint32_t p = static_cast<uint32_t>(e) * kFinBS + tid;
+    v[e] = p < kk ? sh.sortbuf[p] : 0ull;
+  }
+  bitonic_sort_regs_desc<kFinBS, E>(v, reinterpret_cast<uint64_t*>(sh.cache));
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const uint32_t p = static_cast<uint32_t>(e) * kFinBS + tid;
+    if (p >= k) continue;
     uint32_t bits;
     int64_t id;
-    if (i < kk) {
-      const uint64_t c = sh.sortbuf[i];
-      bits = bits_of_key<DT>(comp_key(c));
-      id = comp_idx(c);
+    if (p < kk) {
+      bits = bits_of_key<DT>(comp_key(v[e]));
+      id = comp_idx(v[e]);
     } else {
       bits = DT == 0 ? 0xFF800000u : 0xFF80u;  // -inf padding (relaxed recall)
       id = -1;
     }
-    if (DT == 0) static_cast<uint32_t*>(out_vals)[i] = bits;
-    else static_cast<uint16_t*>(out_vals)[i] = static_cast<uint16_t>(bits);
-    out_idx[i] = id;
+    if (DT == 0) static_cast<uint32_t*>(out_vals)[p] = bits;
+    else static_cast<uint16_t*>(out_vals)[p] = static_cast<uint16_t>(bits);
+    out_idx[p] = id;
   }
+}
+
+// Sorts the kk collected candidates and writes the k outputs.
+template <int DT>
+__device__ __forceinline__ void write_sorted(FinShared& sh, uint32_t kk, uint32_t k, void* out_vals,
+                                             int64_t* out_idx) {
+  const uint32_t P = next_pow2(max(kk, k));
+  if (P <= static_cast<uint32_t>(kFinBS)) sort_and_write<DT, 1>(sh, kk, k, out_vals, out_idx);
+  else if (P <= 2u * kFinBS) sort_and_write<DT, 2>(sh, kk, k, out_vals, out_idx);
+  else sort_and_write<DT, 4>(sh, kk, k, out_vals, out_idx);
 }
 
 struct FinishArgs {
   const void* values;
   uint32_t n, k, k_req, M;
   int direct;
-  uint32_t G_f, C;
-  const uint32_t *blk_cnt, *blk_max, *reg_key, *reg_idx, *spill_key, *spill_idx;
+  uint32_t G_f, seg_cap;
+  const uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
   CallState* st;
   uint32_t G_fb, chunk;
   uint32_t *cand_key, *cand_idx, *cand_cnt;
@@ -452,19 +631,25 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   const uint32_t tid = threadIdx.x, b = blockIdx.x;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
   if (!a.direct) {
-    const uint32_t cnt = tid < a.G_f ? a.blk_cnt[tid] : 0u;
-    const uint32_t stored = min(cnt, a.C);
-    uint32_t R;
-    const uint32_t pre = block_excl_sum<kFinBS>(stored, sh.sel.wsum, &R);
-    if (tid < a.G_f) sh.pre[tid] = pre;
-    total = block_sum<kFinBS>(cnt, sh.sel.wsum);
+    if (tid < kSegs) sh.seg_n[tid] = a.seg_cnt[tid * kSegStride];
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t run = 0;
+      for (int x = 0; x < kSegs; ++x) {
+        sh.seg_pre[x] = run;
+        run += sh.seg_n[x];
+      }
+      sh.seg_pre[kSegs] = run;
+    }
+    __syncthreads();
+    total = sh.seg_pre[kSegs];
     status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
     if (status == PROFK_STATUS_FILTERED) {
       if (b != 0) return;
-      const uint32_t gmax = block_max<kFinBS>(cnt ? a.blk_max[tid] : 0u, sh.sel.wsum);
+      const uint32_t gmax = block_max<kFinBS>(tid < a.G_f ? a.blk_max[tid] : 0u, sh.sel.wsum);
       const uint32_t tau = a.st->tau_key;
-      RegionSrc src{a.reg_key, a.reg_idx, a.C, a.G_f, R, sh.pre, a.spill_key, a.spill_idx};
+      SegSrc src{a.seg_key, a.seg_idx, a.seg_cap, sh.seg_pre};
       const uint32_t kk = min(a.k, total);
       select_topk(src, total, kk, tau, max(gmax, tau), KB, sh);
       write_sorted<DT>(sh, kk, a.k, a.out_vals, a.out_idx);
@@ -507,7 +692,7 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   const uint32_t pre = block_excl_sum<kFinBS>(cc, sh.sel.wsum, &R);
   if (tid < gridDim.x) sh.pre[tid] = pre;
   __syncthreads();
-  RegionSrc src{a.cand_key, a.cand_idx, a.k, gridDim.x, R, sh.pre, nullptr, nullptr};
+  RegionSrc src{a.cand_key, a.cand_idx, a.k, gridDim.x, R, sh.pre};
   select_topk(src, R, a.k, 0u, key_max, KB, sh);
   write_sorted<DT>(sh, a.k, a.k, a.out_vals, a.out_idx);
   if (tid == 0) {
@@ -533,30 +718,30 @@ __global__ void k_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64
   }
 }
 
-// Gathers the regions and the spill list into one contiguous buffer.
-__global__ __launch_bounds__(1024) void k_gather_buffer(uint32_t G, uint32_t C, uint32_t cap,
-                                                        const uint32_t* blk_cnt,
-                                                        const uint32_t* reg_key, const uint32_t* reg_idx,
-                                                        const uint32_t* spill_key, const uint32_t* spill_idx,
-                                                        const CallState* st, uint32_t* out_key,
-                                                        uint32_t* out_idx, uint32_t* count) {
-  __shared__ uint32_t pre[1024];
-  __shared__ uint32_t wsum[20];
+// Gathers the candidate segments into one contiguous buffer.
+__global__ __launch_bounds__(1024) void k_gather_buffer(uint32_t cap, const uint32_t* seg_cnt,
+                                                        const uint32_t* seg_key, const uint32_t* seg_idx,
+                                                        uint32_t* out_key, uint32_t* out_idx, uint32_t* count) {
+  __shared__ uint32_t pre[kSegs + 1];
   const uint32_t tid = threadIdx.x;
-  const uint32_t cnt = tid < G ? blk_cnt[tid] : 0u;
-  uint32_t R;
-  const uint32_t p = block_excl_sum<1024>(min(cnt, C), wsum, &R);
-  if (tid < G) pre[tid] = p;
-  const uint32_t total = block_sum<1024>(cnt, wsum);
-  __syncthreads();
-  RegionSrc src{reg_key, reg_idx, C, G, R, pre, spill_key, spill_idx};
-  const uint32_t stored = min(total, cap);
-  for (uint32_t i = tid; i < stored; i += 1024) {
-    out_key[i] = src.get_key(i);
-    out_idx[i] = src.get_idx(i);
+  if (tid == 0) {
+    uint32_t run = 0;
+    for (int x = 0; x < kSegs; ++x) {
+      pre[x] = run;
+      run += min(seg_cnt[x * kSegStride], cap);
+    }
+    pre[kSegs] = run;
+    uint32_t total = 0;
+    for (int x = 0; x < kSegs; ++x) total += seg_cnt[x * kSegStride];
+    *count = total;
   }
-  if (tid == 0) *count = total;
-  (void)st;
+  __syncthreads();
+  SegSrc src{seg_key, seg_idx, cap, pre};
+  const uint32_t stored = min(pre[kSegs], cap);
+  src.visit<1024>(stored, nullptr, [&](uint32_t i, uint32_t key, auto idx) {
+    out_key[i] = key;
+    out_idx[i] = idx();
+  });
 }
 
 // ------------------------------------------------------------- host -------
@@ -576,9 +761,7 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   const uint32_t maxg = static_cast<uint32_t>(num_cus * 4 < kFiltMaxBlocks ? num_cus * 4 : kFiltMaxBlocks);
   uint32_t g = cdiv(cdiv(N, epv), kFiltBS * kFiltU);
   L.G_f = g < 1 ? 1 : (g > maxg ? maxg : g);
-  const uint64_t c = 64 + (2ull * M + L.G_f - 1) / L.G_f;
-  L.C = static_cast<uint32_t>(c < M ? c : M);
-  if (L.C < 1) L.C = 1;
+  L.seg_cap = M;
   const uint32_t fbmax = static_cast<uint32_t>(num_cus < kFbMaxBlocks ? num_cus : kFbMaxBlocks);
   uint32_t gb = cdiv(N, kFbMinChunk);
   L.G_fb = gb < 1 ? 1 : (gb > fbmax ? fbmax : gb);
@@ -586,13 +769,11 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
   L.off_state = take(sizeof(CallState));
+  L.off_segcnt = take(static_cast<size_t>(kSegs) * kSegStride * 4);
   L.off_union = take(static_cast<size_t>(L.G_s) * L.tcap * 4);
-  L.off_blk_cnt = take(static_cast<size_t>(L.G_f) * 4);
   L.off_blk_max = take(static_cast<size_t>(L.G_f) * 4);
-  L.off_reg_key = take(static_cast<size_t>(L.G_f) * L.C * 4);
-  L.off_reg_idx = take(static_cast<size_t>(L.G_f) * L.C * 4);
-  L.off_spill_key = take(static_cast<size_t>(M) * 4);
-  L.off_spill_idx = take(static_cast<size_t>(M) * 4);
+  L.off_seg_key = take(static_cast<size_t>(kSegs) * M * 4);
+  L.off_seg_idx = take(static_cast<size_t>(kSegs) * M * 4);
   L.off_cand_key = take(static_cast<size_t>(L.G_fb) * k * 4);
   L.off_cand_idx = take(static_cast<size_t>(L.G_fb) * k * 4);
   L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
@@ -602,8 +783,9 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
 
 template <class T> static T* at(uint8_t* ws, size_t off) { return reinterpret_cast<T*>(ws + off); }
 
+// union_keys null: the filter reads tau from the call state.
 template <int DT>
-static hipError_t launch_filter(const FlatCall& c, CallState* st) {
+static hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t* union_keys) {
   const FlatLayout& L = c.L;
   constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV;
   const uintptr_t addr = reinterpret_cast<uintptr_t>(c.values);
@@ -612,11 +794,13 @@ static hipError_t launch_filter(const FlatCall& c, CallState* st) {
   const uint32_t nvec = (c.n - head) / EPV;
   uint32_t vpb = cdiv(nvec, L.G_f);
   vpb = cdiv(vpb, kFiltBS) * kFiltBS;
-  FilterArgs fa{c.values, c.n, head, nvec, vpb, L.C, static_cast<uint32_t>(c.plan->M), st,
-                at<uint32_t>(c.ws, L.off_reg_key), at<uint32_t>(c.ws, L.off_reg_idx),
-                at<uint32_t>(c.ws, L.off_blk_cnt), at<uint32_t>(c.ws, L.off_blk_max),
-                at<uint32_t>(c.ws, L.off_spill_key), at<uint32_t>(c.ws, L.off_spill_idx)};
+  FilterArgs fa{c.values, c.n, head, nvec, vpb, L.seg_cap, st,
+                union_keys, union_keys ? L.union_n : 0u, static_cast<uint32_t>(c.plan->t),
+                at<uint32_t>(c.ws, L.off_segcnt), at<uint32_t>(c.ws, L.off_seg_key),
+                at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max)};
+  if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
   hipLaunchKernelGGL(k_filter<DT>, dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
   return hipGetLastError();
 }
 
@@ -625,24 +809,31 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   const FlatLayout& L = c.L;
   const profk_plan_t& p = *c.plan;
   CallState* st = at<CallState>(c.ws, L.off_state);
+  uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
   const bool direct = p.mode == PROFK_MODE_DIRECT && !c.use_tau;
+  const uint32_t* union_for_filter = nullptr;
   hipError_t e;
   if (direct || c.use_tau) {
-    hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, st, c.use_tau ? c.tau_key : 0u);
+    hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream,
+                       InitArgs{st, seg_cnt, c.use_tau ? c.tau_key : 0u});
   } else {
+    uint32_t* uk = at<uint32_t>(c.ws, L.off_union);
     SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
-                  L.tcap, at<uint32_t>(c.ws, L.off_union), st};
+                  L.tcap, uk, st, seg_cnt};
     hipLaunchKernelGGL(k_sample<DT>, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
-    TauArgs ta{at<uint32_t>(c.ws, L.off_union), L.union_n, static_cast<uint32_t>(p.t), Elem<DT>::KEYBITS, st};
-    hipLaunchKernelGGL(k_select_tau, dim3(1), dim3(kTauBS), 0, c.stream, ta);
+    if (L.union_n <= kFiltTauMax) {
+      union_for_filter = uk;
+    } else {
+      TauArgs ta{uk, L.union_n, static_cast<uint32_t>(p.t), Elem<DT>::KEYBITS, st};
+      hipLaunchKernelGGL(k_select_tau, dim3(1), dim3(kTauBS), 0, c.stream, ta);
+    }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (!direct && (e = launch_filter<DT>(c, st)) != hipSuccess) return e;
+  if (!direct && (e = launch_filter<DT>(c, st, union_for_filter)) != hipSuccess) return e;
   FinishArgs fa{c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
-                direct ? 1 : 0, L.G_f, L.C,
-                at<uint32_t>(c.ws, L.off_blk_cnt), at<uint32_t>(c.ws, L.off_blk_max),
-                at<uint32_t>(c.ws, L.off_reg_key), at<uint32_t>(c.ws, L.off_reg_idx),
-                at<uint32_t>(c.ws, L.off_spill_key), at<uint32_t>(c.ws, L.off_spill_idx), st,
+                direct ? 1 : 0, L.G_f, L.seg_cap,
+                seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
+                at<uint32_t>(c.ws, L.off_blk_max), st,
                 L.G_fb, L.chunk, at<uint32_t>(c.ws, L.off_cand_key), at<uint32_t>(c.ws, L.off_cand_idx),
                 at<uint32_t>(c.ws, L.off_cand_cnt), c.out_vals, c.out_idx, c.info};
   hipLaunchKernelGGL(k_finish<DT>, dim3(L.G_fb), dim3(kFinBS), 0, c.stream, fa);
@@ -664,13 +855,12 @@ hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* b
                                uint32_t* count_dev) {
   const FlatLayout& L = c.L;
   CallState* st = at<CallState>(c.ws, L.off_state);
-  hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, st, c.tau_key);
-  hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st) : launch_filter<1>(c, st);
+  uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
+  hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, InitArgs{st, seg_cnt, c.tau_key});
+  hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st, nullptr) : launch_filter<1>(c, st, nullptr);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_gather_buffer, dim3(1), dim3(1024), 0, c.stream, L.G_f, L.C,
-                     static_cast<uint32_t>(c.plan->M), at<uint32_t>(c.ws, L.off_blk_cnt),
-                     at<uint32_t>(c.ws, L.off_reg_key), at<uint32_t>(c.ws, L.off_reg_idx),
-                     at<uint32_t>(c.ws, L.off_spill_key), at<uint32_t>(c.ws, L.off_spill_idx), st,
+  hipLaunchKernelGGL(k_gather_buffer, dim3(1), dim3(1024), 0, c.stream, L.seg_cap, seg_cnt,
+                     at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
                      buf_key, buf_idx, count_dev);
   return hipGetLastError();
 }

@@ -13,19 +13,23 @@ namespace profk {
 // Per-call device state at the start of a workspace (256 bytes).
 struct CallState {
   uint32_t tau_key;    // threshold key (stage 2)
-  uint32_t spill_cnt;  // survivors that did not fit their block's region
   uint32_t ticket;     // last-block-done counter of the fallback
   uint32_t status;     // PROFK_STATUS_* of the call
-  uint32_t pad[60];
+  uint32_t pad[61];
 };
 
 // Launch geometry.
-constexpr int kSampBS = 1024;                 // threads of a sample block
+constexpr int kSampBS = 256;                  // threads of a sample block
 constexpr int kSampPerBlock = 4 * kSampBS;    // draws per sample block
+constexpr uint32_t kWaveTopMax = 32;          // largest t of the wave-level top-t
 constexpr int kTauBS = 1024;
 constexpr int kFiltBS = 256;                  // threads of a filter block
 constexpr int kFiltU = 8;                     // 16-byte loads in flight per lane
 constexpr int kFiltMaxBlocks = 1024;
+constexpr uint32_t kFiltTauMax = 2048;        // largest sample union a filter block selects from
+constexpr uint32_t kStage = 1024;             // survivors a filter block stages in LDS
+constexpr int kSegs = 8;                      // candidate segments (one counter each)
+constexpr int kSegStride = 64;                // words between segment counters
 constexpr int kFinBS = 1024;
 constexpr int kFinMaxK = 4096;                // largest k of the one-block refinement
 constexpr int kFbMaxBlocks = 256;
@@ -34,10 +38,11 @@ constexpr uint32_t kFbMinChunk = 8192;
 // Workspace layout of one flat (vector) call.
 struct FlatLayout {
   uint32_t G_s = 0, tcap = 0, union_n = 0;    // sampling
-  uint32_t G_f = 0, C = 0;                    // filter blocks, region capacity
+  uint32_t G_f = 0;                           // filter blocks
+  uint32_t seg_cap = 0;                       // entries per candidate segment (= M)
   uint32_t G_fb = 0, chunk = 0;               // fallback blocks, elements each
-  size_t off_state = 0, off_union = 0, off_blk_cnt = 0, off_blk_max = 0;
-  size_t off_reg_key = 0, off_reg_idx = 0, off_spill_key = 0, off_spill_idx = 0;
+  size_t off_state = 0, off_segcnt = 0, off_union = 0, off_blk_max = 0;
+  size_t off_seg_key = 0, off_seg_idx = 0;
   size_t off_cand_key = 0, off_cand_idx = 0, off_cand_cnt = 0;
   size_t bytes = 0;
 };
@@ -59,6 +64,7 @@ struct FlatCall {
   profk_info_t* info;
   int use_tau;          // 1: threshold given by the caller
   uint32_t tau_key;
+  hipEvent_t ev_before = nullptr, ev_after = nullptr;  // around the filter launch
 };
 
 hipError_t launch_flat(const FlatCall& c);
