@@ -135,7 +135,10 @@ int profk_topk_simple(const float* values, int64_t N, int64_t k, uint64_t seed,
  * draws its own sample (Philox counter word 1 = r) and falls back on its
  * own.  out_vals[B, k] and out_idx[B, k] (column indices) are contiguous.
  * `row_plan` comes from profk_plan_rows(D, k, ...).  info_dev is NULL or an
- * array of B reports. */
+ * array of B reports.  One workgroup handles a row entirely in LDS, so `ws`
+ * is not used (NULL, 0 are accepted).  Limits: k <= 1024 and a plan whose
+ * sample and buffer fit the row block's LDS (4*max(S, M) + 4*M bytes plus
+ * about 9 KiB within 144 KiB; PROFK_EINVAL otherwise). */
 int profk_topk_rows(const profk_plan_t* row_plan, int32_t dtype,
                     const void* values, int64_t B, int64_t D,
                     int64_t row_stride, int64_t k, uint64_t seed,

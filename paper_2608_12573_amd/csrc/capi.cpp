@@ -93,7 +93,8 @@ int profk_plan_rows(int64_t D, int64_t k, double eps, double recall, const profk
 }
 
 size_t profk_workspace_size(const profk_plan_t* plan, int32_t dtype, int64_t batch) {
-  if (!plan || !dtype_ok(dtype) || !plan_consistent(plan) || batch != 1) return 0;
+  if (!plan || !dtype_ok(dtype) || !plan_consistent(plan) || batch < 1) return 0;
+  if (batch > 1) return 256;  // the per-row kernel keeps everything in LDS
   return profk::flat_layout(*plan, dtype, profk::device_cu_count()).bytes;
 }
 
@@ -120,9 +121,24 @@ int profk_batchtopk(const profk_plan_t* plan, int32_t dtype, const void* values,
                   stream, info_dev, 0, 0);
 }
 
-int profk_topk_rows(const profk_plan_t*, int32_t, const void*, int64_t, int64_t, int64_t, int64_t,
-                    uint64_t, void*, int64_t*, void*, size_t, void*, profk_info_t*) {
-  return PROFK_EINVAL;
+int profk_topk_rows(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t B, int64_t D,
+                    int64_t row_stride, int64_t k, uint64_t seed, void* out_vals, int64_t* out_idx,
+                    void* ws, size_t ws_bytes, void* stream, profk_info_t* info_dev) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!plan || !values || !out_vals || !out_idx) return PROFK_ENULL;
+  if (!dtype_ok(dtype)) return PROFK_EDTYPE;
+  if (!plan_consistent(plan) || plan->N != D || plan->k != k) return PROFK_EINVAL;
+  if (B < 1 || B > static_cast<int64_t>(INT32_MAX) || row_stride < D || k > profk::kRowMaxK)
+    return PROFK_EINVAL;
+  if (reinterpret_cast<uintptr_t>(values) % elem_size(dtype) != 0) return PROFK_EINVAL;
+  const profk::RowLayout L = profk::row_layout(*plan);
+  if (L.bytes > profk::kRowMaxLds) return PROFK_EINVAL;
+  profk::RowCall c{plan, dtype, values, static_cast<uint32_t>(B), static_cast<uint32_t>(D),
+                   static_cast<uint32_t>(k), static_cast<uint64_t>(row_stride), seed, out_vals, out_idx,
+                   info_dev, L, static_cast<hipStream_t>(stream)};
+  const hipError_t e = profk::launch_rows(c);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
 }
 
 int profk_debug_sample_indices(uint64_t seed, int64_t row, int64_t S, int64_t N, int64_t* out_dev,

@@ -177,10 +177,17 @@ __device__ __forceinline__ void for_items(uint32_t n, Load load, Body body) {
 constexpr int kSelBins = 2048;
 constexpr int kSelDigit = 11;
 
+// Scratch of the block reductions and digit search.
+struct SelectScratch {
+  uint32_t wsum[20];
+  uint32_t found[4];
+};
+
 struct alignas(16) SelectShared {
   uint32_t hist[kSelBins];
   uint32_t wsum[20];
   uint32_t found[4];
+  __device__ __forceinline__ SelectScratch& scratch() { return *reinterpret_cast<SelectScratch*>(wsum); }
 };
 
 struct SelectResult {
@@ -201,7 +208,7 @@ struct SelectResult {
 template <int BS, int DIGIT, class Visit>
 __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t kk, int nbits,
                                                          uint32_t prefix, uint32_t* hist,
-                                                         SelectShared& sh) {
+                                                         SelectScratch& sh) {
   static_assert(DIGIT >= 8 && DIGIT <= 13, "digit width");
   const uint32_t tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -297,7 +304,7 @@ __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t k
 template <int BS, class Visit>
 __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t kk, int nbits,
                                                          uint32_t prefix, SelectShared& sh) {
-  return block_select_kth<BS, kSelDigit>(visit, kk, nbits, prefix, sh.hist, sh);
+  return block_select_kth<BS, kSelDigit>(visit, kk, nbits, prefix, sh.hist, sh.scratch());
 }
 
 // Top-t of up to 64*E keys held by one wave (E per lane, `valid` bits mark

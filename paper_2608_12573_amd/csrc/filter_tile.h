@@ -1,0 +1,120 @@
+// The filter test of Sec. 3 stage 3 on one tile of 16-byte vectors held in
+// registers, shared by the vector and per-row filter kernels.
+//
+// Survival test on a transformed word: for a threshold whose pattern is
+// non-negative, key(x) >= key(tau) iff bits(x) >= bits(tau) as signed
+// integers; for a negative one, iff bits(x) <= bits(tau) as unsigned, which
+// is the signed test on bits ^ 0x7FFFFFFF.  So every element costs one XOR
+// and one signed compare (bf16: the same per 16-bit half, two per word).
+#pragma once
+
+#include <climits>
+
+#include "device_common.h"
+
+namespace profk {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+template <int DT> struct Elem;
+template <> struct Elem<0> { static constexpr int EPV = 4, ES = 4, KEYBITS = 32; };
+template <> struct Elem<1> { static constexpr int EPV = 8, ES = 2, KEYBITS = 16; };
+
+// The transformed threshold of a key: survive iff transform(word) >= thr.
+template <int DT>
+struct Thresh {
+  uint32_t flip;
+  int thr;
+  uint32_t neutral;  // a word that fails the fast test unless every word passes
+  __device__ __forceinline__ explicit Thresh(uint32_t tau) {
+    if (DT == 0) {
+      const uint32_t tb = bits_from_key_f32(tau);
+      flip = (tb >> 31) ? 0x7FFFFFFFu : 0u;
+      thr = static_cast<int>(tb ^ flip);
+      neutral = 0x80000000u ^ flip;
+    } else {
+      const uint32_t tb = bits_from_key_bf16(tau);
+      const uint32_t f16 = (tb & 0x8000u) ? 0x7FFFu : 0u;
+      flip = f16 | (f16 << 16);
+      thr = static_cast<int>(static_cast<int16_t>(static_cast<uint16_t>(tb ^ f16)));
+      neutral = (0x8000u * 0x10001u) ^ flip;
+    }
+  }
+};
+
+// Fast test: does any element of the lane's tile survive?
+template <int DT, int U>
+__device__ __forceinline__ bool tile_any(const u32x4 (&v)[U], const Thresh<DT>& th) {
+  int mx;
+  if (DT == 0) {
+    mx = INT_MIN;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mx = max(mx, static_cast<int>(v[u][e] ^ th.flip));
+  } else {
+    s16x2 m2 = s16x2{SHRT_MIN, SHRT_MIN};
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(s16x2, v[u][e] ^ th.flip));
+    mx = max(static_cast<int>(m2.x), static_cast<int>(m2.y));
+  }
+  return mx >= th.thr;
+}
+
+// Exact pass over a lane's tile.  Vector u of the lane is tile vector
+// vb + u*BS + lane_pos, valid when below vend; element e of a vector is
+// input element base + vector*EPV + e.  count() returns the lane's survivor
+// count; emit(f) calls f(key, index) for each survivor in element order.
+template <int DT, int U, int BS>
+struct TileExact {
+  const u32x4 (&v)[U];
+  const Thresh<DT>& th;
+  uint32_t vb, vend, pos, base;
+
+  __device__ __forceinline__ uint32_t count() const {
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool valid = vb + u * BS + pos < vend;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t w = v[u][e] ^ th.flip;
+        if (DT == 0) {
+          cnt += (valid && static_cast<int>(w) >= th.thr) ? 1u : 0u;
+        } else {
+          cnt += (valid && (static_cast<int>(w << 16) >> 16) >= th.thr) ? 1u : 0u;
+          cnt += (valid && (static_cast<int>(w) >> 16) >= th.thr) ? 1u : 0u;
+        }
+      }
+    }
+    return cnt;
+  }
+
+  template <class F>
+  __device__ __forceinline__ void emit(F f) const {
+    constexpr int EPV = Elem<DT>::EPV;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t vi = vb + u * BS + pos;
+      const bool valid = vi < vend;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t raw = v[u][e];
+        const uint32_t w = raw ^ th.flip;
+        if (DT == 0) {
+          if (valid && static_cast<int>(w) >= th.thr) f(key_f32(raw), base + vi * EPV + e);
+        } else {
+          if (valid && (static_cast<int>(w << 16) >> 16) >= th.thr)
+            f(key_bf16(raw & 0xFFFFu), base + vi * EPV + 2 * e);
+          if (valid && (static_cast<int>(w) >> 16) >= th.thr)
+            f(key_bf16(raw >> 16), base + vi * EPV + 2 * e + 1);
+        }
+      }
+    }
+  }
+};
+
+}  // namespace profk

@@ -20,16 +20,11 @@
 #include <climits>
 
 #include "device_common.h"
+#include "filter_tile.h"
 #include "launch.h"
+#include "topk_block.h"
 
 namespace profk {
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef short s16x2 __attribute__((ext_vector_type(2)));
-
-template <int DT> struct Elem;
-template <> struct Elem<0> { static constexpr int EPV = 4, ES = 4, KEYBITS = 32; };
-template <> struct Elem<1> { static constexpr int EPV = 8, ES = 2, KEYBITS = 16; };
 
 __device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt) {
   if (threadIdx.x < kSegs) seg_cnt[threadIdx.x * kSegStride] = 0;
@@ -177,11 +172,7 @@ struct FilterArgs {
   uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
 };
 
-// Survival test on a transformed word: for a threshold whose pattern is
-// non-negative, key(x) >= key(tau) iff bits(x) >= bits(tau) as signed
-// integers; for a negative one, iff bits(x) <= bits(tau) as unsigned, which
-// is the signed test on bits ^ 0x7FFFFFFF.  So every element costs one XOR
-// and one signed compare (bf16: the same per 16-bit half).
+// The filter pass; the survival test is in filter_tile.h.
 template <int DT>
 __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   constexpr int EPV = Elem<DT>::EPV;
@@ -248,20 +239,7 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     tau = a.st->tau_key;
   }
 
-  uint32_t flip;
-  int thr;
-  if (DT == 0) {
-    const uint32_t tb = bits_from_key_f32(tau);
-    flip = (tb >> 31) ? 0x7FFFFFFFu : 0u;
-    thr = static_cast<int>(tb ^ flip);
-  } else {
-    const uint32_t tb = bits_from_key_bf16(tau);
-    const uint32_t f16 = (tb & 0x8000u) ? 0x7FFFu : 0u;
-    flip = f16 | (f16 << 16);
-    thr = static_cast<int>(static_cast<int16_t>(static_cast<uint16_t>(tb ^ f16)));
-  }
-  // a vector that can never pass the fast test unless every element survives
-  const uint32_t neutral = DT == 0 ? (0x80000000u ^ flip) : ((0x8000u * 0x10001u) ^ flip);
+  const Thresh<DT> th(tau);
   __syncthreads();
 
   uint32_t* const seg_counter = a.seg_cnt + seg * kSegStride;
@@ -310,68 +288,14 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     for (int u = 0; u < kFiltU; ++u) {
       const uint32_t vi = vb + u * kFiltBS + tid;
       if (vi < vend) v[u] = __builtin_nontemporal_load(vec + vi);
-      else v[u] = u32x4{neutral, neutral, neutral, neutral};
+      else v[u] = u32x4{th.neutral, th.neutral, th.neutral, th.neutral};
     }
-    int mx;
-    if (DT == 0) {
-      mx = INT_MIN;
-#pragma unroll
-      for (int u = 0; u < kFiltU; ++u)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) mx = max(mx, static_cast<int>(v[u][e] ^ flip));
-    } else {
-      s16x2 m2 = s16x2{SHRT_MIN, SHRT_MIN};
-#pragma unroll
-      for (int u = 0; u < kFiltU; ++u)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(s16x2, v[u][e] ^ flip));
-      mx = max(static_cast<int>(m2.x), static_cast<int>(m2.y));
-    }
-    if (__ballot(mx >= thr) == 0) continue;
-
+    if (__ballot(tile_any<DT, kFiltU>(v, th)) == 0) continue;
     // Rare path: exact per-element test, one slot reservation per wave.
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int u = 0; u < kFiltU; ++u) {
-      const bool valid = vb + u * kFiltBS + tid < vend;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t w = v[u][e] ^ flip;
-        if (DT == 0) {
-          cnt += (valid && static_cast<int>(w) >= thr) ? 1u : 0u;
-        } else {
-          cnt += (valid && (static_cast<int>(w << 16) >> 16) >= thr) ? 1u : 0u;
-          cnt += (valid && (static_cast<int>(w) >> 16) >= thr) ? 1u : 0u;
-        }
-      }
-    }
+    const TileExact<DT, kFiltU, kFiltBS> tx{v, th, vb, vend, tid, a.head};
     uint32_t slot, first_over, gbase;
-    reserve(cnt, slot, first_over, gbase);
-#pragma unroll
-    for (int u = 0; u < kFiltU; ++u) {
-      const uint32_t vi = vb + u * kFiltBS + tid;
-      const bool valid = vi < vend;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t raw = v[u][e];
-        const uint32_t w = raw ^ flip;
-        if (DT == 0) {
-          if (valid && static_cast<int>(w) >= thr) {
-            store(slot, first_over, gbase, key_f32(raw), a.head + vi * EPV + e);
-            ++slot;
-          }
-        } else {
-          if (valid && (static_cast<int>(w << 16) >> 16) >= thr) {
-            store(slot, first_over, gbase, key_bf16(raw & 0xFFFFu), a.head + vi * EPV + 2 * e);
-            ++slot;
-          }
-          if (valid && (static_cast<int>(w) >> 16) >= thr) {
-            store(slot, first_over, gbase, key_bf16(raw >> 16), a.head + vi * EPV + 2 * e + 1);
-            ++slot;
-          }
-        }
-      }
-    }
+    reserve(tx.count(), slot, first_over, gbase);
+    tx.emit([&](uint32_t key, uint32_t idx) { store(slot++, first_over, gbase, key, idx); });
   }
 
   // Elements before the first aligned vector and after the last one.
@@ -385,6 +309,7 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
       key = key_of<DT>(load_raw<DT>(a.values, idx));
       ok = key >= tau;
     }
+    (void)EPV;
     if (__ballot(ok)) {
       uint32_t slot, first_over, gbase;
       reserve(ok ? 1u : 0u, slot, first_over, gbase);
@@ -417,25 +342,18 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
 
 // ------------------------------------------------------------ stage 4 -----
 constexpr uint32_t kFinCache = 28672;
+constexpr int kFinDigit = 12;
 
 struct FinShared {
   uint32_t cache[kFinCache];       // candidate keys; later the sort's exchange buffers
-  uint64_t sortbuf[kFinMaxK];
+  uint64_t sortbuf[kFinMaxK];      // radix histogram, then the collected top k
   uint32_t pre[1024];
-  SelectShared sel;
+  SelectScratch sel;
   uint32_t seg_n[kSegs], seg_pre[kSegs + 1];
   uint32_t misc[8];
-};
-
-// Index accessors handed to candidate visitors: an index is loaded only
-// when a visitor asks for it.
-struct LoadIdx {
-  const uint32_t* p;
-  __device__ __forceinline__ uint32_t operator()() const { return *p; }
-};
-struct PosIdx {
-  uint32_t v;
-  __device__ __forceinline__ uint32_t operator()() const { return v; }
+  __device__ __forceinline__ TopkSmem topk() {
+    return TopkSmem{cache, kFinCache, reinterpret_cast<uint32_t*>(sortbuf), sortbuf, &sel, &misc[0]};
+  }
 };
 
 // The filter's candidates: segment x holds n_x entries at x*cap; candidate i
@@ -498,117 +416,6 @@ struct RegionSrc {
   }
 };
 
-// A contiguous range of the input, keys computed on the fly.
-template <int DT>
-struct InputSrc {
-  const void* values;
-  uint32_t lo;
-  template <int BS, class F>
-  __device__ __forceinline__ void visit(uint32_t n, const uint32_t* cache, F f) const {
-    for_items<BS, 8>(n, [&](uint32_t i) { return cache ? cache[i] : key_of<DT>(load_raw<DT>(values, lo + i)); },
-                     [&](uint32_t i, uint32_t v) { f(i, v, PosIdx{lo + i}); });
-  }
-  __device__ __forceinline__ uint32_t idx_at(uint32_t i) const { return lo + i; }
-};
-
-// Exact top-kk (kk <= kFinMaxK, kk <= n) of a candidate set under the total
-// order, collected unsorted into sh.sortbuf[0..kk).  Every candidate key lies
-// in [lo_key, hi_key].  The radix histogram (12-bit digits) borrows the sort
-// buffer; the collection first reserves slots for (key, candidate number)
-// and then loads all selected indices at once.
-template <class Src>
-__device__ __forceinline__ void select_topk(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
-                                            uint32_t hi_key, int keybits, FinShared& sh) {
-  constexpr int kDigit = 12;
-  uint32_t* const hist = reinterpret_cast<uint32_t*>(sh.sortbuf);
-  const uint32_t tid = threadIdx.x;
-  const bool cached = n <= kFinCache;
-  if (cached) {
-    src.template visit<kFinBS>(n, nullptr, [&](uint32_t i, uint32_t key, auto) { sh.cache[i] = key; });
-    __syncthreads();
-  }
-  const uint32_t* cache = cached ? sh.cache : nullptr;
-  auto keys_only = [&](auto f) {
-    if (cached) {
-      for (uint32_t i = tid; i < n; i += kFinBS) f(sh.cache[i]);
-    } else {
-      src.template visit<kFinBS>(n, nullptr, [&](uint32_t, uint32_t key, auto) { f(key); });
-    }
-  };
-  const int shared = shared_prefix_bits(lo_key, hi_key, keybits);
-  const SelectResult r =
-      block_select_kth<kFinBS, kDigit>(keys_only, kk, keybits - shared, lo_key, hist, sh.sel);
-  const uint32_t kstar = r.kth;
-  const uint32_t krem = kk - r.above;
-  const bool cut = krem < r.equal;
-  uint32_t istar = 0xFFFFFFFFu;
-  if (cut) {
-    // the krem smallest indices among the ties at kstar
-    const SelectResult ri = block_select_kth<kFinBS, kDigit>(
-        [&](auto f) {
-          src.template visit<kFinBS>(n, cache, [&](uint32_t, uint32_t key, auto idx) {
-            if (key == kstar) f(~idx());
-          });
-        },
-        krem, 32, 0u, hist, sh.sel);
-    istar = ~ri.kth;
-  }
-  if (tid == 0) sh.misc[0] = 0;
-  __syncthreads();
-  src.template visit<kFinBS>(n, cache, [&](uint32_t i, uint32_t key, auto idx) {
-    if (key > kstar || (key == kstar && (!cut || idx() <= istar))) {
-      const uint32_t p = atomicAdd(&sh.misc[0], 1u);
-      if (p < kFinMaxK) sh.sortbuf[p] = (static_cast<uint64_t>(key) << 32) | i;
-    }
-  });
-  __syncthreads();
-  for (uint32_t p = tid; p < kk; p += kFinBS) {
-    const uint64_t e = sh.sortbuf[p];
-    sh.sortbuf[p] = composite(static_cast<uint32_t>(e >> 32), src.idx_at(static_cast<uint32_t>(e)));
-  }
-  __syncthreads();
-}
-
-template <int DT, int E>
-__device__ __forceinline__ void sort_and_write(FinShared& sh, uint32_t kk, uint32_t k, void* out_vals,
-                                               int64_t* out_idx) {
-  const uint32_t tid = threadIdx.x;
-  uint64_t v[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const uint32_t p = static_cast<uint32_t>(e) * kFinBS + tid;
-    v[e] = p < kk ? sh.sortbuf[p] : 0ull;
-  }
-  bitonic_sort_regs_desc<kFinBS, E>(v, reinterpret_cast<uint64_t*>(sh.cache));
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const uint32_t p = static_cast<uint32_t>(e) * kFinBS + tid;
-    if (p >= k) continue;
-    uint32_t bits;
-    int64_t id;
-    if (p < kk) {
-      bits = bits_of_key<DT>(comp_key(v[e]));
-      id = comp_idx(v[e]);
-    } else {
-      bits = DT == 0 ? 0xFF800000u : 0xFF80u;  // -inf padding (relaxed recall)
-      id = -1;
-    }
-    if (DT == 0) static_cast<uint32_t*>(out_vals)[p] = bits;
-    else static_cast<uint16_t*>(out_vals)[p] = static_cast<uint16_t>(bits);
-    out_idx[p] = id;
-  }
-}
-
-// Sorts the kk collected candidates and writes the k outputs.
-template <int DT>
-__device__ __forceinline__ void write_sorted(FinShared& sh, uint32_t kk, uint32_t k, void* out_vals,
-                                             int64_t* out_idx) {
-  const uint32_t P = next_pow2(max(kk, k));
-  if (P <= static_cast<uint32_t>(kFinBS)) sort_and_write<DT, 1>(sh, kk, k, out_vals, out_idx);
-  else if (P <= 2u * kFinBS) sort_and_write<DT, 2>(sh, kk, k, out_vals, out_idx);
-  else sort_and_write<DT, 4>(sh, kk, k, out_vals, out_idx);
-}
-
 struct FinishArgs {
   const void* values;
   uint32_t n, k, k_req, M;
@@ -651,8 +458,9 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
       const uint32_t tau = a.st->tau_key;
       SegSrc src{a.seg_key, a.seg_idx, a.seg_cap, sh.seg_pre};
       const uint32_t kk = min(a.k, total);
-      select_topk(src, total, kk, tau, max(gmax, tau), KB, sh);
-      write_sorted<DT>(sh, kk, a.k, a.out_vals, a.out_idx);
+      block_topk<kFinBS, kFinDigit>(src, total, kk, tau, max(gmax, tau), KB, sh.topk());
+      sort_write_any<DT, kFinBS>(sh.sortbuf, kk, a.k, reinterpret_cast<uint64_t*>(sh.cache), a.out_vals,
+                                 a.out_idx);
       if (tid == 0) {
         a.st->status = status;
         if (a.info) {
@@ -672,7 +480,7 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   const uint32_t kb = min(a.k, nb);
   if (kb) {
     InputSrc<DT> src{a.values, lo};
-    select_topk(src, nb, kb, 0u, key_max, KB, sh);
+    block_topk<kFinBS, kFinDigit>(src, nb, kb, 0u, key_max, KB, sh.topk());
     for (uint32_t i = tid; i < kb; i += kFinBS) {
       const uint64_t c = sh.sortbuf[i];
       a.cand_key[static_cast<size_t>(b) * a.k + i] = comp_key(c);
@@ -693,8 +501,8 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   if (tid < gridDim.x) sh.pre[tid] = pre;
   __syncthreads();
   RegionSrc src{a.cand_key, a.cand_idx, a.k, gridDim.x, R, sh.pre};
-  select_topk(src, R, a.k, 0u, key_max, KB, sh);
-  write_sorted<DT>(sh, a.k, a.k, a.out_vals, a.out_idx);
+  block_topk<kFinBS, kFinDigit>(src, R, a.k, 0u, key_max, KB, sh.topk());
+  sort_write_any<DT, kFinBS>(sh.sortbuf, a.k, a.k, reinterpret_cast<uint64_t*>(sh.cache), a.out_vals, a.out_idx);
   if (tid == 0) {
     a.st->status = status;
     if (a.info) {

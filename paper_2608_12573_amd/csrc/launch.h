@@ -69,6 +69,37 @@ struct FlatCall {
 
 hipError_t launch_flat(const FlatCall& c);
 
+// Per-row kernel: one workgroup per row, everything in LDS.
+constexpr int kRowBS = 256;                   // threads of a row block
+constexpr int kRowU = 8;                      // 16-byte loads in flight per lane
+constexpr uint32_t kRowWaveSample = 4096;     // largest S of the wave-level threshold
+constexpr int kRowMaxK = 4 * kRowBS;          // largest k per row
+constexpr uint32_t kRowMaxLds = 144 * 1024;   // dynamic LDS the row layout may use
+
+// Dynamic LDS of a row block: region a holds the sample keys and then the
+// buffer keys (and, last, the sort exchange), region b the buffer indices.
+struct RowLayout {
+  uint32_t off_a = 0, off_b = 0, off_hist = 0, off_collect = 0, bytes = 0;
+};
+
+RowLayout row_layout(const profk_plan_t& plan);
+
+struct RowCall {
+  const profk_plan_t* plan;
+  int dtype;
+  const void* values;
+  uint32_t B, D, k;
+  uint64_t row_stride;
+  uint64_t seed;
+  void* out_vals;
+  int64_t* out_idx;
+  profk_info_t* info;
+  RowLayout L;
+  hipStream_t stream;
+};
+
+hipError_t launch_rows(const RowCall& c);
+
 // Inspection helpers.
 hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t N,
                                  int64_t* out, hipStream_t s);
