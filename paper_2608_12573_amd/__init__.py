@@ -57,11 +57,21 @@ _lib = None
 
 
 def lib():
-    """The loaded libprofk.so; raises when it has not been built."""
+    """The loaded libprofk.so; raises when it has not been built.
+
+    PyTorch-ROCm ships its own HIP runtime.  Importing torch first makes the
+    library's libamdhip64.so.7 dependency resolve to that same runtime (by
+    soname), so tensors, streams and our kernels share one HIP instance;
+    loading the library first would bring in a second runtime whose launches
+    cannot use torch's streams."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise ProfkError(f"{LIB_PATH} is missing: run paper_2608_12573_amd.build.build() first")
+        try:
+            import torch  # noqa: F401  (see the docstring)
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         vp, i32, i64, u32, u64, dbl = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                                        ctypes.c_uint32, ctypes.c_uint64, ctypes.c_double)

@@ -39,7 +39,6 @@ int check_flat(const profk_plan_t* plan, int32_t dtype, const void* values, int6
   if (!plan || !values || !out_vals || !out_idx || !ws) return PROFK_ENULL;
   if (!dtype_ok(dtype)) return PROFK_EDTYPE;
   if (!plan_consistent(plan) || plan->N != N || plan->k != k) return PROFK_EINVAL;
-  if (k > profk::kFinMaxK) return PROFK_EINVAL;
   if (reinterpret_cast<uintptr_t>(values) % elem_size(dtype) != 0) return PROFK_EINVAL;
   *L = profk::flat_layout(*plan, dtype, profk::device_cu_count());
   if (ws_bytes < L->bytes) return PROFK_EWORKSPACE;

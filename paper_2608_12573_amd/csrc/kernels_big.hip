@@ -1,0 +1,472 @@
+// Refinement and fallback for k above what one workgroup can hold (the
+// BatchTopK case of Sec. 5: K = B*k of a flattened latent matrix).
+//
+// Same result as the one-block path -- the exact top-k under the total
+// order, sorted -- computed across the GPU:
+//   k_big_begin    status from the candidate counts; the source is the
+//                  candidate segments, or the whole input on fallback.
+//   k_big_pass     one radix digit per launch: block histograms are merged
+//                  into a global histogram and the last block (ticket) picks
+//                  the digit holding rank k.  Key digits first, then, if the
+//                  tie class at the k-th key is split, digits of ~index.
+//   k_big_collect  every item of the top k, as a composite key, into a
+//                  staging array (one atomic per block).
+//   k_big_tile     sorts tiles of 4096 composites in LDS.
+//   k_big_merge    merge-path passes doubling the sorted run length.
+//   k_big_write    values, indices and the per-call report.
+#include "device_common.h"
+#include "filter_tile.h"
+#include "launch.h"
+
+namespace profk {
+
+struct BigState {
+  uint32_t status;     // PROFK_STATUS_* of the call
+  uint32_t n_src;      // items in the source
+  uint32_t from_input; // 1: the source is the input itself
+  uint32_t kk;         // how many to select
+  uint32_t total;      // filter survivors
+  uint32_t tau;
+  // key stage
+  uint32_t prefix, krem, above, equal;
+  int32_t hi;
+  uint32_t kstar;
+  // index stage (on ~index among keys equal to kstar)
+  uint32_t cut;
+  uint32_t iprefix, ikrem;
+  int32_t ihi;
+  uint32_t istar;
+  uint32_t ticket;
+  uint32_t out_count;
+  uint32_t pad[45];
+};
+static_assert(sizeof(BigState) <= 256, "state size");
+
+struct BigArgs {
+  const void* values;
+  uint32_t n, k, k_req, M;
+  int direct;
+  const uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
+  uint32_t seg_cap, G_f;
+  const CallState* st;
+  BigState* bs;
+  uint32_t* ghist;     // kBigBins
+  uint64_t* staging;   // P
+  uint64_t* runs;      // P
+  uint32_t P;          // padded length: k rounded up to kBigTile
+  void* out_vals;
+  int64_t* out_idx;
+  profk_info_t* info;
+};
+
+// Candidate i of the segments: segment x holds n_x entries at x*cap.
+struct SegPos {
+  const uint32_t* n;  // kSegs counts (already capped)
+  uint32_t cap;
+  __device__ __forceinline__ size_t operator()(uint32_t i) const {
+    uint32_t x = 0, base = 0;
+#pragma unroll
+    for (int j = 0; j < kSegs - 1; ++j) {
+      if (x == static_cast<uint32_t>(j) && i >= base + n[j]) { base += n[j]; ++x; }
+    }
+    return static_cast<size_t>(x) * cap + (i - base);
+  }
+};
+
+// Grid-stride visit of the call's source: f(key, index) for every item.
+template <int DT, int BS, class F>
+__device__ __forceinline__ void big_visit(const BigArgs& a, const BigState& s, const uint32_t* segn, F f) {
+  const uint32_t n = s.n_src;
+  const uint32_t stride = gridDim.x * BS * 8;
+  if (s.from_input) {
+    for (uint32_t base = blockIdx.x * BS * 8; base < n; base += stride) {
+      uint32_t kv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = base + u * BS + threadIdx.x;
+        kv[u] = i < n ? key_of<DT>(load_raw<DT>(a.values, i)) : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = base + u * BS + threadIdx.x;
+        if (i < n) f(kv[u], i);
+      }
+    }
+  } else {
+    const SegPos pos{segn, a.seg_cap};
+    for (uint32_t base = blockIdx.x * BS * 8; base < n; base += stride) {
+      uint32_t kv[8], iv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = base + u * BS + threadIdx.x;
+        if (i < n) {
+          const size_t p = pos(i);
+          kv[u] = a.seg_key[p];
+          iv[u] = a.seg_idx[p];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = base + u * BS + threadIdx.x;
+        if (i < n) f(kv[u], iv[u]);
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void load_segn(const BigArgs& a, uint32_t* segn) {
+  if (threadIdx.x < kSegs) segn[threadIdx.x] = min(a.seg_cnt[threadIdx.x * kSegStride], a.seg_cap);
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- begin ---
+template <int DT>
+__global__ __launch_bounds__(1024) void k_big_begin(BigArgs a) {
+  constexpr int KB = Elem<DT>::KEYBITS;
+  __shared__ uint32_t wsum[20];
+  __shared__ uint32_t s_total;
+  const uint32_t tid = threadIdx.x;
+  BigState* s = a.bs;
+  for (uint32_t i = tid; i < kBigBins; i += 1024) a.ghist[i] = 0;
+  uint32_t status = PROFK_STATUS_DIRECT, total = 0;
+  if (!a.direct) {
+    if (tid == 0) {
+      uint32_t t = 0;
+      for (int x = 0; x < kSegs; ++x) t += a.seg_cnt[x * kSegStride];
+      s_total = t;
+    }
+    __syncthreads();
+    total = s_total;
+    status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
+                             : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
+  }
+  const uint32_t key_max = KB == 32 ? 0xFFFFFFFFu : 0xFFFFu;
+  uint32_t lo = 0, hi = key_max;
+  if (status == PROFK_STATUS_FILTERED) {
+    lo = a.st->tau_key;
+    hi = max(lo, block_max<1024>(tid < a.G_f ? a.blk_max[tid] : 0u, wsum));
+  }
+  if (tid == 0) {
+    const bool filtered = status == PROFK_STATUS_FILTERED;
+    s->status = status;
+    s->total = total;
+    s->tau = a.direct ? 0u : a.st->tau_key;
+    s->from_input = filtered ? 0u : 1u;
+    s->n_src = filtered ? total : a.n;
+    s->kk = filtered ? min(a.k, total) : a.k;
+    s->prefix = lo;
+    s->krem = s->kk;
+    s->above = 0;
+    s->equal = 0;
+    s->hi = KB - shared_prefix_bits(lo, hi, KB);
+    s->kstar = lo;
+    s->cut = 0;
+    s->iprefix = 0;
+    s->ikrem = 0;
+    s->ihi = 0;
+    s->istar = 0xFFFFFFFFu;
+    s->ticket = 0;
+    s->out_count = 0;
+    if (s->hi == 0) {
+      // every candidate carries the same key: only the index cut is left
+      s->equal = s->n_src;
+      if (s->kk < s->n_src) {
+        s->cut = 1;
+        s->ikrem = s->kk;
+        s->ihi = 32;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ one digit ---
+// STAGE 0: a digit of the key; STAGE 1: a digit of ~index among the items
+// whose key is kstar.
+template <int DT, int STAGE>
+__global__ __launch_bounds__(kBigBS) void k_big_pass(BigArgs a) {
+  constexpr int NB = 1 << kBigDigit;
+  __shared__ uint32_t hist[NB];
+  __shared__ uint32_t segn[kSegs];
+  __shared__ uint32_t wsum[20];
+  __shared__ uint32_t s_last, s_found[3];
+  BigState* s = a.bs;
+  const int hi = STAGE == 0 ? s->hi : s->ihi;
+  if (hi <= 0 || (STAGE == 1 && !s->cut)) return;  // uniform: nothing left to resolve
+  const uint32_t tid = threadIdx.x;
+  const int bits = hi < kBigDigit ? hi : kBigDigit;
+  const int shift = hi - bits;
+  const uint32_t nb = 1u << bits;
+  const uint32_t hmask = hi >= 32 ? 0u : ~((1u << hi) - 1u);
+  const uint32_t pre = (STAGE == 0 ? s->prefix : s->iprefix) & hmask;
+  const uint32_t kstar = s->kstar;
+  for (uint32_t b = tid; b < nb; b += kBigBS) hist[b] = 0;
+  if (!s->from_input) load_segn(a, segn); else __syncthreads();
+  big_visit<DT, kBigBS>(a, *s, segn, [&](uint32_t key, uint32_t idx) {
+    uint32_t v = key;
+    if (STAGE == 1) {
+      if (key != kstar) return;
+      v = ~idx;
+    }
+    if ((v & hmask) == pre) atomicAdd(&hist[(v >> shift) & (nb - 1)], 1u);
+  });
+  __syncthreads();
+  for (uint32_t b = tid; b < nb; b += kBigBS)
+    if (hist[b]) atomicAdd(&a.ghist[b], hist[b]);
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) s_last = (atomicAdd(&s->ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  // The last block finds the digit holding the remaining rank.
+  const uint32_t krem = STAGE == 0 ? s->krem : s->ikrem;
+  const uint32_t per = (nb + kBigBS - 1) / kBigBS;  // bins per thread, descending
+  uint32_t loc = 0;
+  for (uint32_t r = tid * per; r < (tid + 1) * per && r < nb; ++r) loc += a.ghist[nb - 1 - r];
+  uint32_t run = block_excl_sum<kBigBS>(loc, wsum, nullptr);
+  for (uint32_t r = tid * per; r < (tid + 1) * per && r < nb; ++r) {
+    const uint32_t c = a.ghist[nb - 1 - r];
+    if (run < krem && krem <= run + c) {
+      s_found[0] = nb - 1 - r;
+      s_found[1] = run;
+      s_found[2] = c;
+    }
+    run += c;
+  }
+  __syncthreads();
+  for (uint32_t b = tid; b < nb; b += kBigBS) a.ghist[b] = 0;
+  if (tid == 0) {
+    const uint32_t d = s_found[0], ab = s_found[1], eq = s_found[2];
+    const uint32_t np = (pre & hmask) | (d << shift);
+    if (STAGE == 0) {
+      s->prefix = np;
+      s->krem = krem - ab;
+      s->above += ab;
+      s->equal = eq;
+      s->hi = shift;
+      if (shift == 0) {
+        s->kstar = np;
+        const bool cut = s->krem < eq;
+        s->cut = cut ? 1u : 0u;
+        if (cut) {
+          s->ikrem = s->krem;
+          s->ihi = 32;
+          s->iprefix = 0;
+        }
+      }
+    } else {
+      s->iprefix = np;
+      s->ikrem = krem - ab;
+      s->ihi = shift;
+      if (shift == 0) s->istar = ~np;
+    }
+    s->ticket = 0;
+  }
+}
+
+// -------------------------------------------------------------- collect ---
+template <int DT>
+__global__ __launch_bounds__(kBigBS) void k_big_collect(BigArgs a) {
+  __shared__ uint64_t stage[kBigStage];
+  __shared__ uint32_t segn[kSegs];
+  __shared__ uint32_t s_cnt, s_base;
+  const BigState* s = a.bs;
+  const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1);
+  const uint32_t kstar = s->kstar, istar = s->istar, cut = s->cut;
+  if (tid == 0) s_cnt = 0;
+  if (!s->from_input) load_segn(a, segn); else __syncthreads();
+  BigState* sw = a.bs;
+  big_visit<DT, kBigBS>(a, *s, segn, [&](uint32_t key, uint32_t idx) {
+    const bool take = key > kstar || (key == kstar && (!cut || idx <= istar));
+    const uint64_t bal = __ballot(take);
+    if (bal == 0) return;
+    const uint32_t total = __popcll(bal);
+    const uint32_t rank = __popcll(bal & ((1ull << lane) - 1ull));
+    uint32_t base = 0;
+    if (lane == __ffsll(static_cast<unsigned long long>(bal)) - 1) base = atomicAdd(&s_cnt, total);
+    base = __shfl(base, __ffsll(static_cast<unsigned long long>(bal)) - 1, kWave);
+    if (take) {
+      const uint32_t slot = base + rank;
+      const uint64_t c = composite(key, idx);
+      if (slot < kBigStage) {
+        stage[slot] = c;
+      } else {
+        // overflow of the LDS stage: one global atomic per such item (rare)
+        const uint32_t g = atomicAdd(&sw->out_count, 1u);
+        if (g < a.P) a.staging[g] = c;
+      }
+    }
+  });
+  __syncthreads();
+  const uint32_t n_st = min(s_cnt, static_cast<uint32_t>(kBigStage));
+  if (tid == 0) s_base = n_st ? atomicAdd(&sw->out_count, n_st) : 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < n_st; i += kBigBS) {
+    const uint32_t g = s_base + i;
+    if (g < a.P) a.staging[g] = stage[i];
+  }
+}
+
+// ----------------------------------------------------------------- sort ---
+// Sorts each tile of kBigTile composites descending; entries past kk are
+// padding (0, below every real composite).
+__global__ __launch_bounds__(1024) void k_big_tile(BigArgs a) {
+  __shared__ uint64_t exch[2 * kBigTile];
+  const uint32_t kk = a.bs->kk;
+  const uint32_t t0 = blockIdx.x * kBigTile;
+  constexpr int E = kBigTile / 1024;
+  uint64_t v[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const uint32_t p = t0 + e * 1024 + threadIdx.x;
+    v[e] = p < kk ? a.staging[p] : 0ull;
+  }
+  bitonic_sort_regs_desc<1024, E>(v, exch);
+#pragma unroll
+  for (int e = 0; e < E; ++e) a.runs[t0 + e * 1024 + threadIdx.x] = v[e];
+}
+
+// One merge-path pass: sorted runs of length L in `in` become runs of 2L in
+// `out`.  Block b writes outputs [b*kBigTile, (b+1)*kBigTile), which lie in
+// one pair of runs; the split points are found by a wave-parallel search
+// on the runs in memory, the block's slices are staged in LDS, and each
+// thread merges kBigTile/1024 outputs from its own split.
+__device__ __forceinline__ bool take_more_a(const uint64_t* A, uint32_t la, const uint64_t* B, uint32_t lb,
+                                            uint32_t o, uint32_t i) {
+  // With i items from A among the first o outputs, should there be more?
+  const uint32_t j = o - i;
+  return i < la && j > 0 && (j > lb || A[i] > B[j - 1]);
+}
+
+__device__ __forceinline__ uint32_t corank_wave(const uint64_t* A, uint32_t la, const uint64_t* B, uint32_t lb,
+                                                uint32_t o) {
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  uint32_t lo = o > lb ? o - lb : 0u;   // smallest feasible i
+  uint32_t hi = o < la ? o : la;         // largest feasible i
+  // find the smallest i in [lo, hi] with take_more_a false
+  while (hi > lo) {
+    const uint32_t span = hi - lo;
+    const uint32_t step = (span + kWave - 1) / kWave;
+    const uint32_t i = lo + lane * step;
+    const bool more = i < hi && take_more_a(A, la, B, lb, o, i);
+    const uint64_t m = __ballot(more);
+    // lanes 0..c-1 say "more": the answer is in (lo + (c-1)*step, lo + c*step]
+    const uint32_t c = __popcll(m);
+    if (c == 0) {
+      hi = lo;
+    } else {
+      lo = lo + (c - 1) * step + 1;
+      const uint32_t nhi = lo - 1 + step;
+      hi = nhi < hi ? nhi : hi;
+    }
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(1024) void k_big_merge(const uint64_t* in, uint64_t* out, uint32_t P, uint32_t L) {
+  __shared__ uint64_t sa[kBigTile], sb[kBigTile];
+  __shared__ uint32_t s_i[2];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t o_begin = blockIdx.x * kBigTile;
+  const uint32_t pair0 = (o_begin / (2 * L)) * (2 * L);
+  const uint64_t* A = in + pair0;
+  const uint32_t la = min(L, P - pair0);
+  const uint64_t* B = A + la;
+  const uint32_t lb = min(L, P - pair0 - la);
+  const uint32_t o0 = o_begin - pair0;
+  const uint32_t o1 = o0 + kBigTile;
+  if (tid < 2 * kWave) {
+    const uint32_t i = corank_wave(A, la, B, lb, tid < kWave ? o0 : o1);
+    if ((tid & (kWave - 1)) == 0) s_i[tid / kWave] = i;
+  }
+  __syncthreads();
+  const uint32_t i0 = s_i[0], i1 = s_i[1];
+  const uint32_t j0 = o0 - i0, j1 = o1 - i1;
+  const uint32_t na = i1 - i0, nbb = j1 - j0;
+  for (uint32_t p = tid; p < na; p += 1024) sa[p] = A[i0 + p];
+  for (uint32_t p = tid; p < nbb; p += 1024) sb[p] = B[j0 + p];
+  __syncthreads();
+  // each thread: outputs [q0, q0 + E) of this block's tile
+  constexpr uint32_t E = kBigTile / 1024;
+  const uint32_t q0 = tid * E;
+  uint32_t lo = q0 > nbb ? q0 - nbb : 0u, hi = q0 < na ? q0 : na;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (take_more_a(sa, na, sb, nbb, q0, mid)) lo = mid + 1; else hi = mid;
+  }
+  uint32_t ia = lo, ib = q0 - lo;
+#pragma unroll
+  for (uint32_t q = 0; q < E; ++q) {
+    uint64_t v;
+    if (ib >= nbb || (ia < na && sa[ia] > sb[ib])) v = sa[ia++];
+    else v = sb[ib++];
+    out[o_begin + q0 + q] = v;
+  }
+}
+
+// ---------------------------------------------------------------- write ---
+template <int DT>
+__global__ void k_big_write(BigArgs a, const uint64_t* sorted) {
+  const BigState* s = a.bs;
+  const uint32_t kk = s->kk;
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < a.k) {
+    uint32_t bits;
+    int64_t id;
+    if (i < kk) {
+      const uint64_t c = sorted[i];
+      bits = bits_of_key<DT>(comp_key(c));
+      id = comp_idx(c);
+    } else {
+      bits = DT == 0 ? 0xFF800000u : 0xFF80u;
+      id = -1;
+    }
+    if (DT == 0) static_cast<uint32_t*>(a.out_vals)[i] = bits;
+    else static_cast<uint16_t*>(a.out_vals)[i] = static_cast<uint16_t>(bits);
+    a.out_idx[i] = id;
+  }
+  if (i == 0 && a.info) {
+    a.info->count = s->total;
+    a.info->tau_key = s->tau;
+    a.info->status = static_cast<int32_t>(s->status);
+    a.info->n_valid = kk;
+  }
+}
+
+// ------------------------------------------------------------- host -------
+static inline uint32_t cdiv_u(uint64_t a, uint64_t b) { return static_cast<uint32_t>((a + b - 1) / b); }
+
+template <int DT>
+static hipError_t launch_big_t(const BigCall& c) {
+  constexpr int KB = Elem<DT>::KEYBITS;
+  const uint32_t P = cdiv_u(c.k, kBigTile) * kBigTile;
+  BigArgs a{c.values, c.n, c.k, c.k_req, c.M, c.direct, c.seg_cnt, c.seg_key, c.seg_idx, c.blk_max,
+            c.seg_cap, c.G_f, c.st, reinterpret_cast<BigState*>(c.big_state), c.ghist, c.staging, c.runs, P,
+            c.out_vals, c.out_idx, c.info};
+  hipLaunchKernelGGL(k_big_begin<DT>, dim3(1), dim3(1024), 0, c.stream, a);
+  const uint32_t key_passes = cdiv_u(KB, kBigDigit);
+  for (uint32_t p = 0; p < key_passes; ++p)
+    hipLaunchKernelGGL((k_big_pass<DT, 0>), dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
+  for (uint32_t p = 0; p < cdiv_u(32, kBigDigit); ++p)
+    hipLaunchKernelGGL((k_big_pass<DT, 1>), dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
+  hipLaunchKernelGGL(k_big_collect<DT>, dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
+  const uint32_t tiles = P / kBigTile;
+  hipLaunchKernelGGL(k_big_tile, dim3(tiles), dim3(1024), 0, c.stream, a);
+  uint64_t* src = c.runs;
+  uint64_t* dst = c.staging;
+  for (uint32_t L = kBigTile; L < P; L *= 2) {
+    hipLaunchKernelGGL(k_big_merge, dim3(tiles), dim3(1024), 0, c.stream, src, dst, P, L);
+    uint64_t* t = src;
+    src = dst;
+    dst = t;
+  }
+  hipLaunchKernelGGL(k_big_write<DT>, dim3(cdiv_u(c.k, 256)), dim3(256), 0, c.stream, a,
+                     static_cast<const uint64_t*>(src));
+  return hipGetLastError();
+}
+
+hipError_t launch_big(const BigCall& c) {
+  return c.dtype == PROFK_F32 ? launch_big_t<0>(c) : launch_big_t<1>(c);
+}
+
+}  // namespace profk

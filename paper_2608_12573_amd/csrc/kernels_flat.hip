@@ -582,9 +582,19 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   L.off_blk_max = take(static_cast<size_t>(L.G_f) * 4);
   L.off_seg_key = take(static_cast<size_t>(kSegs) * M * 4);
   L.off_seg_idx = take(static_cast<size_t>(kSegs) * M * 4);
-  L.off_cand_key = take(static_cast<size_t>(L.G_fb) * k * 4);
-  L.off_cand_idx = take(static_cast<size_t>(L.G_fb) * k * 4);
-  L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
+  L.big = k > static_cast<uint32_t>(kFinMaxK);
+  if (L.big) {
+    const size_t P = static_cast<size_t>(cdiv(k, kBigTile)) * kBigTile;
+    L.G_big = static_cast<uint32_t>(num_cus < kBigMaxBlocks ? num_cus : kBigMaxBlocks);
+    L.off_big_state = take(256);
+    L.off_ghist = take(static_cast<size_t>(kBigBins) * 4);
+    L.off_staging = take(P * 8);
+    L.off_runs = take(P * 8);
+  } else {
+    L.off_cand_key = take(static_cast<size_t>(L.G_fb) * k * 4);
+    L.off_cand_idx = take(static_cast<size_t>(L.G_fb) * k * 4);
+    L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
+  }
   L.bytes = off;
   return L;
 }
@@ -638,6 +648,14 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (!direct && (e = launch_filter<DT>(c, st, union_for_filter)) != hipSuccess) return e;
+  if (L.big) {
+    BigCall bc{DT, c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
+               direct ? 1 : 0, seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
+               at<uint32_t>(c.ws, L.off_blk_max), L.seg_cap, L.G_f, st, c.ws + L.off_big_state,
+               at<uint32_t>(c.ws, L.off_ghist), at<uint64_t>(c.ws, L.off_staging), at<uint64_t>(c.ws, L.off_runs),
+               L.G_big, c.out_vals, c.out_idx, c.info, c.stream};
+    return launch_big(bc);
+  }
   FinishArgs fa{c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
                 direct ? 1 : 0, L.G_f, L.seg_cap,
                 seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
@@ -649,12 +667,14 @@ static hipError_t launch_flat_t(const FlatCall& c) {
 }
 
 hipError_t launch_flat(const FlatCall& c) {
+  (void)hipGetLastError();  // report only errors of this call's launches
   return c.dtype == PROFK_F32 ? launch_flat_t<0>(c) : launch_flat_t<1>(c);
 }
 
 hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t N, int64_t* out,
                                  hipStream_t s) {
   const uint32_t nblk = cdiv(S, 4);
+  (void)hipGetLastError();
   hipLaunchKernelGGL(k_sample_indices, dim3(cdiv(nblk, 256)), dim3(256), 0, s, seed, row, S, N, out);
   return hipGetLastError();
 }
@@ -664,6 +684,7 @@ hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* b
   const FlatLayout& L = c.L;
   CallState* st = at<CallState>(c.ws, L.off_state);
   uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
+  (void)hipGetLastError();
   hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, InitArgs{st, seg_cnt, c.tau_key});
   hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st, nullptr) : launch_filter<1>(c, st, nullptr);
   if (e != hipSuccess) return e;

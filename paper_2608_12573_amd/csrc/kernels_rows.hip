@@ -218,6 +218,7 @@ static hipError_t launch_rows_t(const RowCall& c) {
 }
 
 hipError_t launch_rows(const RowCall& c) {
+  (void)hipGetLastError();  // report only errors of this call's launches
   return c.dtype == PROFK_F32 ? launch_rows_t<0>(c) : launch_rows_t<1>(c);
 }
 

@@ -35,6 +35,14 @@ constexpr int kFinMaxK = 4096;                // largest k of the one-block refi
 constexpr int kFbMaxBlocks = 256;
 constexpr uint32_t kFbMinChunk = 8192;
 
+// Multi-block refinement for k > kFinMaxK.
+constexpr int kBigBS = 256;
+constexpr int kBigDigit = 11;
+constexpr uint32_t kBigBins = 1u << kBigDigit;
+constexpr int kBigStage = 4096;               // composites a collect block stages in LDS
+constexpr uint32_t kBigTile = 4096;           // composites sorted per block
+constexpr int kBigMaxBlocks = 256;
+
 // Workspace layout of one flat (vector) call.
 struct FlatLayout {
   uint32_t G_s = 0, tcap = 0, union_n = 0;    // sampling
@@ -44,6 +52,9 @@ struct FlatLayout {
   size_t off_state = 0, off_segcnt = 0, off_union = 0, off_blk_max = 0;
   size_t off_seg_key = 0, off_seg_idx = 0;
   size_t off_cand_key = 0, off_cand_idx = 0, off_cand_cnt = 0;
+  bool big = false;                           // k > kFinMaxK: multi-block refinement
+  uint32_t G_big = 0;
+  size_t off_big_state = 0, off_ghist = 0, off_staging = 0, off_runs = 0;
   size_t bytes = 0;
 };
 
@@ -68,6 +79,26 @@ struct FlatCall {
 };
 
 hipError_t launch_flat(const FlatCall& c);
+
+struct BigCall {
+  int dtype;
+  const void* values;
+  uint32_t n, k, k_req, M;
+  int direct;
+  const uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
+  uint32_t seg_cap, G_f;
+  const CallState* st;
+  void* big_state;
+  uint32_t* ghist;
+  uint64_t *staging, *runs;
+  uint32_t G_big;
+  void* out_vals;
+  int64_t* out_idx;
+  profk_info_t* info;
+  hipStream_t stream;
+};
+
+hipError_t launch_big(const BigCall& c);
 
 // Per-row kernel: one workgroup per row, everything in LDS.
 constexpr int kRowBS = 256;                   // threads of a row block

@@ -124,3 +124,23 @@ def test_oracle_and_product_share_no_code():
                         text = f.read()
                     assert f"import {needle}" not in text and f"from {needle}" not in text, fn
                     assert f"{needle}/" not in text, fn
+
+
+def test_binding_shares_torchs_hip_runtime():
+    # A fresh process that loads the library through the binding must end up
+    # with a single HIP runtime (torch's), whatever it touches first.
+    import subprocess
+    import sys
+    code = (
+        "import os, sys\n"
+        f"sys.path.insert(0, {repr(__import__('os').path.dirname(__import__('os').path.dirname(__import__('os').path.abspath(__file__))))})\n"
+        "import paper_2608_12573_amd as pk\n"
+        "pk.plan(1 << 20, 64)\n"
+        "import torch\n"
+        "maps = open('/proc/self/maps').read()\n"
+        "libs = sorted(set(l.split()[-1] for l in maps.splitlines() if 'libamdhip64' in l))\n"
+        "print(len(libs)); print(libs)\n"
+    )
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.splitlines()[0] == "1", out.stdout
