@@ -28,7 +28,18 @@ HBM_PEAK_GBPS = 8000.0
 N_DEFAULT = 2**28
 K_DEFAULT = 1024
 COUNTERS = os.path.join(ROOT, "profiles", "filter_counters.json")
-FILTER_SRC = os.path.join(ROOT, "paper_2608_12573_amd", "csrc", "kernels_flat.hip")
+CSRC = os.path.join(ROOT, "paper_2608_12573_amd", "csrc")
+# Every source the filter kernel is compiled from: the committed counters
+# stand for this exact code and are dropped once any of these changes.
+FILTER_SRCS = ("kernels_flat.hip", "filter_tile.h", "device_common.h", "launch.h", "topk_block.h")
+
+
+def filter_source_sha256():
+    h = hashlib.sha256()
+    for name in FILTER_SRCS:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
 
 
 class HipEvents:
@@ -63,8 +74,7 @@ def counters_traffic(n_launch_bytes):
     try:
         with open(COUNTERS) as f:
             c = json.load(f)
-        with open(FILTER_SRC, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
+        sha = filter_source_sha256()
     except OSError:
         return None
     if c.get("kernel_source_sha256") != sha:
@@ -101,6 +111,7 @@ def main():
     ap.add_argument("--k", type=int, default=K_DEFAULT)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-torch-baseline", action="store_true")
+    ap.add_argument("--no-copy-probe", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -196,6 +207,25 @@ def main():
         same_vals = bool(torch.equal(tv, out[0]))
         line["torch_topk"] = {"ms": round(t_ms, 4), "GB/s": round(in_bytes / (t_ms * 1e-3) / 1e9, 1),
                               "values_equal": same_vals, "speedup_vs_torch": round(t_ms / ms_per_step, 3)}
+
+    if not args.no_copy_probe:
+        # A plain device-to-device copy of the same 1 GiB: the practical
+        # streaming ceiling on this GPU, and the reference kernel that scales
+        # the FETCH_SIZE / WRITE_SIZE counters into bytes.
+        dst = torch.empty_like(x)
+        for _ in range(2):
+            dst.copy_(x)
+        torch.cuda.synchronize()
+        reps = 5
+        start.record()
+        for _ in range(reps):
+            dst.copy_(x)
+        stop.record()
+        torch.cuda.synchronize()
+        c_ms = start.elapsed_time(stop) / reps
+        line["copy_probe"] = {"bytes_read": in_bytes, "bytes_written": in_bytes, "ms": round(c_ms, 4),
+                              "GB/s": round(2 * in_bytes / (c_ms * 1e-3) / 1e9, 1)}
+        del dst
 
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(x_np, k)
