@@ -1,16 +1,21 @@
 #!/usr/bin/env python3
 """Prof-K top-k throughput on one MI355X.
 
-Workload: one vector of N = 2^28 standard-normal fp32 values (seed 1), exact
-top-k with k = 1024 and eps = 1e-6 -- the large-N, small-k regime of the
-paper's synthetic study (Sec. 5), synthetic data.  One step is one
-profk_topk call: sampling, threshold, the filter-and-compact pass and the
-exact refinement, with the input already resident in HBM.
+Default workload: one vector of N = 2^28 standard-normal fp32 values
+(seed 1), exact top-k with k = 1024 and eps = 1e-6 -- the large-N, small-k
+regime of the paper's synthetic study (Sec. 5), synthetic data.  One step
+is one profk_topk call: sampling, threshold, the filter-and-compact pass
+and the exact refinement, with the input already resident in HBM.
 
-Prints one JSON line.  `value` is effective GB/s (N * 4 bytes / step time);
-`roofline` times the filter kernel alone with HIP events recorded by the
-library around each launch on its own stream; `cpu_baseline` times the CPU
-oracle (exact stable-sort top-k) on a prefix of the same input.
+--workload picks one of the other shapes the parity tests cover (the small
+uniform vector, the adversarial 2^26 vectors, the per-row bf16 batch and
+the flattened BatchTopK select); the printed line then describes that one.
+
+Prints one JSON line.  `value` is effective GB/s (input bytes / step time);
+`roofline` times the dominant kernel -- the filter, or for the per-row
+path its single fused kernel -- with HIP events recorded by the library
+around the launch on its own stream; `cpu_baseline` times the CPU oracle
+(exact stable-sort top-k) on a bounded prefix of the same input.
 """
 
 import argparse
@@ -25,13 +30,13 @@ import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
-N_DEFAULT = 2**28
-K_DEFAULT = 1024
 COUNTERS = os.path.join(ROOT, "profiles", "filter_counters.json")
 CSRC = os.path.join(ROOT, "paper_2608_12573_amd", "csrc")
 # Every source the filter kernel is compiled from: the committed counters
 # stand for this exact code and are dropped once any of these changes.
 FILTER_SRCS = ("kernels_flat.hip", "filter_tile.h", "device_common.h", "launch.h", "topk_block.h")
+WORKLOADS = ("c2", "c1", "c3a", "c3b", "c3c", "c3d", "c3d2", "c4", "c5", "c5r")
+FLUSH_BYTES = 512 << 20
 
 
 def filter_source_sha256():
@@ -68,38 +73,137 @@ class HipEvents:
         self.hip.hipEventDestroy(ev)
 
 
-def counters_traffic(n_launch_bytes):
+def counters_traffic(workload_key):
     """HBM bytes per filter launch from the committed rocprofv3 counter
-    summary, or None when it is missing or the kernel source changed since."""
+    summary, or None when it covers another workload or the kernel source
+    changed since it was taken."""
     try:
         with open(COUNTERS) as f:
             c = json.load(f)
         sha = filter_source_sha256()
     except OSError:
         return None
-    if c.get("kernel_source_sha256") != sha:
+    if c.get("kernel_source_sha256") != sha or c.get("workload_key") != workload_key:
         return None
     return c.get("traffic_bytes_per_launch")
 
 
-def cpu_baseline(x_np, k, budget_s=10.0):
-    """The oracle's exact top-k (full stable sort, oracle.exact) on a 2^24
-    prefix of the workload, repeated for about budget_s seconds."""
+class Workload:
+    """Input, preallocated outputs and one step of the path for one shape."""
+
+    def __init__(self, name, k_arg, torch, pk, wl):
+        self.name = name
+        self.rows = False
+        self.es = 4
+        self.recall = 1.0
+
+        def f32(a):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+        if name in ("c1", "c2") or name.startswith("c3"):
+            if name == "c1":
+                N, k, host, what = 2**20, 64, wl.uniform_f32(2**20, seed=0), "Uniform(0,1) (seed 0)"
+            elif name == "c2":
+                N, k = 2**28, k_arg
+                host, what = wl.normal_f32(N, seed=1), "standard normal (seed 1)"
+            else:
+                N, k = 2**26, 512
+                host, what = {
+                    "c3a": lambda: (wl.pareto_f32(N, seed=2), "Pareto alpha=1.1 (seed 2)"),
+                    "c3b": lambda: (wl.zeros90_f32(N, seed=2), "90% +0.0, 10% Uniform(0,1) (seed 2)"),
+                    "c3c": lambda: (wl.ramp_f32(N), "ascending ramp float32(i)"),
+                    "c3d": lambda: (wl.plateau_f32(N, seed=2, first_rank=257, width=10_000),
+                                    "Uniform(0,1) with a 1e4-wide plateau at ranks 257..10256 (seed 2)"),
+                    "c3d2": lambda: (wl.plateau_f32(N, seed=2, first_rank=257, width=200_000),
+                                     "Uniform(0,1) with a 2e5-wide plateau at ranks 257..200256 (seed 2)"),
+                }[name]()
+            self.desc = (f"one fp32 vector, N=2^{N.bit_length() - 1} {what}, exact top-k k={k}, "
+                         f"eps=1e-6, sample seed 0")
+            self.host = host
+            self.x = f32(host)
+            self.p = pk.plan(N, k, 1e-6, 1.0)
+            self.kernel = "k_filter<f32>"
+            self.ws = pk.workspace(self.p, pk.F32)
+            self.out = (torch.empty(k, dtype=torch.float32, device="cuda"),
+                        torch.empty(k, dtype=torch.int64, device="cuda"))
+            self.info = torch.empty(pk.INFO_BYTES, dtype=torch.uint8, device="cuda")
+            self.step = lambda: pk.topk(self.x, k, p=self.p, ws=self.ws, out=self.out, info=self.info,
+                                        seed=0)
+            self.torch_ref = lambda: torch.topk(self.x, k, sorted=True)
+            self.N, self.k = N, k
+        elif name == "c4":
+            B, D, k = 4096, 131072, 32
+            bits = wl.relu_normal_bf16((B, D), seed=3)
+            self.host = bits
+            self.x = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
+            self.rows, self.es = True, 2
+            self.p = pk.plan_rows(D, k, 1e-6, 1.0)
+            self.kernel = "k_rows<bf16>"
+            self.desc = (f"bf16 rows [4096, 131072] of ReLU(N(0,1)) (seed 3), per-row top-k k={k}, "
+                         f"eps=1e-6, one row plan, sample seed 0")
+            self.ws = pk.workspace(self.p, pk.BF16, B)
+            self.out = (torch.empty((B, k), dtype=torch.bfloat16, device="cuda"),
+                        torch.empty((B, k), dtype=torch.int64, device="cuda"))
+            self.info = torch.empty(B * pk.INFO_BYTES, dtype=torch.uint8, device="cuda")
+            self.step = lambda: pk.topk_rows(self.x, k, p=self.p, ws=self.ws, out=self.out,
+                                             info=self.info, seed=0)
+            self.torch_ref = lambda: torch.topk(self.x, k, dim=1, sorted=True)
+            self.N, self.k, self.B, self.D = B * D, k, B, D
+        elif name in ("c5", "c5r"):
+            B, D, k_row = 4096, 65536, 64
+            self.recall = 1.0 if name == "c5" else 0.95
+            host = wl.sae_preacts_f32(B=B, D=D, seed=4)
+            self.host = host.reshape(-1)
+            self.x = f32(host).view(B, D)
+            K = B * k_row
+            self.p = pk.plan(B * D, K, 1e-6, self.recall)
+            self.kernel = "k_filter<f32>"
+            self.desc = (f"BatchTopK select over fp32 [4096, 65536] N(-0.5,1) pre-activations with 1% "
+                         f"hot columns +3 (seed 4), K=4096*64=262144, eps=1e-6, recall {self.recall}, "
+                         f"sample seed 0")
+            self.ws = pk.workspace(self.p, pk.F32)
+            self.out = (torch.empty(K, dtype=torch.float32, device="cuda"),
+                        torch.empty(K, dtype=torch.int64, device="cuda"))
+            self.info = torch.empty(pk.INFO_BYTES, dtype=torch.uint8, device="cuda")
+            self.step = lambda: pk.batchtopk(self.x, k_row, recall=self.recall, p=self.p, ws=self.ws,
+                                             out=self.out, info=self.info, seed=0)
+            self.torch_ref = lambda: torch.topk(self.x.view(-1), K, sorted=True)
+            self.N, self.k = B * D, K
+        else:
+            raise SystemExit(f"unknown workload {name}; choose from {', '.join(WORKLOADS)}")
+        self.in_bytes = self.N * self.es
+
+    def key(self):
+        return f"{self.name}-k{self.k}"
+
+
+def cpu_baseline(w, budget_s=10.0):
+    """The oracle's exact top-k (full stable sort, oracle.exact) on a bounded
+    prefix of the workload -- 2^24 values, or 128 rows of the per-row batch --
+    repeated for about budget_s seconds."""
     sys.path.insert(0, ROOT)
     from oracle import exact, keys
-    n_s = min(x_np.size, 2**24)
-    bits = keys.f32_bits(x_np[:n_s])
+    if w.rows:
+        R = 128
+        bits = w.host[:R]
+        run = lambda: exact.topk_rows(bits, "bf16", w.k)
+        n_s, what = R * w.D, f"oracle.exact.topk_rows on the first {R} of the {w.B} rows"
+    else:
+        n_s = min(w.N, 2**24)
+        bits = keys.f32_bits(w.host[:n_s])
+        kk = min(w.k, n_s)
+        run = lambda: exact.topk(bits, "f32", kk)
+        what = f"oracle.exact.topk on the first 2^{n_s.bit_length() - 1} of the {w.N} values, k={kk}"
     reps, t0 = 0, time.perf_counter()
     while True:
-        exact.topk(bits, "f32", k)
+        run()
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
     per = el / reps
-    return {"value": round(n_s * 4 / per / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"oracle.exact.topk (numpy stable argsort, one thread) on the first 2^24 of the "
-                      f"2^28 values, k={k}, {reps} runs, {per * 1e3:.0f} ms each",
+    return {"value": round(n_s * w.es / per / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{what} (numpy stable argsort, one thread), {reps} runs, {per * 1e3:.0f} ms each",
             "elements_per_s": round(n_s / per, 1)}
 
 
@@ -108,7 +212,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--k", type=int, default=K_DEFAULT)
+    ap.add_argument("--workload", default="c2", choices=WORKLOADS)
+    ap.add_argument("--k", type=int, default=1024, help="k of the default N=2^28 workload")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time each step after overwriting 512 MiB (flushes the last-level cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-torch-baseline", action="store_true")
     ap.add_argument("--no-copy-probe", action="store_true")
@@ -123,21 +230,10 @@ def main():
     import paper_2608_12573_amd as pk
     import workloads
 
-    N, k = N_DEFAULT, args.k
-    x_np = workloads.normal_f32(N, seed=1)
-    x = torch.from_numpy(x_np).cuda()
-    p = pk.plan(N, k, 1e-6, 1.0)
-    ws = pk.workspace(p, pk.F32)
-    out = (torch.empty(k, dtype=torch.float32, device="cuda"),
-           torch.empty(k, dtype=torch.int64, device="cuda"))
-    info = torch.empty(pk.INFO_BYTES, dtype=torch.uint8, device="cuda")
+    w = Workload(args.workload, args.k, torch, pk, workloads)
     lib = pk.lib()
-
-    def step():
-        pk.topk(x, k, p=p, ws=ws, out=out, info=info, seed=0)
-
     for _ in range(args.warmup):
-        step()
+        w.step()
     torch.cuda.synchronize()
 
     ev = HipEvents()
@@ -147,23 +243,31 @@ def main():
     start.record()
     for a, b in pairs:
         lib.profk_set_trace_events(a, b)
-        step()
+        w.step()
     stop.record()
     torch.cuda.synchronize()
     lib.profk_set_trace_events(None, None)
-    total_ms = start.elapsed_time(stop)
-    filt_ms = [ev.elapsed_ms(a, b) for a, b in pairs]
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    if w.rows:
+        kern_ms = ms_per_step  # the per-row path is one kernel
+    else:
+        kern_ms = float(np.mean([ev.elapsed_ms(a, b) for a, b in pairs]))
     for a, b in pairs:
         ev.destroy(a)
         ev.destroy(b)
 
-    rec = pk.read_info(info)[0]
-    ms_per_step = total_ms / args.steps
-    filt_avg_ms = float(np.mean(filt_ms))
-    in_bytes = N * 4
-    value = in_bytes / (ms_per_step * 1e-3) / 1e9
-    filt_bytes = in_bytes + int(rec["count"]) * 8
-    achieved = filt_bytes / (filt_avg_ms * 1e-3) / 1e9
+    recs = pk.read_info(w.info)
+    if w.rows:
+        count = int(recs["count"].sum())
+        status = {str(int(s)): int((recs["status"] == s).sum()) for s in np.unique(recs["status"])}
+        # one read of the batch, the outputs and the per-row reports
+        kern_bytes = w.in_bytes + w.B * w.k * (w.es + 8) + w.B * pk.INFO_BYTES
+    else:
+        count = int(recs[0]["count"])
+        status = int(recs[0]["status"])
+        kern_bytes = w.in_bytes + count * 8  # one read of the input, (key, index) per survivor
+    value = w.in_bytes / (ms_per_step * 1e-3) / 1e9
+    achieved = kern_bytes / (kern_ms * 1e-3) / 1e9
 
     line = {
         "metric": "effective GB/s and elements/s at N=2^28 fp32, k=1024; % of HBM peak",
@@ -176,59 +280,72 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u32",
+        "dtype": "u16" if w.es == 2 else "u32",
         "data": "synthetic",
-        "config": {"workload": f"one fp32 vector, N=2^28 standard normal (seed 1), exact top-k k={k}, "
-                               f"eps=1e-6, sample seed 0", "N": N, "k": k, "eps": 1e-6,
-                   "plan": {"S": p.S, "t": p.t, "M": p.M}},
-        "elements_per_s": round(N / (ms_per_step * 1e-3), 1),
+        "config": {"workload": w.desc, "N": w.N, "k": w.k, "eps": 1e-6, "recall": w.recall,
+                   "plan": {"S": w.p.S, "t": w.p.t, "M": w.p.M, "mode": w.p.mode}},
+        "elements_per_s": round(w.N / (ms_per_step * 1e-3), 1),
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
-        "filter_ms": round(filt_avg_ms, 5),
-        "filter_pct_hbm_peak": round(100 * in_bytes / (filt_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
-        "count": int(rec["count"]),
-        "status": int(rec["status"]),
+        "kernel_ms": round(kern_ms, 5),
+        "kernel_pct_hbm_peak": round(100 * w.in_bytes / (kern_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+        "count": count,
+        "status": status,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": counters_traffic(filt_bytes), "kernel": "k_filter<f32>",
-                     "algorithmic_bytes_per_launch": filt_bytes},
+                     "traffic": counters_traffic(w.key()), "kernel": w.kernel,
+                     "algorithmic_bytes_per_launch": kern_bytes},
     }
 
-    if not args.no_torch_baseline:
-        for _ in range(3):
-            torch.topk(x, k, sorted=True)
-        torch.cuda.synchronize()
-        reps = 10
-        start.record()
-        for _ in range(reps):
-            tv, ti = torch.topk(x, k, sorted=True)
-        stop.record()
-        torch.cuda.synchronize()
-        t_ms = start.elapsed_time(stop) / reps
-        same_vals = bool(torch.equal(tv, out[0]))
-        line["torch_topk"] = {"ms": round(t_ms, 4), "GB/s": round(in_bytes / (t_ms * 1e-3) / 1e9, 1),
-                              "values_equal": same_vals, "speedup_vs_torch": round(t_ms / ms_per_step, 3)}
+    if args.cold:
+        flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+        cold = []
+        for i in range(args.steps):
+            flush.fill_(float(i))
+            start.record()
+            w.step()
+            stop.record()
+            torch.cuda.synchronize()
+            cold.append(start.elapsed_time(stop))
+        line["cold_ms_per_step"] = round(float(np.median(cold)), 5)
+        del flush
 
-    if not args.no_copy_probe:
-        # A plain device-to-device copy of the same 1 GiB: the practical
-        # streaming ceiling on this GPU, and the reference kernel that scales
-        # the FETCH_SIZE / WRITE_SIZE counters into bytes.
-        dst = torch.empty_like(x)
+    if not args.no_torch_baseline:
         for _ in range(2):
-            dst.copy_(x)
+            w.torch_ref()
         torch.cuda.synchronize()
         reps = 5
         start.record()
         for _ in range(reps):
-            dst.copy_(x)
+            tv, ti = w.torch_ref()
+        stop.record()
+        torch.cuda.synchronize()
+        t_ms = start.elapsed_time(stop) / reps
+        line["torch_topk"] = {"ms": round(t_ms, 4), "GB/s": round(w.in_bytes / (t_ms * 1e-3) / 1e9, 1),
+                              "values_equal": bool(torch.equal(tv, w.out[0])),
+                              "speedup_vs_torch": round(t_ms / ms_per_step, 3)}
+        del tv, ti
+
+    if not args.no_copy_probe:
+        # A plain device-to-device copy of the same input: the practical
+        # streaming ceiling on this GPU, and the reference kernel that scales
+        # the FETCH_SIZE / WRITE_SIZE counters into bytes.
+        dst = torch.empty_like(w.x)
+        for _ in range(2):
+            dst.copy_(w.x)
+        torch.cuda.synchronize()
+        reps = 5
+        start.record()
+        for _ in range(reps):
+            dst.copy_(w.x)
         stop.record()
         torch.cuda.synchronize()
         c_ms = start.elapsed_time(stop) / reps
-        line["copy_probe"] = {"bytes_read": in_bytes, "bytes_written": in_bytes, "ms": round(c_ms, 4),
-                              "GB/s": round(2 * in_bytes / (c_ms * 1e-3) / 1e9, 1)}
+        line["copy_probe"] = {"bytes_read": w.in_bytes, "bytes_written": w.in_bytes, "ms": round(c_ms, 4),
+                              "GB/s": round(2 * w.in_bytes / (c_ms * 1e-3) / 1e9, 1)}
         del dst
 
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(x_np, k)
+        line["cpu_baseline"] = cpu_baseline(w)
 
     print(json.dumps(line), flush=True)
 
