@@ -414,6 +414,17 @@ __device__ __forceinline__ void bitonic_sort_regs_desc(uint64_t (&v)[E], uint64_
   }
 }
 
+// Monotone log-scale bin of a key distance d = key - tau, in
+// [0, kLogBins): exact below 128, then 128 bins per octave (the 7 bits after
+// the leading one).  Larger d never maps to a smaller bin, and a bin spans a
+// relative width of at most 1/128 of its distance.
+constexpr uint32_t kLogBins = 3328;
+__device__ __forceinline__ uint32_t log_bin(uint32_t d) {
+  if (d < 128u) return d;
+  const uint32_t e = 31u - static_cast<uint32_t>(__clz(d));  // 7..31
+  return (e - 6u) * 128u + ((d >> (e - 7u)) & 127u);
+}
+
 // Composite ordering key: larger key first, then smaller index.
 __device__ __forceinline__ uint64_t composite(uint32_t key, uint32_t idx) {
   return (static_cast<uint64_t>(key) << 32) | static_cast<uint64_t>(~idx);

@@ -26,8 +26,12 @@
 
 namespace profk {
 
-__device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt) {
+// Clears the per-call counters; fhist (kLogBins words, or null) is the
+// refinement histogram the filter accumulates into.
+__device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt, uint32_t* fhist) {
   if (threadIdx.x < kSegs) seg_cnt[threadIdx.x * kSegStride] = 0;
+  if (fhist)
+    for (uint32_t i = threadIdx.x; i < kLogBins; i += blockDim.x) fhist[i] = 0;
   if (threadIdx.x == 0) {
     st->ticket = 0;
     st->status = 0;
@@ -42,6 +46,7 @@ struct SampleArgs {
   uint32_t* union_keys;
   CallState* st;
   uint32_t* seg_cnt;
+  uint32_t* fhist;
 };
 
 template <int DT>
@@ -53,7 +58,7 @@ __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
   __shared__ SelectShared sel;
   __shared__ uint32_t emitted;
   const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-  if (b == 0) reset_state(a.st, a.seg_cnt);
+  if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist);
   const uint32_t j0 = b * kSampPerBlock;
   const uint32_t nb = min(static_cast<uint32_t>(kSampPerBlock), a.S - j0);
   uint32_t kv[4];
@@ -153,11 +158,12 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
 struct InitArgs {
   CallState* st;
   uint32_t* seg_cnt;
+  uint32_t* fhist;
   uint32_t tau_key;
 };
 
 __global__ void k_init_state(InitArgs a) {
-  reset_state(a.st, a.seg_cnt);
+  reset_state(a.st, a.seg_cnt, a.fhist);
   if (threadIdx.x == 0) a.st->tau_key = a.tau_key;
 }
 
@@ -170,6 +176,7 @@ struct FilterArgs {
   const uint32_t* union_keys;  // sample union to select tau from, or null: tau in st
   uint32_t union_n, t;
   uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
+  uint32_t* fhist;             // refinement histogram (or null), zero on entry
 };
 
 // The filter pass; the survival test is in filter_tile.h.
@@ -178,8 +185,13 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   constexpr int EPV = Elem<DT>::EPV;
   constexpr int ES = Elem<DT>::ES;
   __shared__ uint32_t s_skey[kStage], s_sidx[kStage];
-  __shared__ uint32_t s_union[kFiltTauMax];
-  __shared__ SelectShared s_sel;
+  // the sample union and the select histogram while tau is chosen, then the
+  // block's log-bin histogram of its survivors
+  __shared__ __align__(16) uint32_t s_pool[kFiltTauMax + kSelBins];
+  __shared__ SelectScratch s_scr;
+  static_assert(kLogBins <= kFiltTauMax + kSelBins, "filter histogram");
+  uint32_t* const s_union = s_pool;
+  uint32_t* const s_lists = s_pool + kFiltTauMax;
   __shared__ uint32_t s_cnt, s_tau, s_base;
   __shared__ uint32_t s_wmax[kFiltBS / kWave];
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), b = blockIdx.x;
@@ -205,8 +217,8 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
       }
       uint32_t last = 0;
       const uint32_t w = tid / kWave;
-      const uint32_t got = wave_top_t<E>(uk, valid, a.t, s_sel.hist + w * kWaveTopMax, last);
-      if (lane == 0) s_sel.found[w] = got;
+      const uint32_t got = wave_top_t<E>(uk, valid, a.t, s_lists + w * kWaveTopMax, last);
+      if (lane == 0) s_scr.found[w] = got;
       __syncthreads();
       if (w == 0) {
         constexpr int E2 = NW * kWaveTopMax / kWave;
@@ -218,18 +230,18 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
           v2[e] = 0;
 #pragma unroll
           for (int i = 0; i < NW; ++i)
-            if (li == static_cast<uint32_t>(i) && c >= s_sel.found[i]) { c -= s_sel.found[i]; li = i + 1; }
-          if (li < NW) { v2[e] = s_sel.hist[li * kWaveTopMax + c]; valid2 |= 1u << e; }
+            if (li == static_cast<uint32_t>(i) && c >= s_scr.found[i]) { c -= s_scr.found[i]; li = i + 1; }
+          if (li < NW) { v2[e] = s_lists[li * kWaveTopMax + c]; valid2 |= 1u << e; }
         }
         wave_top_t<E2>(v2, valid2, a.t, nullptr, last);
         if (lane == 0) s_tau = last;
       }
     } else {
-      const SelectResult r = block_select_kth<kFiltBS>(
+      const SelectResult r = block_select_kth<kFiltBS, kSelDigit>(
           [&](auto f) {
             for (uint32_t i = tid; i < a.union_n; i += kFiltBS) f(s_union[i]);
           },
-          a.t, Elem<DT>::KEYBITS, 0u, s_sel);
+          a.t, Elem<DT>::KEYBITS, 0u, s_lists, s_scr);
       if (tid == 0) s_tau = r.kth;
     }
     __syncthreads();
@@ -240,6 +252,9 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   }
 
   const Thresh<DT> th(tau);
+  uint32_t* const s_hist = s_pool;
+  if (a.fhist)
+    for (uint32_t i = tid; i < kLogBins; i += kFiltBS) s_hist[i] = 0;
   __syncthreads();
 
   uint32_t* const seg_counter = a.seg_cnt + seg * kSegStride;
@@ -266,6 +281,7 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   };
   auto store = [&](uint32_t slot, uint32_t first_over, uint32_t gbase, uint32_t key, uint32_t idx) {
     my_max = max(my_max, key);
+    if (a.fhist) atomicAdd(&s_hist[log_bin(key - tau)], 1u);
     if (slot < kStage) {
       s_skey[slot] = key;
       s_sidx[slot] = idx;
@@ -338,22 +354,43 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
       seg_idx[gp] = s_sidx[i];
     }
   }
+  // Add the block's non-empty bins to the refinement histogram.
+  if (a.fhist && n_st) {
+    for (uint32_t i = tid; i < kLogBins; i += kFiltBS) {
+      const uint32_t c = s_hist[i];
+      if (c) atomicAdd(&a.fhist[i], c);
+    }
+  }
 }
 
 // ------------------------------------------------------------ stage 4 -----
 constexpr uint32_t kFinCache = 28672;
 constexpr int kFinDigit = 12;
 
+// LDS of the general refinement (radix select over the candidates).
 struct FinShared {
   uint32_t cache[kFinCache];       // candidate keys; later the sort's exchange buffers
   uint64_t sortbuf[kFinMaxK];      // radix histogram, then the collected top k
   uint32_t pre[1024];
   SelectScratch sel;
-  uint32_t seg_n[kSegs], seg_pre[kSegs + 1];
   uint32_t misc[8];
   __device__ __forceinline__ TopkSmem topk() {
     return TopkSmem{cache, kFinCache, reinterpret_cast<uint32_t*>(sortbuf), sortbuf, &sel, &misc[0]};
   }
+};
+
+// LDS of the bucket refinement: the candidates at or above the bucket of
+// rank k, placed bucket by bucket in descending bucket order.
+struct BucketShared {
+  uint32_t off[kLogBins];          // first slot of each bucket
+  uint32_t fill[kLogBins];         // entries placed in each bucket
+  uint64_t comp[kFastCap];         // (key, ~index) composites
+};
+
+union FinLds {
+  FinShared gen;
+  BucketShared bkt;
+  uint32_t hist[kLogBins];         // a block's histogram of its slice
 };
 
 // The filter's candidates: segment x holds n_x entries at x*cap; candidate i
@@ -425,51 +462,165 @@ struct FinishArgs {
   CallState* st;
   uint32_t G_fb, chunk;
   uint32_t *cand_key, *cand_idx, *cand_cnt;
+  const uint32_t* fhist;           // the filter's histogram of log_bin(key - tau)
   void* out_vals;
   int64_t* out_idx;
   profk_info_t* info;
 };
 
+// Refinement of a filtered call (k_req <= total <= M) by one block, from
+// the filter's histogram of log_bin(key - tau) over the candidates:
+//   1. find the bucket b* holding rank kk;
+//   2. when the candidates at or above b* are few and every such bucket is
+//      small, place them bucket by bucket in LDS and rank each one within its
+//      bucket by comparison: its output position is the bucket's first slot
+//      plus the number of larger composites in the bucket;
+//   3. otherwise run the general radix refinement.
+template <int DT>
+__device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh, const uint32_t* seg_pre,
+                                                uint32_t total, SelectScratch& fs) {
+  constexpr int KB = Elem<DT>::KEYBITS;
+  constexpr int UNR = 16;
+  const uint32_t tid = threadIdx.x;
+  const uint32_t tau = a.st->tau_key;
+  const SegSrc src{a.seg_key, a.seg_idx, a.seg_cap, seg_pre};
+  const uint32_t kk = min(a.k, total);
+
+  // 1. bucket offsets in descending bucket order: thread t owns buckets
+  //    [kLogBins - 4(t+1), kLogBins - 4t)
+  constexpr uint32_t kOwners = kLogBins / 4;
+  static_assert(kLogBins % 4 == 0 && kOwners <= kFinBS, "bucket ownership");
+  uint32_t h[4] = {0u, 0u, 0u, 0u};
+  const uint32_t bbase = kLogBins - 4 * (tid + 1);
+  if (tid < kOwners) {
+    const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
+    h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
+  }
+  const uint32_t above_me = block_excl_sum<kFinBS>(h[0] + h[1] + h[2] + h[3], fs.wsum, nullptr);
+  if (tid < kOwners) {
+    uint32_t run = above_me;
+#pragma unroll
+    for (int j = 3; j >= 0; --j) {
+      sh.bkt.off[bbase + j] = run;
+      sh.bkt.fill[bbase + j] = 0;
+      if (run < kk && kk <= run + h[j]) {
+        fs.found[0] = bbase + j;
+        fs.found[1] = run;
+        fs.found[2] = h[j];
+      }
+      run += h[j];
+    }
+  }
+  __syncthreads();
+  const uint32_t bstar = fs.found[0], n_sel = fs.found[1] + fs.found[2];
+  uint32_t big = 0;
+  if (tid < kOwners) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (bbase + j >= bstar) big = max(big, h[j]);
+  }
+  big = block_max<kFinBS>(big, fs.wsum);
+
+  if (n_sel <= kFastCap && big <= kFastBucket) {
+    // place (key, candidate number) of buckets >= b* ...
+    for (uint32_t base = 0; base < total; base += kFinBS * UNR) {
+      uint32_t kv[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const uint32_t i = base + u * kFinBS + tid;
+        kv[u] = i < total ? a.seg_key[src.pos(i)] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const uint32_t i = base + u * kFinBS + tid;
+        if (i < total) {
+          const uint32_t bin = log_bin(kv[u] - tau);
+          if (bin >= bstar) {
+            const uint32_t slot = sh.bkt.off[bin] + atomicAdd(&sh.bkt.fill[bin], 1u);
+            sh.bkt.comp[slot] = (static_cast<uint64_t>(kv[u]) << 32) | i;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // ... then turn them into composites, all index loads in flight at once
+    constexpr int PER = kFastCap / kFinBS;
+    uint32_t ix[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const uint32_t p = u * kFinBS + tid;
+      ix[u] = p < n_sel ? a.seg_idx[src.pos(static_cast<uint32_t>(sh.bkt.comp[p]))] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const uint32_t p = u * kFinBS + tid;
+      if (p < n_sel) sh.bkt.comp[p] = composite(static_cast<uint32_t>(sh.bkt.comp[p] >> 32), ix[u]);
+    }
+    __syncthreads();
+    // rank within the bucket, write the kk largest
+    for (uint32_t p = tid; p < n_sel; p += kFinBS) {
+      const uint64_t c = sh.bkt.comp[p];
+      const uint32_t bin = log_bin(comp_key(c) - tau);
+      const uint32_t s = sh.bkt.off[bin], m = sh.bkt.fill[bin];
+      uint32_t r = 0;
+      for (uint32_t q = s; q < s + m; ++q) r += sh.bkt.comp[q] > c ? 1u : 0u;
+      const uint32_t dst = s + r;
+      if (dst < kk) {
+        const uint32_t bits = bits_of_key<DT>(comp_key(c));
+        if (DT == 0) static_cast<uint32_t*>(a.out_vals)[dst] = bits;
+        else static_cast<uint16_t*>(a.out_vals)[dst] = static_cast<uint16_t>(bits);
+        a.out_idx[dst] = comp_idx(c);
+      }
+    }
+    for (uint32_t p = kk + tid; p < a.k; p += kFinBS) {  // relaxed recall: padding
+      if (DT == 0) static_cast<uint32_t*>(a.out_vals)[p] = 0xFF800000u;
+      else static_cast<uint16_t*>(a.out_vals)[p] = 0xFF80u;
+      a.out_idx[p] = -1;
+    }
+  } else {
+    __syncthreads();
+    const uint32_t gmax = block_max<kFinBS>(tid < a.G_f ? a.blk_max[tid] : 0u, fs.wsum);
+    block_topk<kFinBS, kFinDigit>(src, total, kk, tau, max(gmax, tau), KB, sh.gen.topk());
+    sort_write_any<DT, kFinBS>(sh.gen.sortbuf, kk, a.k, reinterpret_cast<uint64_t*>(sh.gen.cache),
+                               a.out_vals, a.out_idx);
+  }
+  if (tid == 0) {
+    a.st->status = PROFK_STATUS_FILTERED;
+    if (a.info) {
+      a.info->count = total;
+      a.info->tau_key = tau;
+      a.info->status = PROFK_STATUS_FILTERED;
+      a.info->n_valid = kk;
+    }
+  }
+}
+
 template <int DT>
 __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
-  __shared__ FinShared sh;
+  __shared__ FinLds sh;
+  __shared__ SelectScratch fs;
+  __shared__ uint32_t seg_n[kSegs], seg_pre[kSegs + 1], flag;
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t key_max = KB == 32 ? 0xFFFFFFFFu : 0xFFFFu;
   const uint32_t tid = threadIdx.x, b = blockIdx.x;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
   if (!a.direct) {
-    if (tid < kSegs) sh.seg_n[tid] = a.seg_cnt[tid * kSegStride];
+    if (tid < kSegs) seg_n[tid] = a.seg_cnt[tid * kSegStride];
     __syncthreads();
     if (tid == 0) {
       uint32_t run = 0;
       for (int x = 0; x < kSegs; ++x) {
-        sh.seg_pre[x] = run;
-        run += sh.seg_n[x];
+        seg_pre[x] = run;
+        run += seg_n[x];
       }
-      sh.seg_pre[kSegs] = run;
+      seg_pre[kSegs] = run;
     }
     __syncthreads();
-    total = sh.seg_pre[kSegs];
+    total = seg_pre[kSegs];
     status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
     if (status == PROFK_STATUS_FILTERED) {
-      if (b != 0) return;
-      const uint32_t gmax = block_max<kFinBS>(tid < a.G_f ? a.blk_max[tid] : 0u, sh.sel.wsum);
-      const uint32_t tau = a.st->tau_key;
-      SegSrc src{a.seg_key, a.seg_idx, a.seg_cap, sh.seg_pre};
-      const uint32_t kk = min(a.k, total);
-      block_topk<kFinBS, kFinDigit>(src, total, kk, tau, max(gmax, tau), KB, sh.topk());
-      sort_write_any<DT, kFinBS>(sh.sortbuf, kk, a.k, reinterpret_cast<uint64_t*>(sh.cache), a.out_vals,
-                                 a.out_idx);
-      if (tid == 0) {
-        a.st->status = status;
-        if (a.info) {
-          a.info->count = total;
-          a.info->tau_key = tau;
-          a.info->status = static_cast<int32_t>(status);
-          a.info->n_valid = kk;
-        }
-      }
+      if (b == 0) finish_filtered<DT>(a, sh, seg_pre, total, fs);
       return;
     }
   }
@@ -480,9 +631,9 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   const uint32_t kb = min(a.k, nb);
   if (kb) {
     InputSrc<DT> src{a.values, lo};
-    block_topk<kFinBS, kFinDigit>(src, nb, kb, 0u, key_max, KB, sh.topk());
+    block_topk<kFinBS, kFinDigit>(src, nb, kb, 0u, key_max, KB, sh.gen.topk());
     for (uint32_t i = tid; i < kb; i += kFinBS) {
-      const uint64_t c = sh.sortbuf[i];
+      const uint64_t c = sh.gen.sortbuf[i];
       a.cand_key[static_cast<size_t>(b) * a.k + i] = comp_key(c);
       a.cand_idx[static_cast<size_t>(b) * a.k + i] = comp_idx(c);
     }
@@ -491,18 +642,19 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   // ... and the last block to finish merges the per-chunk results.
   __threadfence();
   __syncthreads();
-  if (tid == 0) sh.misc[1] = (atomicAdd(&a.st->ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
+  if (tid == 0) flag = (atomicAdd(&a.st->ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
   __syncthreads();
-  if (!sh.misc[1]) return;
+  if (!flag) return;
   __threadfence();
   const uint32_t cc = tid < gridDim.x ? a.cand_cnt[tid] : 0u;
   uint32_t R;
-  const uint32_t pre = block_excl_sum<kFinBS>(cc, sh.sel.wsum, &R);
-  if (tid < gridDim.x) sh.pre[tid] = pre;
+  const uint32_t pre = block_excl_sum<kFinBS>(cc, fs.wsum, &R);
+  if (tid < gridDim.x) sh.gen.pre[tid] = pre;
   __syncthreads();
-  RegionSrc src{a.cand_key, a.cand_idx, a.k, gridDim.x, R, sh.pre};
-  block_topk<kFinBS, kFinDigit>(src, R, a.k, 0u, key_max, KB, sh.topk());
-  sort_write_any<DT, kFinBS>(sh.sortbuf, a.k, a.k, reinterpret_cast<uint64_t*>(sh.cache), a.out_vals, a.out_idx);
+  RegionSrc src{a.cand_key, a.cand_idx, a.k, gridDim.x, R, sh.gen.pre};
+  block_topk<kFinBS, kFinDigit>(src, R, a.k, 0u, key_max, KB, sh.gen.topk());
+  sort_write_any<DT, kFinBS>(sh.gen.sortbuf, a.k, a.k, reinterpret_cast<uint64_t*>(sh.gen.cache), a.out_vals,
+                             a.out_idx);
   if (tid == 0) {
     a.st->status = status;
     if (a.info) {
@@ -594,6 +746,7 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
     L.off_cand_key = take(static_cast<size_t>(L.G_fb) * k * 4);
     L.off_cand_idx = take(static_cast<size_t>(L.G_fb) * k * 4);
     L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
+    L.off_fhist = take(static_cast<size_t>(kLogBins) * 4);
   }
   L.bytes = off;
   return L;
@@ -615,7 +768,8 @@ static hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t
   FilterArgs fa{c.values, c.n, head, nvec, vpb, L.seg_cap, st,
                 union_keys, union_keys ? L.union_n : 0u, static_cast<uint32_t>(c.plan->t),
                 at<uint32_t>(c.ws, L.off_segcnt), at<uint32_t>(c.ws, L.off_seg_key),
-                at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max)};
+                at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max),
+                L.big ? nullptr : at<uint32_t>(c.ws, L.off_fhist)};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
   hipLaunchKernelGGL(k_filter<DT>, dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
@@ -629,15 +783,16 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   CallState* st = at<CallState>(c.ws, L.off_state);
   uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
   const bool direct = p.mode == PROFK_MODE_DIRECT && !c.use_tau;
+  uint32_t* fhist = L.big ? nullptr : at<uint32_t>(c.ws, L.off_fhist);
   const uint32_t* union_for_filter = nullptr;
   hipError_t e;
   if (direct || c.use_tau) {
     hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream,
-                       InitArgs{st, seg_cnt, c.use_tau ? c.tau_key : 0u});
+                       InitArgs{st, seg_cnt, fhist, c.use_tau ? c.tau_key : 0u});
   } else {
     uint32_t* uk = at<uint32_t>(c.ws, L.off_union);
     SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
-                  L.tcap, uk, st, seg_cnt};
+                  L.tcap, uk, st, seg_cnt, fhist};
     hipLaunchKernelGGL(k_sample<DT>, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
     if (L.union_n <= kFiltTauMax) {
       union_for_filter = uk;
@@ -661,7 +816,8 @@ static hipError_t launch_flat_t(const FlatCall& c) {
                 seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
                 at<uint32_t>(c.ws, L.off_blk_max), st,
                 L.G_fb, L.chunk, at<uint32_t>(c.ws, L.off_cand_key), at<uint32_t>(c.ws, L.off_cand_idx),
-                at<uint32_t>(c.ws, L.off_cand_cnt), c.out_vals, c.out_idx, c.info};
+                at<uint32_t>(c.ws, L.off_cand_cnt), at<uint32_t>(c.ws, L.off_fhist),
+                c.out_vals, c.out_idx, c.info};
   hipLaunchKernelGGL(k_finish<DT>, dim3(L.G_fb), dim3(kFinBS), 0, c.stream, fa);
   return hipGetLastError();
 }
@@ -685,7 +841,8 @@ hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* b
   CallState* st = at<CallState>(c.ws, L.off_state);
   uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, InitArgs{st, seg_cnt, c.tau_key});
+  uint32_t* fhist = L.big ? nullptr : at<uint32_t>(c.ws, L.off_fhist);
+  hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, InitArgs{st, seg_cnt, fhist, c.tau_key});
   hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st, nullptr) : launch_filter<1>(c, st, nullptr);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_gather_buffer, dim3(1), dim3(1024), 0, c.stream, L.seg_cap, seg_cnt,

@@ -33,6 +33,9 @@ constexpr int kSegStride = 64;                // words between segment counters
 constexpr int kFinBS = 1024;
 constexpr int kFinMaxK = 4096;                // largest k of the one-block refinement
 constexpr int kFbMaxBlocks = 256;
+constexpr uint32_t kFinSlice = 1024;          // candidates a block histograms, at least
+constexpr uint32_t kFastCap = 8192;           // candidates the bucket refinement holds in LDS
+constexpr uint32_t kFastBucket = 128;         // largest bucket it ranks by comparison
 constexpr uint32_t kFbMinChunk = 8192;
 
 // Multi-block refinement for k > kFinMaxK.
@@ -52,6 +55,7 @@ struct FlatLayout {
   size_t off_state = 0, off_segcnt = 0, off_union = 0, off_blk_max = 0;
   size_t off_seg_key = 0, off_seg_idx = 0;
   size_t off_cand_key = 0, off_cand_idx = 0, off_cand_cnt = 0;
+  size_t off_fhist = 0;                       // log-bin histogram of the candidates
   bool big = false;                           // k > kFinMaxK: multi-block refinement
   uint32_t G_big = 0;
   size_t off_big_state = 0, off_ghist = 0, off_staging = 0, off_runs = 0;
