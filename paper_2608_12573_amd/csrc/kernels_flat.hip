@@ -134,9 +134,45 @@ struct TauArgs {
 };
 
 __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
+  constexpr int NW = kTauBS / kWave;
+  constexpr int E = 8;  // union keys per lane on the wave path
   __shared__ uint32_t cache[kTauCache];
   __shared__ SelectShared sel;
-  const uint32_t tid = threadIdx.x;
+  __shared__ uint32_t lists[NW][kWaveTopMax];
+  __shared__ uint32_t list_n[NW];
+  const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  if (a.t <= kWaveTopMax && a.n <= static_cast<uint32_t>(kTauBS * E)) {
+    // every wave keeps the top t of its share, wave 0 merges the lists
+    uint32_t v[E];
+    uint32_t valid = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const uint32_t i = w * (kWave * E) + e * kWave + lane;
+      v[e] = i < a.n ? a.keys[i] : 0u;
+      if (i < a.n) valid |= 1u << e;
+    }
+    uint32_t last = 0;
+    const uint32_t got = wave_top_t<E>(v, valid, a.t, lists[w], last);
+    if (lane == 0) list_n[w] = got;
+    __syncthreads();
+    if (w == 0) {
+      constexpr int E2 = NW * kWaveTopMax / kWave;
+      uint32_t v2[E2];
+      uint32_t valid2 = 0;
+#pragma unroll
+      for (int e = 0; e < E2; ++e) {
+        uint32_t c = lane + kWave * e, li = 0;
+        v2[e] = 0;
+#pragma unroll
+        for (int i = 0; i < NW; ++i)
+          if (li == static_cast<uint32_t>(i) && c >= list_n[i]) { c -= list_n[i]; li = i + 1; }
+        if (li < NW) { v2[e] = lists[li][c]; valid2 |= 1u << e; }
+      }
+      wave_top_t<E2>(v2, valid2, a.t, nullptr, last);
+      if (lane == 0) a.st->tau_key = last;
+    }
+    return;
+  }
   auto gload = [&](uint32_t i) { return a.keys[i]; };
   SelectResult r;
   if (a.n <= kTauCache) {
@@ -198,12 +234,46 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   const uint32_t seg = b & (kSegs - 1);
   if (tid == 0) s_cnt = 0;
 
+  // The block's first step is loaded before the threshold is known, so the
+  // loads are in flight while tau is chosen.
+  const u32x4* vec = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.values) +
+                                                    static_cast<size_t>(a.head) * ES);
+  const uint32_t vbeg = b * a.vpb;
+  const uint32_t vend = min(vbeg + a.vpb, a.nvec);
+  u32x4 v[kFiltU];
+  auto load_step = [&](uint32_t vb, uint32_t fill) {
+#pragma unroll
+    for (int u = 0; u < kFiltU; ++u) {
+      const uint32_t vi = vb + u * kFiltBS + tid;
+      if (vi < vend) v[u] = __builtin_nontemporal_load(vec + vi);
+      else v[u] = u32x4{fill, fill, fill, fill};
+    }
+  };
+  // 0xFFFFFFFF is the lowest key: it fails the fast test unless every key
+  // passes, and the exact test skips slots past the end anyway.
+  load_step(vbeg, 0xFFFFFFFFu);
+
   // ---- threshold (stage 2) when the sample union is small
   uint32_t tau;
   if (a.union_n) {
-    for (uint32_t i = tid; i < a.union_n; i += kFiltBS) s_union[i] = a.union_keys[i];
-    __syncthreads();
-    if (a.t <= kWaveTopMax) {
+    if (a.t <= kWaveTopMax && a.union_n <= kWave * kFiltTauWave) {
+      // one wave holds the whole union in registers
+      if (tid < kWave) {
+        uint32_t uk[kFiltTauWave];
+        uint32_t valid = 0;
+#pragma unroll
+        for (int e = 0; e < static_cast<int>(kFiltTauWave); ++e) {
+          const uint32_t i = lane + kWave * e;
+          uk[e] = i < a.union_n ? a.union_keys[i] : 0u;
+          if (i < a.union_n) valid |= 1u << e;
+        }
+        uint32_t last = 0;
+        wave_top_t<kFiltTauWave>(uk, valid, a.t, nullptr, last);
+        if (lane == 0) s_tau = last;
+      }
+    } else if (a.t <= kWaveTopMax) {
+      for (uint32_t i = tid; i < a.union_n; i += kFiltBS) s_union[i] = a.union_keys[i];
+      __syncthreads();
       // every wave keeps the top t of its share, wave 0 merges the lists
       constexpr int NW = kFiltBS / kWave;
       constexpr int E = kFiltTauMax / kFiltBS;
@@ -237,6 +307,8 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
         if (lane == 0) s_tau = last;
       }
     } else {
+      for (uint32_t i = tid; i < a.union_n; i += kFiltBS) s_union[i] = a.union_keys[i];
+      __syncthreads();
       const SelectResult r = block_select_kth<kFiltBS, kSelDigit>(
           [&](auto f) {
             for (uint32_t i = tid; i < a.union_n; i += kFiltBS) f(s_union[i]);
@@ -294,18 +366,8 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     }
   };
 
-  const u32x4* vec = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.values) +
-                                                    static_cast<size_t>(a.head) * ES);
-  const uint32_t vbeg = b * a.vpb;
-  const uint32_t vend = min(vbeg + a.vpb, a.nvec);
   for (uint32_t vb = vbeg; vb < vend; vb += kFiltBS * kFiltU) {
-    u32x4 v[kFiltU];
-#pragma unroll
-    for (int u = 0; u < kFiltU; ++u) {
-      const uint32_t vi = vb + u * kFiltBS + tid;
-      if (vi < vend) v[u] = __builtin_nontemporal_load(vec + vi);
-      else v[u] = u32x4{th.neutral, th.neutral, th.neutral, th.neutral};
-    }
+    if (vb != vbeg) load_step(vb, th.neutral);
     if (__ballot(tile_any<DT, kFiltU>(v, th)) == 0) continue;
     // Rare path: exact per-element test, one slot reservation per wave.
     const TileExact<DT, kFiltU, kFiltBS> tx{v, th, vb, vend, tid, a.head};
@@ -708,6 +770,21 @@ __global__ __launch_bounds__(1024) void k_gather_buffer(uint32_t cap, const uint
 static inline uint32_t cdiv(uint64_t a, uint64_t b) { return static_cast<uint32_t>((a + b - 1) / b); }
 static inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Filter workgroups one CU holds at once (the persistent grid is sized to
+// what is resident, so no workgroup starts after the others have finished).
+static int filter_blocks_per_cu(int dtype) {
+  static int cached[2] = {0, 0};
+  const int d = dtype == PROFK_F32 ? 0 : 1;
+  if (cached[d] == 0) {
+    int n = 0;
+    const hipError_t e = d == 0
+        ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0>, kFiltBS, 0)
+        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1>, kFiltBS, 0);
+    cached[d] = (e == hipSuccess && n > 0) ? (n < 4 ? n : 4) : 4;
+  }
+  return cached[d];
+}
+
 FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   FlatLayout L;
   const uint64_t N = static_cast<uint64_t>(p.N);
@@ -718,7 +795,8 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   L.tcap = t < static_cast<uint32_t>(kSampPerBlock) ? t : kSampPerBlock;
   const uint32_t last_nb = S - (L.G_s - 1) * kSampPerBlock;
   L.union_n = (L.G_s - 1) * L.tcap + (t < last_nb ? t : last_nb);
-  const uint32_t maxg = static_cast<uint32_t>(num_cus * 4 < kFiltMaxBlocks ? num_cus * 4 : kFiltMaxBlocks);
+  const int per_cu = filter_blocks_per_cu(dtype);
+  const uint32_t maxg = static_cast<uint32_t>(num_cus * per_cu < kFiltMaxBlocks ? num_cus * per_cu : kFiltMaxBlocks);
   uint32_t g = cdiv(cdiv(N, epv), kFiltBS * kFiltU);
   L.G_f = g < 1 ? 1 : (g > maxg ? maxg : g);
   L.seg_cap = M;
@@ -794,7 +872,7 @@ static hipError_t launch_flat_t(const FlatCall& c) {
     SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
                   L.tcap, uk, st, seg_cnt, fhist};
     hipLaunchKernelGGL(k_sample<DT>, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
-    if (L.union_n <= kFiltTauMax) {
+    if (L.union_n <= kFiltTauMax && static_cast<uint32_t>(p.t) <= kFiltTauInMaxT) {
       union_for_filter = uk;
     } else {
       TauArgs ta{uk, L.union_n, static_cast<uint32_t>(p.t), Elem<DT>::KEYBITS, st};
