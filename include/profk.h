@@ -137,8 +137,8 @@ int profk_topk_simple(const float* values, int64_t N, int64_t k, uint64_t seed,
  * `row_plan` comes from profk_plan_rows(D, k, ...).  info_dev is NULL or an
  * array of B reports.  One workgroup handles a row entirely in LDS, so `ws`
  * is not used (NULL, 0 are accepted).  Limits: k <= 1024 and a plan whose
- * sample and buffer fit the row block's LDS (4*max(S, M) + 4*M bytes plus
- * about 9 KiB within 144 KiB; PROFK_EINVAL otherwise). */
+ * sample and buffer fit the row block's LDS (4*max(S, M) + 4*M + 16*k
+ * bytes plus about 14 KiB, within 144 KiB; PROFK_EINVAL otherwise). */
 int profk_topk_rows(const profk_plan_t* row_plan, int32_t dtype,
                     const void* values, int64_t B, int64_t D,
                     int64_t row_stride, int64_t k, uint64_t seed,

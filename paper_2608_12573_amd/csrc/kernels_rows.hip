@@ -2,11 +2,14 @@
 // batch element).  One workgroup owns one row and runs all four stages in
 // LDS:
 //   1. draw S indices of the row (Philox counter word 1 = row);
-//   2. tau = t-th largest sampled key;
+//   2. tau = t-th largest sampled key (radix select in LDS);
 //   3. stream the row once with 16-byte loads, appending survivors to an
-//      LDS buffer of capacity M and counting all of them;
-//   4. k_req <= count <= M: exact top-k of the buffer; otherwise the exact
-//      top-k of the row itself (per-row fallback, no second launch).
+//      LDS buffer of capacity M, counting all of them and histogramming them
+//      by log_bin(key - tau);
+//   4. k_req <= count <= M: the survivors at or above the bucket of rank k
+//      are ranked within their buckets and written directly (the radix
+//      refinement when those buckets are large); otherwise the exact top-k
+//      of the row itself (per-row fallback, no second launch).
 // The LDS layout is sized from the plan at launch (dynamic shared memory).
 #include "device_common.h"
 #include "filter_tile.h"
@@ -15,7 +18,7 @@
 
 namespace profk {
 
-constexpr int kRowDigit = 11;
+constexpr int kRowDigit = 11;  // radix digit of the refinement and fallback
 
 struct RowArgs {
   const void* values;
@@ -32,18 +35,20 @@ struct RowArgs {
 template <int DT>
 __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV, KB = Elem<DT>::KEYBITS;
+  constexpr int kSelDigitRow = KB == 16 ? 8 : 11;  // sample select: 2 or 3 passes
   constexpr int NW = kRowBS / kWave;
+  constexpr uint32_t RB = kLogBins / kRowBS;        // log bins owned per thread
+  static_assert(kLogBins % kRowBS == 0, "log-bin ownership");
   extern __shared__ __align__(16) uint8_t smem[];
   uint32_t* const samp = reinterpret_cast<uint32_t*>(smem + a.L.off_a);  // samples, then buffer keys
   uint32_t* const bkey = samp;
   uint32_t* const bidx = reinterpret_cast<uint32_t*>(smem + a.L.off_b);
   uint32_t* const hist = reinterpret_cast<uint32_t*>(smem + a.L.off_hist);
   uint64_t* const collect = reinterpret_cast<uint64_t*>(smem + a.L.off_collect);
+  uint64_t* const comp = reinterpret_cast<uint64_t*>(smem + a.L.off_comp);
   uint64_t* const exch = reinterpret_cast<uint64_t*>(smem + a.L.off_a);      // after the buffer is done
   __shared__ SelectScratch scr;
-  __shared__ uint32_t lists[NW][kWaveTopMax];
-  __shared__ uint32_t list_n[NW];
-  __shared__ uint32_t s_cnt, s_tau, s_counter, s_wmax[NW];
+  __shared__ uint32_t s_cnt, s_counter, s_wmax[NW];
 
   const uint32_t r = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const char* row = static_cast<const char*>(a.values) + static_cast<size_t>(r) * a.row_stride * ES;
@@ -54,58 +59,41 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
 
   uint32_t status = PROFK_STATUS_DIRECT, count = 0, tau = 0, gmax = 0;
   if (!a.direct) {
-    // 1. sample
-    for (uint32_t blk = tid; 4 * blk < a.S; blk += kRowBS) {
-      const U64x4 rnd = philox4x64_10(blk, r, 0, 0, a.seed, 0);
+    // 1. sample: the Philox words first, then all gathers in flight at once
+    for (uint32_t blk0 = 0; 4 * blk0 < a.S; blk0 += 2 * kRowBS) {
+      U64x4 rnd[2];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t j = 4 * blk + q;
-        if (j < a.S) samp[j] = key_of<DT>(load_raw<DT>(row, index_of_word(rnd.w[q], a.D)));
+      for (int q = 0; q < 2; ++q) {
+        const uint32_t blk = blk0 + q * kRowBS + tid;
+        if (4 * blk < a.S) rnd[q] = philox4x64_10(blk, r, 0, 0, a.seed, 0);
       }
+      uint32_t raw[8];
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const uint32_t j = 4 * (blk0 + q * kRowBS + tid) + x;
+          raw[4 * q + x] = j < a.S ? load_raw<DT>(row, index_of_word(rnd[q].w[x], a.D)) : 0u;
+        }
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const uint32_t j = 4 * (blk0 + q * kRowBS + tid) + x;
+          if (j < a.S) samp[j] = key_of<DT>(raw[4 * q + x]);
+        }
     }
     if (tid == 0) s_cnt = 0;
     __syncthreads();
     // 2. threshold
-    if (a.t <= kWaveTopMax && a.S <= kRowWaveSample) {
-      constexpr int E = kRowWaveSample / kRowBS;
-      uint32_t sk[E];
-      uint32_t valid = 0;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint32_t i = tid + kRowBS * e;
-        sk[e] = i < a.S ? samp[i] : 0u;
-        if (i < a.S) valid |= 1u << e;
-      }
-      uint32_t last = 0;
-      const uint32_t got = wave_top_t<E>(sk, valid, a.t, lists[w], last);
-      if (lane == 0) list_n[w] = got;
-      __syncthreads();
-      if (w == 0) {
-        constexpr int E2 = NW * kWaveTopMax / kWave;
-        uint32_t v2[E2];
-        uint32_t valid2 = 0;
-#pragma unroll
-        for (int e = 0; e < E2; ++e) {
-          uint32_t c = lane + kWave * e, li = 0;
-          v2[e] = 0;
-#pragma unroll
-          for (int i = 0; i < NW; ++i)
-            if (li == static_cast<uint32_t>(i) && c >= list_n[i]) { c -= list_n[i]; li = i + 1; }
-          if (li < NW) { v2[e] = lists[li][c]; valid2 |= 1u << e; }
-        }
-        wave_top_t<E2>(v2, valid2, a.t, nullptr, last);
-        if (lane == 0) s_tau = last;
-      }
-    } else {
-      const SelectResult sr = block_select_kth<kRowBS, kRowDigit>(
-          [&](auto f) {
-            for (uint32_t i = tid; i < a.S; i += kRowBS) f(samp[i]);
-          },
-          a.t, KB, 0u, hist, scr);
-      if (tid == 0) s_tau = sr.kth;
-    }
+    tau = block_select_kth<kRowBS, kSelDigitRow>(
+              [&](auto f) {
+                for (uint32_t i = tid; i < a.S; i += kRowBS) f(samp[i]);
+              },
+              a.t, KB, 0u, hist, scr)
+              .kth;
+    for (uint32_t i = tid; i < kLogBins; i += kRowBS) hist[i] = 0;
     __syncthreads();
-    tau = s_tau;
 
     // 3. filter the row into the LDS buffer (which reuses the sample space)
     const Thresh<DT> th(tau);
@@ -119,6 +107,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
     };
     auto store = [&](uint32_t slot, uint32_t key, uint32_t idx) {
       my_max = max(my_max, key);
+      atomicAdd(&hist[log_bin(key - tau)], 1u);
       if (slot < a.M) {
         bkey[slot] = key;
         bidx[slot] = idx;
@@ -170,13 +159,73 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
 
   // 4. refinement, or the exact per-row fallback
   uint32_t kk = a.k;
+  bool done = false;
   if (status == PROFK_STATUS_FILTERED) {
     kk = min(a.k, count);
-    block_topk<kRowBS, kRowDigit>(LdsSrc{bkey, bidx}, count, kk, tau, max(gmax, tau), KB, sm);
+    // Bucket offsets in descending bucket order, in place: thread t owns
+    // buckets [kLogBins - RB(t+1), kLogBins - RB t).
+    const uint32_t bb = kLogBins - RB * (tid + 1);
+    uint32_t h[RB];
+    uint32_t s = 0;
+#pragma unroll
+    for (uint32_t j = 0; j < RB; ++j) {
+      h[j] = hist[bb + j];
+      s += h[j];
+    }
+    uint32_t run = block_excl_sum<kRowBS>(s, scr.wsum, nullptr);
+#pragma unroll
+    for (int j = static_cast<int>(RB) - 1; j >= 0; --j) {
+      hist[bb + j] = run;
+      if (run < kk && kk <= run + h[j]) {
+        scr.found[0] = bb + j;
+        scr.found[1] = run;
+        scr.found[2] = h[j];
+      }
+      run += h[j];
+    }
+    __syncthreads();
+    const uint32_t bstar = scr.found[0], n_sel = scr.found[1] + scr.found[2];
+    uint32_t big = 0;
+#pragma unroll
+    for (uint32_t j = 0; j < RB; ++j)
+      if (bb + j >= bstar) big = max(big, h[j]);
+    big = block_max<kRowBS>(big, scr.wsum);
+    if (n_sel <= a.k + kFastBucket && big <= kFastBucket) {
+      // place the buckets >= b*: afterwards hist[b] is the end of bucket b
+      // and hist[b + 1] its start
+      for (uint32_t i = tid; i < count; i += kRowBS) {
+        const uint32_t key = bkey[i];
+        const uint32_t bin = log_bin(key - tau);
+        if (bin >= bstar) comp[atomicAdd(&hist[bin], 1u)] = composite(key, bidx[i]);
+      }
+      __syncthreads();
+      for (uint32_t p = tid; p < n_sel; p += kRowBS) {
+        const uint64_t c = comp[p];
+        const uint32_t bin = log_bin(comp_key(c) - tau);
+        const uint32_t s0 = bin + 1 < kLogBins ? hist[bin + 1] : 0u, s1 = hist[bin];
+        uint32_t rank = 0;
+        for (uint32_t q = s0; q < s1; ++q) rank += comp[q] > c ? 1u : 0u;
+        const uint32_t dst = s0 + rank;
+        if (dst < kk) {
+          const uint32_t bits = bits_of_key<DT>(comp_key(c));
+          if (DT == 0) static_cast<uint32_t*>(out_vals)[dst] = bits;
+          else static_cast<uint16_t*>(out_vals)[dst] = static_cast<uint16_t>(bits);
+          out_idx[dst] = comp_idx(c);
+        }
+      }
+      for (uint32_t p = kk + tid; p < a.k; p += kRowBS) {  // relaxed recall: padding
+        if (DT == 0) static_cast<uint32_t*>(out_vals)[p] = 0xFF800000u;
+        else static_cast<uint16_t*>(out_vals)[p] = 0xFF80u;
+        out_idx[p] = -1;
+      }
+      done = true;
+    } else {
+      block_topk<kRowBS, kRowDigit>(LdsSrc{bkey, bidx}, count, kk, tau, max(gmax, tau), KB, sm);
+    }
   } else {
     block_topk<kRowBS, kRowDigit>(InputSrc<DT>{row, 0u}, a.D, a.k, 0u, key_max, KB, sm);
   }
-  sort_write_any<DT, kRowBS>(collect, kk, a.k, exch, out_vals, out_idx);
+  if (!done) sort_write_any<DT, kRowBS>(collect, kk, a.k, exch, out_vals, out_idx);
   if (a.info && tid == 0) {
     profk_info_t* inf = a.info + r;
     inf->count = count;
@@ -199,11 +248,13 @@ RowLayout row_layout(const profk_plan_t& p) {
   const uint32_t b_bytes = align16(M * 4u);
   uint32_t a_bytes = align16((S > M ? S : M) * 4u);
   if (a_bytes + b_bytes < exch) a_bytes = exch - b_bytes;
+  const uint32_t hist_words = (1u << kRowDigit) > kLogBins ? (1u << kRowDigit) : kLogBins;
   L.off_a = 0;
   L.off_b = a_bytes;
   L.off_hist = L.off_b + b_bytes;
-  L.off_collect = L.off_hist + align16((1u << kRowDigit) * 4u);
-  L.bytes = L.off_collect + align16(k * 8u);
+  L.off_collect = L.off_hist + align16(hist_words * 4u);
+  L.off_comp = L.off_collect + align16(k * 8u);
+  L.bytes = L.off_comp + align16((k + kFastBucket) * 8u);
   return L;
 }
 

@@ -109,14 +109,13 @@ hipError_t launch_big(const BigCall& c);
 // Per-row kernel: one workgroup per row, everything in LDS.
 constexpr int kRowBS = 256;                   // threads of a row block
 constexpr int kRowU = 8;                      // 16-byte loads in flight per lane
-constexpr uint32_t kRowWaveSample = 4096;     // largest S of the wave-level threshold
 constexpr int kRowMaxK = 4 * kRowBS;          // largest k per row
 constexpr uint32_t kRowMaxLds = 144 * 1024;   // dynamic LDS the row layout may use
 
 // Dynamic LDS of a row block: region a holds the sample keys and then the
 // buffer keys (and, last, the sort exchange), region b the buffer indices.
 struct RowLayout {
-  uint32_t off_a = 0, off_b = 0, off_hist = 0, off_collect = 0, bytes = 0;
+  uint32_t off_a = 0, off_b = 0, off_hist = 0, off_collect = 0, off_comp = 0, bytes = 0;
 };
 
 RowLayout row_layout(const profk_plan_t& plan);
