@@ -425,6 +425,72 @@ __device__ __forceinline__ uint32_t log_bin(uint32_t d) {
   return (e - 6u) * 128u + ((d >> (e - 7u)) & 127u);
 }
 
+// Bitonic sort, descending, of P = E*T 64-bit values held E per thread in
+// blocked order (thread t holds positions t*E .. t*E+E-1).  Strides below E
+// are swaps within a thread, strides up to 32*E shuffles within a wave,
+// larger ones go through `lds` (P values).  Waves holding no position only
+// take part in the barriers.  Every thread of the block must call it with
+// the same P (a power of two, at least E).
+template <int E, int S>
+__device__ __forceinline__ void bitonic_regs_step(uint64_t (&v)[E], uint32_t t, uint32_t size) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    if ((e & S) == 0) {
+      const uint32_t p = t * E + static_cast<uint32_t>(e);
+      const bool desc = (p & size) == 0;
+      const uint64_t x = v[e], y = v[e | S];
+      const bool sw = desc ? (x < y) : (x > y);
+      v[e] = sw ? y : x;
+      v[e | S] = sw ? x : y;
+    }
+  }
+}
+
+template <int E>
+__device__ __forceinline__ void bitonic_blocked_desc(uint64_t (&v)[E], uint32_t P, uint64_t* lds) {
+  static_assert(E == 1 || E == 2 || E == 4 || E == 8 || E == 16, "elements per thread");
+  const uint32_t t = threadIdx.x;
+  const bool act = t * E < P;
+  const bool wave_act = (t & ~static_cast<uint32_t>(kWave - 1)) * E < P;
+  for (uint32_t size = 2; size <= P; size <<= 1) {
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride < static_cast<uint32_t>(E)) {
+        if (!wave_act) continue;
+        if (E > 8 && stride == 8) bitonic_regs_step<E, (E > 8 ? 8 : 0)>(v, t, size);
+        else if (E > 4 && stride == 4) bitonic_regs_step<E, (E > 4 ? 4 : 0)>(v, t, size);
+        else if (E > 2 && stride == 2) bitonic_regs_step<E, (E > 2 ? 2 : 0)>(v, t, size);
+        else if (E > 1 && stride == 1) bitonic_regs_step<E, (E > 1 ? 1 : 0)>(v, t, size);
+        continue;
+      }
+      const uint32_t d = stride / E;  // partner thread distance
+      const bool lower = (t & d) == 0;
+      const bool desc = ((t * E) & size) == 0;
+      if (d < static_cast<uint32_t>(kWave)) {
+        if (!wave_act) continue;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const uint64_t o = shfl_xor_u64(v[e], static_cast<int>(d));
+          v[e] = (lower == desc) ? max(v[e], o) : min(v[e], o);
+        }
+      } else {
+        __syncthreads();
+        if (act) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) lds[t * E + e] = v[e];
+        }
+        __syncthreads();
+        if (act) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const uint64_t o = lds[(t * E + e) ^ stride];
+            v[e] = (lower == desc) ? max(v[e], o) : min(v[e], o);
+          }
+        }
+      }
+    }
+  }
+}
+
 // Composite ordering key: larger key first, then smaller index.
 __device__ __forceinline__ uint64_t composite(uint32_t key, uint32_t idx) {
   return (static_cast<uint64_t>(key) << 32) | static_cast<uint64_t>(~idx);

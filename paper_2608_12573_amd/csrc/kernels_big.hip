@@ -2,7 +2,17 @@
 // BatchTopK case of Sec. 5: K = B*k of a flattened latent matrix).
 //
 // Same result as the one-block path -- the exact top-k under the total
-// order, sorted -- computed across the GPU:
+// order, sorted -- computed across the GPU.  A filtered call whose
+// candidates spread over small buckets takes the bucket path:
+//   k_bkt_plan     status; bucket offsets in descending bucket order from
+//                  the filter's histogram of log_bin(key - tau), and the
+//                  bucket b* holding rank k;
+//   k_bkt_scatter  every candidate of a bucket >= b* into its bucket's range
+//                  of the staging array;
+//   k_bkt_sort     one block per bucket sorts it in LDS and writes the
+//                  outputs at the bucket's offset.
+// Every other call (a fallback, DIRECT, or a bucket larger than kBktCap)
+// takes the radix path, whose kernels return at once after a bucket call:
 //   k_big_begin    status from the candidate counts; the source is the
 //                  candidate segments, or the whole input on fallback.
 //   k_big_pass     one radix digit per launch: block histograms are merged
@@ -38,8 +48,12 @@ struct BigState {
   uint32_t istar;
   uint32_t ticket;
   uint32_t out_count;
-  uint32_t pad[45];
+  uint32_t mode;       // kModeRadix or kModeBucket
+  uint32_t bstar;      // bucket path: the bucket holding rank kk
+  uint32_t nlist;      // bucket path: entries of the bucket list
+  uint32_t pad[42];
 };
+constexpr uint32_t kModeRadix = 0, kModeBucket = 1;
 static_assert(sizeof(BigState) <= 256, "state size");
 
 struct BigArgs {
@@ -53,6 +67,10 @@ struct BigArgs {
   uint32_t* ghist;     // kBigBins
   uint64_t* staging;   // P
   uint64_t* runs;      // P
+  const uint32_t* fhist;  // kLogBins: the filter's histogram of log_bin(key - tau)
+  uint32_t* boff;      // kLogBins: first slot of each bucket (descending order)
+  uint32_t* bcur;      // kLogBins * kBktPad: entries placed in bucket b at b * kBktPad
+  uint32_t* blist;     // kLogBins: the non-empty buckets >= b*, descending
   uint32_t P;          // padded length: k rounded up to kBigTile
   void* out_vals;
   int64_t* out_idx;
@@ -119,6 +137,245 @@ __device__ __forceinline__ void load_segn(const BigArgs& a, uint32_t* segn) {
   __syncthreads();
 }
 
+// ----------------------------------------------------------- bucket path ---
+template <int DT>
+__global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
+  __shared__ SelectScratch fs;
+  __shared__ uint32_t s_total;
+  BigState* s = a.bs;
+  const uint32_t tid = threadIdx.x;
+  uint32_t total = 0, status = PROFK_STATUS_DIRECT;
+  if (!a.direct) {
+    if (tid == 0) {
+      uint32_t t = 0;
+      for (int x = 0; x < kSegs; ++x) t += a.seg_cnt[x * kSegStride];
+      s_total = t;
+    }
+    __syncthreads();
+    total = s_total;
+    status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
+                             : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
+  }
+  if (status != PROFK_STATUS_FILTERED) {
+    if (tid == 0) s->mode = kModeRadix;
+    return;
+  }
+  const uint32_t kk = min(a.k, total);
+  // Bucket offsets in descending bucket order: thread t owns buckets
+  // [kLogBins - 4(t+1), kLogBins - 4t).
+  constexpr uint32_t kOwners = kLogBins / 4;
+  static_assert(kLogBins % 4 == 0 && kOwners <= 1024, "bucket ownership");
+  uint32_t h[4] = {0u, 0u, 0u, 0u};
+  const uint32_t bbase = kLogBins - 4 * (tid + 1);
+  if (tid < kOwners) {
+    const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
+    h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
+  }
+  const uint32_t above_me = block_excl_sum<1024>(h[0] + h[1] + h[2] + h[3], fs.wsum, nullptr);
+  if (tid < kOwners) {
+    uint32_t run = above_me;
+#pragma unroll
+    for (int j = 3; j >= 0; --j) {
+      a.boff[bbase + j] = run;
+      a.bcur[(bbase + j) * kBktPad] = 0;
+      if (run < kk && kk <= run + h[j]) fs.found[0] = bbase + j;
+      run += h[j];
+    }
+  }
+  __syncthreads();
+  const uint32_t bstar = fs.found[0];
+  uint32_t big = 0, nonempty = 0;
+  if (tid < kOwners) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (bbase + j >= bstar) {
+        big = max(big, h[j]);
+        nonempty += h[j] ? 1u : 0u;
+      }
+  }
+  // the list of non-empty buckets >= b*, in descending bucket order
+  uint32_t nlist = 0;
+  uint32_t lpos = block_excl_sum<1024>(nonempty, fs.wsum, &nlist);
+  if (tid < kOwners) {
+#pragma unroll
+    for (int j = 3; j >= 0; --j)
+      if (bbase + j >= bstar && h[j]) a.blist[lpos++] = bbase + j;
+  }
+  big = block_max<1024>(big, fs.wsum);
+  const bool bucket = big <= kBktCap;
+  if (tid == 0) {
+    s->mode = bucket ? kModeBucket : kModeRadix;
+    s->bstar = bstar;
+    s->nlist = nlist;
+    s->status = status;
+    s->total = total;
+    s->tau = a.st->tau_key;
+    s->n_src = total;
+    s->from_input = 0;
+    s->kk = kk;
+  }
+  if (!bucket) return;
+  for (uint32_t p = kk + tid; p < a.k; p += 1024) {  // relaxed recall: padding
+    if (DT == 0) static_cast<uint32_t*>(a.out_vals)[p] = 0xFF800000u;
+    else static_cast<uint16_t*>(a.out_vals)[p] = 0xFF80u;
+    a.out_idx[p] = -1;
+  }
+  if (tid == 0 && a.info) {
+    a.info->count = total;
+    a.info->tau_key = a.st->tau_key;
+    a.info->status = static_cast<int32_t>(status);
+    a.info->n_valid = kk;
+  }
+}
+
+// Candidates are placed sweep by sweep: a block counts one sweep's items per
+// bucket in LDS, reserves each bucket's range with one global atomic, and
+// writes every item at its range base plus its rank within the block.
+constexpr int kScatBS = 1024, kScatU = 4;
+
+template <int DT>
+__global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
+  __shared__ uint32_t hist[kLogBins];  // counts of the sweep, then its range bases
+  __shared__ uint32_t segn[kSegs];
+  const BigState* s = a.bs;
+  if (s->mode != kModeBucket) return;
+  const uint32_t tid = threadIdx.x, n = s->total, tau = s->tau, bstar = s->bstar;
+  load_segn(a, segn);
+  const SegPos pos{segn, a.seg_cap};
+  constexpr uint32_t per = kScatBS * kScatU;
+  for (uint32_t base = blockIdx.x * per; base < n; base += gridDim.x * per) {
+    for (uint32_t b = tid; b < kLogBins; b += kScatBS) hist[b] = 0;
+    __syncthreads();
+    uint32_t key[kScatU], idx[kScatU], bin[kScatU], rank[kScatU];
+#pragma unroll
+    for (int u = 0; u < kScatU; ++u) {
+      const uint32_t i = base + u * kScatBS + tid;
+      key[u] = 0;
+      idx[u] = 0;
+      if (i < n) {
+        const size_t p = pos(i);
+        key[u] = a.seg_key[p];
+        idx[u] = a.seg_idx[p];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kScatU; ++u) {
+      const uint32_t i = base + u * kScatBS + tid;
+      bin[u] = i < n ? log_bin(key[u] - tau) : 0u;
+      rank[u] = (i < n && bin[u] >= bstar) ? atomicAdd(&hist[bin[u]], 1u) : 0u;
+    }
+    __syncthreads();
+    for (uint32_t b = tid; b < kLogBins; b += kScatBS) {
+      const uint32_t c = hist[b];
+      if (c) hist[b] = a.boff[b] + atomicAdd(&a.bcur[b * kBktPad], c);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kScatU; ++u) {
+      const uint32_t i = base + u * kScatBS + tid;
+      if (i < n && bin[u] >= bstar) a.staging[hist[bin[u]] + rank[u]] = composite(key[u], idx[u]);
+    }
+    __syncthreads();
+  }
+}
+
+// The bucket-sort blocks loop over the bucket list.  A bucket b >= 128
+// holds the distances d = key - tau in [dlo(b), dlo(b) + 2^(e-7)), e =
+// b/128 + 6; it is split into 256 sub-bins by the next 8 bits of d - dlo,
+// counted and placed in LDS in descending sub-bin order, and each item is
+// ranked within its sub-bin by comparison (a bucket b < 128 holds a single
+// key, so it is one sub-bin).  A bucket whose largest sub-bin exceeds
+// kSubMax is sorted whole instead (blocked bitonic sort).
+constexpr int kSortBS = 256;
+constexpr uint32_t kSubBins = 256, kSubMax = 64;
+
+__device__ __forceinline__ uint32_t sub_bin(uint32_t d, uint32_t b) {
+  if (b < 128u) return 0u;
+  const uint32_t e = (b >> 7) + 6u;                       // d in [2^e, 2^(e+1))
+  const uint32_t dlo = (128u + (b & 127u)) << (e - 7u);  // bucket start
+  const uint32_t shift = e > 15u ? e - 15u : 0u;          // bucket width 2^(e-7) -> 256 sub-bins
+  return (d - dlo) >> shift;
+}
+
+template <int DT>
+__device__ __forceinline__ void bkt_write(const BigArgs& a, uint32_t dst, uint64_t c) {
+  const uint32_t bits = bits_of_key<DT>(comp_key(c));
+  if (DT == 0) static_cast<uint32_t*>(a.out_vals)[dst] = bits;
+  else static_cast<uint16_t*>(a.out_vals)[dst] = static_cast<uint16_t>(bits);
+  a.out_idx[dst] = comp_idx(c);
+}
+
+template <int DT>
+__global__ __launch_bounds__(kSortBS) void k_bkt_sort(BigArgs a) {
+  constexpr int PER = kBktCap / kSortBS;  // items per thread
+  __shared__ uint64_t A[kBktCap], Bv[kBktCap];
+  __shared__ uint32_t cnt[kSubBins], off[kSubBins];
+  __shared__ SelectScratch scr;
+  const BigState* s = a.bs;
+  if (s->mode != kModeBucket) return;
+  const uint32_t kk = s->kk, nlist = s->nlist, tau = s->tau, t = threadIdx.x;
+  for (uint32_t l = blockIdx.x; l < nlist; l += gridDim.x) {
+    const uint32_t b = a.blist[l];
+    const uint32_t m = a.bcur[b * kBktPad], start = a.boff[b];
+    if (start >= kk) continue;
+    cnt[t] = 0;
+    __syncthreads();
+    uint32_t rk[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const uint32_t i = u * kSortBS + t;
+      rk[u] = 0;
+      if (i < m) {
+        const uint64_t c = a.staging[start + i];
+        A[i] = c;
+        rk[u] = atomicAdd(&cnt[sub_bin(comp_key(c) - tau, b)], 1u);
+      }
+    }
+    __syncthreads();
+    // descending sub-bin order: thread t owns sub-bin 255 - t
+    const uint32_t mine = cnt[kSubBins - 1 - t];
+    const uint32_t before = block_excl_sum<kSortBS>(mine, scr.wsum, nullptr);
+    off[kSubBins - 1 - t] = before;
+    const uint32_t biggest = block_max<kSortBS>(mine, scr.wsum);  // (syncs: off is visible after)
+    if (biggest <= kSubMax) {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const uint32_t i = u * kSortBS + t;
+        if (i < m) Bv[off[sub_bin(comp_key(A[i]) - tau, b)] + rk[u]] = A[i];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const uint32_t p = u * kSortBS + t;
+        if (p < m) {
+          const uint64_t c = Bv[p];
+          const uint32_t sb = sub_bin(comp_key(c) - tau, b);
+          const uint32_t s0 = off[sb], s1 = s0 + cnt[sb];
+          uint32_t r = 0;
+          for (uint32_t q = s0; q < s1; ++q) r += Bv[q] > c ? 1u : 0u;
+          if (start + s0 + r < kk) bkt_write<DT>(a, start + s0 + r, c);
+        }
+      }
+    } else {
+      constexpr int E = kBktCap / kSortBS;  // 16
+      uint64_t v[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t p = t * E + e;
+        v[e] = p < m ? A[p] : 0ull;
+      }
+      __syncthreads();
+      bitonic_blocked_desc<E>(v, max(static_cast<uint32_t>(E), next_pow2(m)), Bv);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t p = t * E + e;
+        if (p < m && start + p < kk) bkt_write<DT>(a, start + p, v[e]);
+      }
+    }
+    __syncthreads();  // the next bucket reuses the LDS
+  }
+}
+
 // ---------------------------------------------------------------- begin ---
 template <int DT>
 __global__ __launch_bounds__(1024) void k_big_begin(BigArgs a) {
@@ -127,6 +384,7 @@ __global__ __launch_bounds__(1024) void k_big_begin(BigArgs a) {
   __shared__ uint32_t s_total;
   const uint32_t tid = threadIdx.x;
   BigState* s = a.bs;
+  if (s->mode == kModeBucket) return;
   for (uint32_t i = tid; i < kBigBins; i += 1024) a.ghist[i] = 0;
   uint32_t status = PROFK_STATUS_DIRECT, total = 0;
   if (!a.direct) {
@@ -190,6 +448,7 @@ __global__ __launch_bounds__(kBigBS) void k_big_pass(BigArgs a) {
   __shared__ uint32_t wsum[20];
   __shared__ uint32_t s_last, s_found[3];
   BigState* s = a.bs;
+  if (s->mode == kModeBucket) return;
   const int hi = STAGE == 0 ? s->hi : s->ihi;
   if (hi <= 0 || (STAGE == 1 && !s->cut)) return;  // uniform: nothing left to resolve
   const uint32_t tid = threadIdx.x;
@@ -271,6 +530,7 @@ __global__ __launch_bounds__(kBigBS) void k_big_collect(BigArgs a) {
   __shared__ uint32_t segn[kSegs];
   __shared__ uint32_t s_cnt, s_base;
   const BigState* s = a.bs;
+  if (s->mode == kModeBucket) return;
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1);
   const uint32_t kstar = s->kstar, istar = s->istar, cut = s->cut;
   if (tid == 0) s_cnt = 0;
@@ -312,6 +572,7 @@ __global__ __launch_bounds__(kBigBS) void k_big_collect(BigArgs a) {
 // padding (0, below every real composite).
 __global__ __launch_bounds__(1024) void k_big_tile(BigArgs a) {
   __shared__ uint64_t exch[2 * kBigTile];
+  if (a.bs->mode == kModeBucket) return;
   const uint32_t kk = a.bs->kk;
   const uint32_t t0 = blockIdx.x * kBigTile;
   constexpr int E = kBigTile / 1024;
@@ -363,9 +624,11 @@ __device__ __forceinline__ uint32_t corank_wave(const uint64_t* A, uint32_t la, 
   return lo;
 }
 
-__global__ __launch_bounds__(1024) void k_big_merge(const uint64_t* in, uint64_t* out, uint32_t P, uint32_t L) {
+__global__ __launch_bounds__(1024) void k_big_merge(const BigState* bs, const uint64_t* in, uint64_t* out,
+                                                    uint32_t P, uint32_t L) {
   __shared__ uint64_t sa[kBigTile], sb[kBigTile];
   __shared__ uint32_t s_i[2];
+  if (bs->mode == kModeBucket) return;
   const uint32_t tid = threadIdx.x;
   const uint32_t o_begin = blockIdx.x * kBigTile;
   const uint32_t pair0 = (o_begin / (2 * L)) * (2 * L);
@@ -408,6 +671,7 @@ __global__ __launch_bounds__(1024) void k_big_merge(const uint64_t* in, uint64_t
 template <int DT>
 __global__ void k_big_write(BigArgs a, const uint64_t* sorted) {
   const BigState* s = a.bs;
+  if (s->mode == kModeBucket) return;
   const uint32_t kk = s->kk;
   const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < a.k) {
@@ -441,8 +705,11 @@ static hipError_t launch_big_t(const BigCall& c) {
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t P = cdiv_u(c.k, kBigTile) * kBigTile;
   BigArgs a{c.values, c.n, c.k, c.k_req, c.M, c.direct, c.seg_cnt, c.seg_key, c.seg_idx, c.blk_max,
-            c.seg_cap, c.G_f, c.st, reinterpret_cast<BigState*>(c.big_state), c.ghist, c.staging, c.runs, P,
-            c.out_vals, c.out_idx, c.info};
+            c.seg_cap, c.G_f, c.st, reinterpret_cast<BigState*>(c.big_state), c.ghist, c.staging, c.runs,
+            c.fhist, c.boff, c.bcur, c.blist, P, c.out_vals, c.out_idx, c.info};
+  hipLaunchKernelGGL(k_bkt_plan<DT>, dim3(1), dim3(1024), 0, c.stream, a);
+  hipLaunchKernelGGL(k_bkt_scatter<DT>, dim3(c.G_big), dim3(kScatBS), 0, c.stream, a);
+  hipLaunchKernelGGL(k_bkt_sort<DT>, dim3(kBktSortBlocks), dim3(kSortBS), 0, c.stream, a);
   hipLaunchKernelGGL(k_big_begin<DT>, dim3(1), dim3(1024), 0, c.stream, a);
   const uint32_t key_passes = cdiv_u(KB, kBigDigit);
   for (uint32_t p = 0; p < key_passes; ++p)
@@ -455,7 +722,7 @@ static hipError_t launch_big_t(const BigCall& c) {
   uint64_t* src = c.runs;
   uint64_t* dst = c.staging;
   for (uint32_t L = kBigTile; L < P; L *= 2) {
-    hipLaunchKernelGGL(k_big_merge, dim3(tiles), dim3(1024), 0, c.stream, src, dst, P, L);
+    hipLaunchKernelGGL(k_big_merge, dim3(tiles), dim3(1024), 0, c.stream, a.bs, src, dst, P, L);
     uint64_t* t = src;
     src = dst;
     dst = t;

@@ -818,14 +818,17 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
     L.G_big = static_cast<uint32_t>(num_cus < kBigMaxBlocks ? num_cus : kBigMaxBlocks);
     L.off_big_state = take(256);
     L.off_ghist = take(static_cast<size_t>(kBigBins) * 4);
-    L.off_staging = take(P * 8);
+    L.off_staging = take((P + kBktCap) * 8);
     L.off_runs = take(P * 8);
+    L.off_boff = take(static_cast<size_t>(kLogBins) * 4);
+    L.off_bcur = take(static_cast<size_t>(kLogBins) * kBktPad * 4);
+    L.off_blist = take(static_cast<size_t>(kLogBins) * 4);
   } else {
     L.off_cand_key = take(static_cast<size_t>(L.G_fb) * k * 4);
     L.off_cand_idx = take(static_cast<size_t>(L.G_fb) * k * 4);
     L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
-    L.off_fhist = take(static_cast<size_t>(kLogBins) * 4);
   }
+  L.off_fhist = take(static_cast<size_t>(kLogBins) * 4);
   L.bytes = off;
   return L;
 }
@@ -847,7 +850,7 @@ static hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t
                 union_keys, union_keys ? L.union_n : 0u, static_cast<uint32_t>(c.plan->t),
                 at<uint32_t>(c.ws, L.off_segcnt), at<uint32_t>(c.ws, L.off_seg_key),
                 at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max),
-                L.big ? nullptr : at<uint32_t>(c.ws, L.off_fhist)};
+                at<uint32_t>(c.ws, L.off_fhist)};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
   hipLaunchKernelGGL(k_filter<DT>, dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
@@ -861,7 +864,7 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   CallState* st = at<CallState>(c.ws, L.off_state);
   uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
   const bool direct = p.mode == PROFK_MODE_DIRECT && !c.use_tau;
-  uint32_t* fhist = L.big ? nullptr : at<uint32_t>(c.ws, L.off_fhist);
+  uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
   const uint32_t* union_for_filter = nullptr;
   hipError_t e;
   if (direct || c.use_tau) {
@@ -886,6 +889,8 @@ static hipError_t launch_flat_t(const FlatCall& c) {
                direct ? 1 : 0, seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
                at<uint32_t>(c.ws, L.off_blk_max), L.seg_cap, L.G_f, st, c.ws + L.off_big_state,
                at<uint32_t>(c.ws, L.off_ghist), at<uint64_t>(c.ws, L.off_staging), at<uint64_t>(c.ws, L.off_runs),
+               fhist, at<uint32_t>(c.ws, L.off_boff), at<uint32_t>(c.ws, L.off_bcur),
+               at<uint32_t>(c.ws, L.off_blist),
                L.G_big, c.out_vals, c.out_idx, c.info, c.stream};
     return launch_big(bc);
   }
@@ -919,7 +924,7 @@ hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* b
   CallState* st = at<CallState>(c.ws, L.off_state);
   uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
   (void)hipGetLastError();
-  uint32_t* fhist = L.big ? nullptr : at<uint32_t>(c.ws, L.off_fhist);
+  uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
   hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, InitArgs{st, seg_cnt, fhist, c.tau_key});
   hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st, nullptr) : launch_filter<1>(c, st, nullptr);
   if (e != hipSuccess) return e;

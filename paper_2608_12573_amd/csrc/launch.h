@@ -47,6 +47,9 @@ constexpr uint32_t kBigBins = 1u << kBigDigit;
 constexpr int kBigStage = 4096;               // composites a collect block stages in LDS
 constexpr uint32_t kBigTile = 4096;           // composites sorted per block
 constexpr int kBigMaxBlocks = 256;
+constexpr uint32_t kBktCap = 4096;            // largest bucket one sort block holds
+constexpr uint32_t kBktPad = 32;              // words between bucket fill counters (own 128-byte line)
+constexpr int kBktSortBlocks = 512;           // bucket-sort grid (loops over the bucket list)
 
 // Workspace layout of one flat (vector) call.
 struct FlatLayout {
@@ -61,6 +64,8 @@ struct FlatLayout {
   bool big = false;                           // k > kFinMaxK: multi-block refinement
   uint32_t G_big = 0;
   size_t off_big_state = 0, off_ghist = 0, off_staging = 0, off_runs = 0;
+  size_t off_boff = 0, off_bcur = 0;          // bucket offsets and fill counts
+  size_t off_blist = 0;                       // non-empty buckets at or above b*
   size_t bytes = 0;
 };
 
@@ -97,6 +102,8 @@ struct BigCall {
   void* big_state;
   uint32_t* ghist;
   uint64_t *staging, *runs;
+  const uint32_t* fhist;
+  uint32_t *boff, *bcur, *blist;
   uint32_t G_big;
   void* out_vals;
   int64_t* out_idx;
