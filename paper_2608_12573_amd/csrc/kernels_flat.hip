@@ -124,7 +124,7 @@ __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
 // ------------------------------------------------------------ stage 2 -----
 // tau = t-th largest key of the union.  Used when the union is too large
 // for the filter blocks to select from it themselves.
-constexpr uint32_t kTauCache = 16384;
+constexpr uint32_t kTauCache = 32768;
 
 struct TauArgs {
   const uint32_t* keys;

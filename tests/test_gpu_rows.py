@@ -107,3 +107,15 @@ def test_config4_bf16_4096x131072_k32():
     q = oracle_plan_of(p, rows=True)
     st = _check_rows(b, "bf16", k, p, q, 0)
     assert st.count(oprofk.STATUS_FILTERED) >= B - 2
+
+
+def test_rows_relaxed_recall_partial_rows():
+    # recall 0.5 of k = 64 with t forced low: rows whose count falls in
+    # [k_req, k) return their count survivors padded, rows below k_req fall
+    # back, the rest are exact top-k
+    b = _bits("f32", 64, 4096, seed=11)
+    p = pk.plan_rows(4096, 64, 1e-2, 0.5, S_min=256, S_max=256, force_mode=pk.FORCE_FILTER)
+    p.t = 3
+    q = plan_from_lib(p)
+    st = _check_rows(b, "f32", 64, p, q, 0)
+    assert oprofk.STATUS_FILTERED in st
