@@ -131,7 +131,7 @@ int profk_topk_rows(const profk_plan_t* plan, int32_t dtype, const void* values,
   if (B < 1 || B > static_cast<int64_t>(INT32_MAX) || row_stride < D || k > profk::kRowMaxK)
     return PROFK_EINVAL;
   if (reinterpret_cast<uintptr_t>(values) % elem_size(dtype) != 0) return PROFK_EINVAL;
-  const profk::RowLayout L = profk::row_layout(*plan);
+  const profk::RowLayout L = profk::row_layout(*plan, dtype);
   if (L.bytes > profk::kRowMaxLds) return PROFK_EINVAL;
   profk::RowCall c{plan, dtype, values, static_cast<uint32_t>(B), static_cast<uint32_t>(D),
                    static_cast<uint32_t>(k), static_cast<uint64_t>(row_stride), seed, out_vals, out_idx,

@@ -32,13 +32,18 @@ struct RowArgs {
   RowLayout L;
 };
 
+// Log-scale buckets a row key distance can fall in: 16-bit keys keep every
+// distance below 2^16, so bf16 rows need only the first 1280.
+template <int DT> constexpr uint32_t row_log_bins() { return Elem<DT>::KEYBITS == 16 ? 1280u : kLogBins; }
+
 template <int DT>
 __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV, KB = Elem<DT>::KEYBITS;
   constexpr int kSelDigitRow = KB == 16 ? 8 : 11;  // sample select: 2 or 3 passes
   constexpr int NW = kRowBS / kWave;
-  constexpr uint32_t RB = kLogBins / kRowBS;        // log bins owned per thread
-  static_assert(kLogBins % kRowBS == 0, "log-bin ownership");
+  constexpr uint32_t NB = row_log_bins<DT>();
+  constexpr uint32_t RB = NB / kRowBS;              // log bins owned per thread
+  static_assert(NB % kRowBS == 0, "log-bin ownership");
   extern __shared__ __align__(16) uint8_t smem[];
   uint32_t* const samp = reinterpret_cast<uint32_t*>(smem + a.L.off_a);  // samples, then buffer keys
   uint32_t* const bkey = samp;
@@ -92,7 +97,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
               },
               a.t, KB, 0u, hist, scr)
               .kth;
-    for (uint32_t i = tid; i < kLogBins; i += kRowBS) hist[i] = 0;
+    for (uint32_t i = tid; i < NB; i += kRowBS) hist[i] = 0;
     __syncthreads();
 
     // 3. filter the row into the LDS buffer (which reuses the sample space)
@@ -163,8 +168,8 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   if (status == PROFK_STATUS_FILTERED) {
     kk = min(a.k, count);
     // Bucket offsets in descending bucket order, in place: thread t owns
-    // buckets [kLogBins - RB(t+1), kLogBins - RB t).
-    const uint32_t bb = kLogBins - RB * (tid + 1);
+    // buckets [NB - RB(t+1), NB - RB t).
+    const uint32_t bb = NB - RB * (tid + 1);
     uint32_t h[RB];
     uint32_t s = 0;
 #pragma unroll
@@ -202,7 +207,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
       for (uint32_t p = tid; p < n_sel; p += kRowBS) {
         const uint64_t c = comp[p];
         const uint32_t bin = log_bin(comp_key(c) - tau);
-        const uint32_t s0 = bin + 1 < kLogBins ? hist[bin + 1] : 0u, s1 = hist[bin];
+        const uint32_t s0 = bin + 1 < NB ? hist[bin + 1] : 0u, s1 = hist[bin];
         uint32_t rank = 0;
         for (uint32_t q = s0; q < s1; ++q) rank += comp[q] > c ? 1u : 0u;
         const uint32_t dst = s0 + rank;
@@ -238,7 +243,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
 // ------------------------------------------------------------- host -------
 static inline uint32_t align16(uint32_t x) { return (x + 15u) & ~15u; }
 
-RowLayout row_layout(const profk_plan_t& p) {
+RowLayout row_layout(const profk_plan_t& p, int dtype) {
   RowLayout L;
   const uint32_t S = static_cast<uint32_t>(p.S), M = static_cast<uint32_t>(p.M);
   const uint32_t k = static_cast<uint32_t>(p.k);
@@ -248,7 +253,8 @@ RowLayout row_layout(const profk_plan_t& p) {
   const uint32_t b_bytes = align16(M * 4u);
   uint32_t a_bytes = align16((S > M ? S : M) * 4u);
   if (a_bytes + b_bytes < exch) a_bytes = exch - b_bytes;
-  const uint32_t hist_words = (1u << kRowDigit) > kLogBins ? (1u << kRowDigit) : kLogBins;
+  const uint32_t nb = dtype == PROFK_F32 ? row_log_bins<0>() : row_log_bins<1>();
+  const uint32_t hist_words = (1u << kRowDigit) > nb ? (1u << kRowDigit) : nb;
   L.off_a = 0;
   L.off_b = a_bytes;
   L.off_hist = L.off_b + b_bytes;

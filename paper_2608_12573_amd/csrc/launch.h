@@ -125,7 +125,7 @@ struct RowLayout {
   uint32_t off_a = 0, off_b = 0, off_hist = 0, off_collect = 0, off_comp = 0, bytes = 0;
 };
 
-RowLayout row_layout(const profk_plan_t& plan);
+RowLayout row_layout(const profk_plan_t& plan, int dtype);
 
 struct RowCall {
   const profk_plan_t* plan;
