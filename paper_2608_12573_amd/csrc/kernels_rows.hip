@@ -4,8 +4,8 @@
 //   1. draw S indices of the row (Philox counter word 1 = row);
 //   2. tau = t-th largest sampled key (radix select in LDS);
 //   3. stream the row once with 16-byte loads, appending survivors to an
-//      LDS buffer of capacity M, counting all of them and histogramming them
-//      by log_bin(key - tau);
+//      LDS buffer of capacity M and counting all of them; a buffer that
+//      holds them all is then histogrammed by log_bin(key - tau);
 //   4. k_req <= count <= M: the survivors at or above the bucket of rank k
 //      are ranked within their buckets and written directly (the radix
 //      refinement when those buckets are large); otherwise the exact top-k
@@ -112,7 +112,6 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
     };
     auto store = [&](uint32_t slot, uint32_t key, uint32_t idx) {
       my_max = max(my_max, key);
-      atomicAdd(&hist[log_bin(key - tau)], 1u);
       if (slot < a.M) {
         bkey[slot] = key;
         bidx[slot] = idx;
@@ -132,9 +131,9 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
         else v[u] = u32x4{th.neutral, th.neutral, th.neutral, th.neutral};
       }
       if (__ballot(tile_any<DT, kRowU>(v, th)) == 0) continue;
-      const TileExact<DT, kRowU, kRowBS> tx{v, th, vb, nvec, tid, head};
+      const TileSparse<DT, kRowU, kRowBS> tx(v, th, vb, nvec, tid, head);
       uint32_t slot = reserve(tx.count());
-      tx.emit([&](uint32_t key, uint32_t idx) { store(slot++, key, idx); });
+      tx.emit(v, [&](uint32_t key, uint32_t idx) { store(slot++, key, idx); });
     }
     if (tid < kWave) {
       // elements before the first aligned vector and after the last one
@@ -160,6 +159,12 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
     for (int i = 0; i < NW; ++i) gmax = max(gmax, s_wmax[i]);
     status = count < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (count > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
+    if (status == PROFK_STATUS_FILTERED) {
+      // bucket histogram of the buffer (after the pass, so that the
+      // streaming loop does no per-survivor histogram atomics)
+      for (uint32_t i = tid; i < count; i += kRowBS) atomicAdd(&hist[log_bin(bkey[i] - tau)], 1u);
+      __syncthreads();
+    }
   }
 
   // 4. refinement, or the exact per-row fallback
