@@ -120,32 +120,60 @@ struct TileExact {
 // The same exact pass for tiles in which survivors are common (a row of
 // the per-row path keeps about M/D of its elements, 0.5 % at C4 shape, so
 // nearly every wave holds a few in every tile).  The survivor bits of each
-// vector are taken first; emit() then visits each lane's set bits in a short
-// loop per vector, instead of one predicated branch per element.
+// vector are formed with packed arithmetic: with thr1 = thr - 1, the
+// saturating difference thr1 - w is negative iff w >= thr, so its sign bits
+// are the survivor flags (bf16: two per word, gathered into one mask per
+// vector with byte permutes).  emit() then visits each lane's set bits in a
+// short loop per vector, instead of one predicated branch per element.
 template <int DT, int U, int BS>
 struct TileSparse {
   static constexpr int EPV = Elem<DT>::EPV;
-  uint32_t m[U];  // bit e: element e of vector u survives
+  uint32_t m[U];  // survivor flags of vector u (bit layout: elem_of_bit)
   uint32_t vb, pos, base;
+
+  // bf16 flag bits: element e in 0..3 at bit 8e+7, element e in 4..7 at bit
+  // 8(e-4)+6; fp32: element e at bit e.
+  static __device__ __forceinline__ uint32_t elem_of_bit(uint32_t p) {
+    return DT == 0 ? p : (p >> 3) + ((p & 1u) ? 0u : 4u);
+  }
 
   __device__ __forceinline__ TileSparse(const u32x4 (&v)[U], const Thresh<DT>& th, uint32_t vb_,
                                         uint32_t vend, uint32_t pos_, uint32_t base_)
       : vb(vb_), pos(pos_), base(base_) {
+    constexpr uint32_t kAll = DT == 0 ? 0xFu : 0xC0C0C0C0u;
+    const bool all = DT == 0 ? th.thr == INT_MIN : th.thr == SHRT_MIN;  // every key survives
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      uint32_t b = 0;
+      uint32_t b;
+      if (DT == 0) {
+        const int thr1 = th.thr - (all ? 0 : 1);
+        b = 0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t w = v[u][e] ^ th.flip;
-        if (DT == 0) {
-          b |= (static_cast<int>(w) >= th.thr ? 1u : 0u) << e;
-        } else {
-          b |= ((static_cast<int>(w << 16) >> 16) >= th.thr ? 1u : 0u) << (2 * e);
-          b |= ((static_cast<int>(w) >> 16) >= th.thr ? 1u : 0u) << (2 * e + 1);
+        for (int e = 0; e < 4; ++e) {
+          const int d = __builtin_elementwise_sub_sat(thr1, static_cast<int>(v[u][e] ^ th.flip));
+          b |= (static_cast<uint32_t>(d) >> 31) << e;
         }
+      } else {
+        const short t1 = static_cast<short>(th.thr - (all ? 0 : 1));
+        const s16x2 thr1 = s16x2{t1, t1};
+        uint32_t d[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          d[e] = __builtin_bit_cast(uint32_t, __builtin_elementwise_sub_sat(
+                                                   thr1, __builtin_bit_cast(s16x2, v[u][e] ^ th.flip)));
+        b = (__builtin_amdgcn_perm(d[1], d[0], 0x07050301u) & 0x80808080u) |
+            ((__builtin_amdgcn_perm(d[3], d[2], 0x07050301u) >> 1) & 0x40404040u);
       }
+      if (all) b = kAll;
       m[u] = vb + u * BS + pos < vend ? b : 0u;
     }
+  }
+
+  __device__ __forceinline__ bool any() const {
+    uint32_t o = 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) o |= m[u];
+    return o != 0;
   }
 
   __device__ __forceinline__ uint32_t count() const {
@@ -155,7 +183,7 @@ struct TileSparse {
     return c;
   }
 
-  // f(key, index) for each survivor, in element order.
+  // f(key, index) for each survivor (in flag-bit order within a vector).
   template <class F>
   __device__ __forceinline__ void emit(const u32x4 (&v)[U], F f) const {
 #pragma unroll
@@ -163,7 +191,7 @@ struct TileSparse {
       const uint32_t vi = vb + u * BS + pos;
       uint32_t b = m[u];
       while (b) {
-        const uint32_t e = __builtin_ctz(b);
+        const uint32_t e = elem_of_bit(__builtin_ctz(b));
         b &= b - 1;
         if (DT == 0) {
           const uint32_t raw = (e & 2) ? ((e & 1) ? v[u][3] : v[u][2]) : ((e & 1) ? v[u][1] : v[u][0]);

@@ -130,8 +130,8 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
         if (vi < nvec) v[u] = __builtin_nontemporal_load(vec + vi);
         else v[u] = u32x4{th.neutral, th.neutral, th.neutral, th.neutral};
       }
-      if (__ballot(tile_any<DT, kRowU>(v, th)) == 0) continue;
       const TileSparse<DT, kRowU, kRowBS> tx(v, th, vb, nvec, tid, head);
+      if (__ballot(tx.any()) == 0) continue;
       uint32_t slot = reserve(tx.count());
       tx.emit(v, [&](uint32_t key, uint32_t idx) { store(slot++, key, idx); });
     }
