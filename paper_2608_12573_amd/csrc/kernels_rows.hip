@@ -11,6 +11,8 @@
 //      refinement when those buckets are large); otherwise the exact top-k
 //      of the row itself (per-row fallback, no second launch).
 // The LDS layout is sized from the plan at launch (dynamic shared memory).
+#include <type_traits>
+
 #include "device_common.h"
 #include "filter_tile.h"
 #include "launch.h"
@@ -18,7 +20,18 @@
 
 namespace profk {
 
-constexpr int kRowDigit = 11;  // radix digit of the refinement and fallback
+// Radix digit of the refinement and fallback: 16-bit keys take two 8-bit
+// passes (a 256-word histogram), 32-bit keys three 11-bit ones.
+template <int DT> constexpr int row_digit() { return Elem<DT>::KEYBITS == 16 ? 8 : 11; }
+
+// Buffer keys are stored at their own width (bf16 keys in 16 bits).
+template <int DT> using RowKey = typename std::conditional<Elem<DT>::KEYBITS == 16, uint16_t, uint32_t>::type;
+
+// tau from the sample held in registers (at most 8 keys per thread): each
+// wave's top-t, then the top-t of their union.
+__host__ __device__ constexpr bool row_fast_tau(uint32_t S, uint32_t t) {
+  return S <= 8u * kRowBS && t >= 1 && t <= kWaveTopMax;
+}
 
 struct RowArgs {
   const void* values;
@@ -40,20 +53,22 @@ template <int DT>
 __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV, KB = Elem<DT>::KEYBITS;
   constexpr int kSelDigitRow = KB == 16 ? 8 : 11;  // sample select: 2 or 3 passes
+  constexpr int kDigit = row_digit<DT>();
+  using K = RowKey<DT>;
   constexpr int NW = kRowBS / kWave;
   constexpr uint32_t NB = row_log_bins<DT>();
   constexpr uint32_t RB = NB / kRowBS;              // log bins owned per thread
   static_assert(NB % kRowBS == 0, "log-bin ownership");
   extern __shared__ __align__(16) uint8_t smem[];
   uint32_t* const samp = reinterpret_cast<uint32_t*>(smem + a.L.off_a);  // samples, then buffer keys
-  uint32_t* const bkey = samp;
+  K* const bkey = reinterpret_cast<K*>(smem + a.L.off_a);
   uint32_t* const bidx = reinterpret_cast<uint32_t*>(smem + a.L.off_b);
   uint32_t* const hist = reinterpret_cast<uint32_t*>(smem + a.L.off_hist);
   uint64_t* const collect = reinterpret_cast<uint64_t*>(smem + a.L.off_collect);
   uint64_t* const comp = reinterpret_cast<uint64_t*>(smem + a.L.off_comp);
   uint64_t* const exch = reinterpret_cast<uint64_t*>(smem + a.L.off_a);      // after the buffer is done
   __shared__ SelectScratch scr;
-  __shared__ uint32_t s_cnt, s_counter, s_wmax[NW];
+  __shared__ uint32_t s_cnt, s_counter, s_tau, s_wmax[NW];
 
   const uint32_t r = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const char* row = static_cast<const char*>(a.values) + static_cast<size_t>(r) * a.row_stride * ES;
@@ -65,6 +80,9 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   uint32_t status = PROFK_STATUS_DIRECT, count = 0, tau = 0, gmax = 0;
   if (!a.direct) {
     // 1. sample: the Philox words first, then all gathers in flight at once
+    const bool fast = row_fast_tau(a.S, a.t);
+    uint32_t keys[8];
+    uint32_t valid = 0;
     for (uint32_t blk0 = 0; 4 * blk0 < a.S; blk0 += 2 * kRowBS) {
       U64x4 rnd[2];
 #pragma unroll
@@ -85,18 +103,46 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
           const uint32_t j = 4 * (blk0 + q * kRowBS + tid) + x;
-          if (j < a.S) samp[j] = key_of<DT>(raw[4 * q + x]);
+          keys[4 * q + x] = key_of<DT>(raw[4 * q + x]);
+          if (j < a.S) {
+            valid |= 1u << (4 * q + x);
+            if (!fast) samp[j] = keys[4 * q + x];
+          }
         }
     }
     if (tid == 0) s_cnt = 0;
-    __syncthreads();
     // 2. threshold
-    tau = block_select_kth<kRowBS, kSelDigitRow>(
-              [&](auto f) {
-                for (uint32_t i = tid; i < a.S; i += kRowBS) f(samp[i]);
-              },
-              a.t, KB, 0u, hist, scr)
-              .kth;
+    if (fast) {
+      // every wave's top-t (hist serves as scratch: NW lists of up to
+      // kWaveTopMax keys, then their lengths), then the top-t of the union
+      uint32_t last = 0;
+      const uint32_t got = wave_top_t<8>(keys, valid, a.t, hist + w * kWaveTopMax, last);
+      if (lane == 0) hist[NW * kWaveTopMax + w] = got;
+      __syncthreads();
+      if (w == 0) {
+        static_assert(NW * kWaveTopMax == 2 * kWave, "union of the wave lists: two keys per lane");
+        uint32_t u[2];
+        uint32_t uv = 0;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const uint32_t s = lane + q * kWave, ww = s / kWaveTopMax;
+          u[q] = hist[s];
+          if (s % kWaveTopMax < hist[NW * kWaveTopMax + ww]) uv |= 1u << q;
+        }
+        wave_top_t<2>(u, uv, a.t, nullptr, last);
+        if (lane == 0) s_tau = last;
+      }
+      __syncthreads();
+      tau = s_tau;
+    } else {
+      __syncthreads();
+      tau = block_select_kth<kRowBS, kSelDigitRow>(
+                [&](auto f) {
+                  for (uint32_t i = tid; i < a.S; i += kRowBS) f(samp[i]);
+                },
+                a.t, KB, 0u, hist, scr)
+                .kth;
+    }
     for (uint32_t i = tid; i < NB; i += kRowBS) hist[i] = 0;
     __syncthreads();
 
@@ -113,7 +159,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
     auto store = [&](uint32_t slot, uint32_t key, uint32_t idx) {
       my_max = max(my_max, key);
       if (slot < a.M) {
-        bkey[slot] = key;
+        bkey[slot] = static_cast<K>(key);
         bidx[slot] = idx;
       }
     };
@@ -230,10 +276,10 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
       }
       done = true;
     } else {
-      block_topk<kRowBS, kRowDigit>(LdsSrc{bkey, bidx}, count, kk, tau, max(gmax, tau), KB, sm);
+      block_topk<kRowBS, kDigit>(LdsSrc<K>{bkey, bidx}, count, kk, tau, max(gmax, tau), KB, sm);
     }
   } else {
-    block_topk<kRowBS, kRowDigit>(InputSrc<DT>{row, 0u}, a.D, a.k, 0u, key_max, KB, sm);
+    block_topk<kRowBS, kDigit>(InputSrc<DT>{row, 0u}, a.D, a.k, 0u, key_max, KB, sm);
   }
   if (!done) sort_write_any<DT, kRowBS>(collect, kk, a.k, exch, out_vals, out_idx);
   if (a.info && tid == 0) {
@@ -251,15 +297,21 @@ static inline uint32_t align16(uint32_t x) { return (x + 15u) & ~15u; }
 RowLayout row_layout(const profk_plan_t& p, int dtype) {
   RowLayout L;
   const uint32_t S = static_cast<uint32_t>(p.S), M = static_cast<uint32_t>(p.M);
-  const uint32_t k = static_cast<uint32_t>(p.k);
+  const uint32_t k = static_cast<uint32_t>(p.k), t = static_cast<uint32_t>(p.t);
+  const bool f32 = dtype == PROFK_F32;
   uint32_t P = 1;
   while (P < (k > static_cast<uint32_t>(kRowBS) ? k : static_cast<uint32_t>(kRowBS))) P <<= 1;
   const uint32_t exch = 2u * P * 8u;
   const uint32_t b_bytes = align16(M * 4u);
-  uint32_t a_bytes = align16((S > M ? S : M) * 4u);
+  const uint32_t samp_bytes = row_fast_tau(S, t) ? 0u : S * 4u;   // samples kept in LDS
+  const uint32_t key_bytes = M * (f32 ? 4u : 2u);
+  uint32_t a_bytes = align16(samp_bytes > key_bytes ? samp_bytes : key_bytes);
   if (a_bytes + b_bytes < exch) a_bytes = exch - b_bytes;
-  const uint32_t nb = dtype == PROFK_F32 ? row_log_bins<0>() : row_log_bins<1>();
-  const uint32_t hist_words = (1u << kRowDigit) > nb ? (1u << kRowDigit) : nb;
+  const uint32_t nb = f32 ? row_log_bins<0>() : row_log_bins<1>();
+  const uint32_t radix = 1u << (f32 ? row_digit<0>() : row_digit<1>());
+  uint32_t hist_words = radix > nb ? radix : nb;
+  if (hist_words < static_cast<uint32_t>(kRowBS / kWave) * (kWaveTopMax + 1))
+    hist_words = static_cast<uint32_t>(kRowBS / kWave) * (kWaveTopMax + 1);
   L.off_a = 0;
   L.off_b = a_bytes;
   L.off_hist = L.off_b + b_bytes;

@@ -26,9 +26,11 @@ struct PosIdx {
   __device__ __forceinline__ uint32_t operator()() const { return v; }
 };
 
-// Candidates held in LDS (keys and indices).
+// Candidates held in LDS (keys of type K and indices).
+template <class K = uint32_t>
 struct LdsSrc {
-  const uint32_t *key, *idx;
+  const K* key;
+  const uint32_t* idx;
   template <int BS, class F>
   __device__ __forceinline__ void visit(uint32_t n, const uint32_t*, F f) const {
     for (uint32_t i = threadIdx.x; i < n; i += BS) f(i, key[i], LoadIdx{idx + i});
