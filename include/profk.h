@@ -94,7 +94,9 @@ typedef struct {
 void profk_default_opts(profk_plan_opts_t* opts);
 
 /* Defaults for one row of a batch: as above with S_min = 256, because a
- * 32768-draw floor oversamples rows of ~10^5 elements. */
+ * 32768-draw floor oversamples rows of ~10^5 elements, and cost ratio 0.5,
+ * the measured tau_B / tau_A of the per-row kernel on MI355X (Sec. 4,
+ * "Optimal Sample Size", leaves the ratio to a benchmark of the hardware). */
 void profk_default_row_opts(profk_plan_opts_t* opts);
 
 /* Parameter selection, host only, pure and thread-safe (Algorithm 1 for S;

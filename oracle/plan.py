@@ -27,6 +27,8 @@ Readings taken where the paper is silent or inconsistent
     the failure probability.  The literal Algorithm 1 is kept as
     paper_literal=True for reporting only.
   * log in S* is log2 (Algorithm 1); round(S*) is round-half-up.
+  * Rows: S_min = 256 and tau_B/tau_A = 0.5 (a measured hardware constant;
+    the flat default stays at the paper's 1).
   * Relaxed recall rho < 1 plans for k_req = ceil(rho k) in the recall tail.
   * mode DIRECT (an exact top-k with no sampling) when S >= N/2, when 8k > N,
     or when no t <= S meets eps_A; it never changes the result.
@@ -55,7 +57,7 @@ class PlanOpts:
     force_mode: int = FORCE_AUTO
 
 
-ROW_OPTS = PlanOpts(S_min=256)
+ROW_OPTS = PlanOpts(S_min=256, cost_ratio=0.5)
 
 
 @dataclass(frozen=True)
@@ -158,6 +160,8 @@ def plan(N, k, eps=1e-6, recall=1.0, opts=PlanOpts()):
 
 
 def plan_rows(D, k, eps=1e-6, recall=1.0, opts=ROW_OPTS):
-    """Per-row plan: the same selection with N = D and a lower S floor, since
-    S_min = 32768 would sample a quarter of a 131072-wide row."""
+    """Per-row plan: the same selection with N = D, a lower S floor, since
+    S_min = 32768 would sample a quarter of a 131072-wide row, and the cost
+    ratio tau_B/tau_A = 0.5, which Sec. 4 ("Optimal Sample Size") leaves to a
+    measurement of the hardware (the per-row kernel's, on MI355X)."""
     return plan(D, k, eps, recall, opts)

@@ -74,7 +74,12 @@ void profk_default_opts(profk_plan_opts_t* o) {
 
 void profk_default_row_opts(profk_plan_opts_t* o) {
   profk_default_opts(o);
-  if (o) o->S_min = 256;
+  if (!o) return;
+  o->S_min = 256;
+  // tau_B / tau_A measured for the per-row kernel on MI355X: a sampled
+  // element costs a scattered line fetch, so fewer draws and a larger buffer
+  // are faster than the unit ratio.
+  o->cost_ratio = 0.5;
 }
 
 int profk_plan(int64_t N, int64_t k, double eps, double recall, const profk_plan_opts_t* opts,
