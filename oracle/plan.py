@@ -29,6 +29,12 @@ Readings taken where the paper is silent or inconsistent
   * log in S* is log2 (Algorithm 1); round(S*) is round-half-up.
   * Rows: S_min = 256 and tau_B/tau_A = 0.5 (a measured hardware constant;
     the flat default stays at the paper's 1).
+  * lexicographic=True selects the tie-exact filter rule of oracle.profk: the
+    rank argument behind both tails counts elements above a threshold in a
+    total order, and (key, -index) is one with no ties, so the same t and M
+    bound Pr(count < k_req) and Pr(count > M) for every input, plateaus
+    included.  Under the paper's rule (key >= tau) the tails hold for
+    distinct values only.
   * Relaxed recall rho < 1 plans for k_req = ceil(rho k) in the recall tail.
   * mode DIRECT (an exact top-k with no sampling) when S >= N/2, when 8k > N,
     or when no t <= S meets eps_A; it never changes the result.
@@ -55,6 +61,7 @@ class PlanOpts:
     eps_split: float = 0.5    # eps_A = eps_split * eps
     paper_literal: bool = False
     force_mode: int = FORCE_AUTO
+    lexicographic: bool = False  # filter on (key, -index), see the module docstring
 
 
 ROW_OPTS = PlanOpts(S_min=256, cost_ratio=0.5)
@@ -73,6 +80,7 @@ class Plan:
     mode: int
     p_underflow: float
     p_overflow: float
+    lexicographic: bool = False
 
 
 def z_upper(eps_tail):
@@ -156,7 +164,8 @@ def plan(N, k, eps=1e-6, recall=1.0, opts=PlanOpts()):
     return Plan(N=N, k=k, eps=float(eps), recall=float(recall), k_req=k_req,
                 S=S, t=t, M=M, mode=mode,
                 p_underflow=p_underflow(S, t, N, k_req),
-                p_overflow=p_overflow(S, t, N, M))
+                p_overflow=p_overflow(S, t, N, M),
+                lexicographic=bool(opts.lexicographic))
 
 
 def plan_rows(D, k, eps=1e-6, recall=1.0, opts=ROW_OPTS):

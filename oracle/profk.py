@@ -9,6 +9,11 @@ For one vector of N values under plan (S, t, M, k_req):
      counted with multiplicity (rank 1 is the largest).
   3. Filtering: the survivors are every i with key_i >= tau; their number
      'count' is exact (counting continues past M).
+     Lexicographic plans (plan.lexicographic) compare (key, -index) pairs
+     instead: stage 2 takes the t-th largest sampled pair (tau, -i_tau), and
+     i survives iff key_i > tau, or key_i = tau and i <= i_tau.  Pairs are
+     all distinct, so count is exactly the rank of the threshold pair even
+     when values repeat (a plateau at tau no longer overflows the buffer).
   4. Refinement: if count < k_req (insufficient recall) or count > M (buffer
      overflow) the result is the exact top-k of the whole input (O1).
      Otherwise it is the top-k of the survivors in the total order; in
@@ -44,6 +49,7 @@ class Result:
     tau_key: int          # -1 when no threshold was drawn (DIRECT)
     count: int            # -1 when no filtering ran (DIRECT)
     n_valid: int
+    tau_idx: int = -1     # lexicographic plans: index of the threshold pair
 
 
 def sample_keys(key, plan, seed, row=0):
@@ -61,24 +67,47 @@ def survivors(key, tau):
     return np.flatnonzero(key >= tau)
 
 
+def threshold_lex(skeys, sidx, t):
+    """Stage 2, lexicographic: the t-th largest sampled pair (key, -index),
+    with multiplicity; returns (tau, i_tau)."""
+    order = np.lexsort((sidx, -skeys.astype(np.int64)))   # key descending, index ascending
+    j = order[t - 1]
+    return int(skeys[j]), int(sidx[j])
+
+
+def survivors_lex(key, tau, tau_idx):
+    """Stage 3, lexicographic: ascending i with (key_i, -i) >= (tau, -tau_idx)."""
+    i = np.arange(key.size)
+    return np.flatnonzero((key > tau) | ((key == tau) & (i <= tau_idx)))
+
+
 def run(bits, dtype, k, plan, seed, row=0, tau_override=None):
     """Prof-K on one vector.  tau_override replaces stages 1-2 (used to force
-    the failure paths)."""
+    the failure paths); it is a key, or for a lexicographic plan a
+    (key, index) pair."""
     bits = np.asarray(bits)
     key = keys_of(bits, dtype)
     if plan.mode == MODE_DIRECT and tau_override is None:
         v, i = exact.topk(bits, dtype, k)
         return Result(v, i, STATUS_DIRECT, -1, -1, k)
-    if tau_override is None:
-        tau = threshold(sample_keys(key, plan, seed, row), plan.t)
+    lex = bool(getattr(plan, "lexicographic", False))
+    tau_idx = -1
+    if tau_override is not None:
+        if lex:
+            tau, tau_idx = (int(v) for v in tau_override)
+        else:
+            tau = int(tau_override)
+    elif lex:
+        sidx = sample_indices(seed, row, plan.S, len(key))
+        tau, tau_idx = threshold_lex(key[sidx], sidx, plan.t)
     else:
-        tau = int(tau_override)
-    surv = survivors(key, tau)
+        tau = threshold(sample_keys(key, plan, seed, row), plan.t)
+    surv = survivors_lex(key, tau, tau_idx) if lex else survivors(key, tau)
     count = int(surv.size)
     if count < plan.k_req or count > plan.M:
         v, i = exact.topk(bits, dtype, k)
         status = STATUS_UNDERFLOW if count < plan.k_req else STATUS_OVERFLOW
-        return Result(v, i, status, tau, count, k)
+        return Result(v, i, status, tau, count, k, tau_idx)
     order = surv[np.argsort(-key[surv], kind="stable")]
     take = order[:k].astype(np.int64)
     n_valid = int(take.size)
@@ -86,7 +115,7 @@ def run(bits, dtype, k, plan, seed, row=0, tau_override=None):
     idx = np.full(k, -1, dtype=np.int64)
     vals[:n_valid] = bits[take]
     idx[:n_valid] = take
-    return Result(vals, idx, STATUS_FILTERED, tau, count, n_valid)
+    return Result(vals, idx, STATUS_FILTERED, tau, count, n_valid, tau_idx)
 
 
 def run_rows(bits2d, dtype, k, row_plan, seed, rows=None):

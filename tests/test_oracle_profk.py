@@ -139,3 +139,78 @@ def test_batchtopk_flat_indices():
     assert np.array_equal(r.idx, i)
     rows, cols = np.divmod(r.idx, 2048)
     assert np.array_equal(x[rows, cols], v.view(np.float32))
+
+
+# ---- the tie-exact (lexicographic) filter rule -----------------------------
+
+def _lex(p):
+    import dataclasses
+    return dataclasses.replace(p, lexicographic=True)
+
+
+def test_lex_on_a_plateau_equals_the_plain_rule_on_a_descending_ramp():
+    # On a constant input the pair order is the index order, which is the
+    # value order of the strictly decreasing ramp N-1, ..., 0.  So the same
+    # draws must give the same count under the two rules, and the threshold
+    # pair's index must be the ramp position of the plain threshold.
+    n, k = 3000, 20
+    p = plan.plan(n, k, 0.05, 1.0, plan.PlanOpts(S_min=200, S_max=200, force_mode=plan.FORCE_FILTER))
+    flat = np.full(n, 2.5, dtype=np.float32)
+    ramp = np.arange(n - 1, -1, -1).astype(np.float32)
+    for seed in range(12):
+        a = profk.run(keys.f32_bits(flat), "f32", k, _lex(p), seed)
+        b = profk.run(keys.f32_bits(ramp), "f32", k, p, seed)
+        ramp_tau = float(keys.bits_from_key_u32(np.uint32(b.tau_key)).view(np.float32))
+        assert a.count == b.count
+        assert a.tau_idx == n - 1 - int(ramp_tau)
+        assert a.status == b.status
+        assert list(a.idx) == list(range(k))      # ties: the smallest indices first
+
+
+def test_lex_equals_plain_rule_on_distinct_values():
+    x = workloads.normal_f32(4000, seed=8)
+    assert np.unique(x).size == x.size
+    p = plan.plan(4000, 16, 0.05, 1.0, plan.PlanOpts(S_min=300, S_max=300, force_mode=plan.FORCE_FILTER))
+    for seed in range(6):
+        a = profk.run(keys.f32_bits(x), "f32", 16, _lex(p), seed)
+        b = profk.run(keys.f32_bits(x), "f32", 16, p, seed)
+        assert (a.count, a.tau_key, a.status) == (b.count, b.tau_key, b.status)
+        assert list(a.idx) == list(b.idx)
+        # the threshold pair is a drawn element carrying the threshold value
+        assert x[a.tau_idx] == keys.bits_from_key_u32(np.uint32(a.tau_key)).view(np.float32)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_lex_count_is_the_rank_of_the_threshold_pair(seed):
+    # brute force on small inputs with many ties: sort all N pairs by the
+    # float value (descending) and then by index, and find the threshold
+    # pair's position.
+    g = np.random.default_rng(100 + seed)
+    n = int(g.integers(80, 300))
+    x = g.integers(0, 6, n).astype(np.float32)
+    k = int(g.integers(1, 10))
+    p = _lex(plan.plan(n, k, 0.3, 1.0, plan.PlanOpts(S_min=40, S_max=40, force_mode=plan.FORCE_FILTER)))
+    r = profk.run(keys.f32_bits(x), "f32", k, p, seed)
+    order = _brute_order(x)
+    assert r.count == order.index(r.tau_idx) + 1
+    # the threshold pair is the t-th largest drawn pair, with multiplicity
+    drawn = philox.sample_indices(seed, 0, p.S, n)
+    ranked = sorted(drawn, key=order.index)
+    assert ranked[p.t - 1] == r.tau_idx
+    assert list(r.idx) == order[:k]
+
+
+def test_lex_keeps_a_plateau_inside_the_buffer():
+    # 90 % of the mass on one value above the top-k boundary region: under
+    # the plain rule every plateau element survives and the buffer overflows;
+    # the pair rule keeps rank(tau) elements, within M.
+    n, k = 200_000, 64
+    x = workloads.normal_f32(n, seed=3)
+    x[np.random.default_rng(0).random(n) < 0.5] = 4.0
+    p = plan.plan(n, k, 1e-6, 1.0, plan.PlanOpts(S_min=4096, S_max=4096))
+    plain = profk.run(keys.f32_bits(x), "f32", k, p, seed=1)
+    lex = profk.run(keys.f32_bits(x), "f32", k, _lex(p), seed=1)
+    assert plain.status == profk.STATUS_OVERFLOW
+    assert lex.status == profk.STATUS_FILTERED and k <= lex.count <= p.M
+    ex_v, ex_i = exact.topk(keys.f32_bits(x), "f32", k)
+    assert list(lex.idx) == list(ex_i) and list(plain.idx) == list(ex_i)
