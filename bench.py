@@ -91,8 +91,10 @@ def counters_traffic(workload_key):
 class Workload:
     """Input, preallocated outputs and one step of the path for one shape."""
 
-    def __init__(self, name, k_arg, torch, pk, wl):
+    def __init__(self, name, k_arg, torch, pk, wl, lex=False):
         self.name = name
+        self.lex = lex
+        rule = dict(lexicographic=1) if lex else {}
         self.rows = False
         self.es = 4
         self.recall = 1.0
@@ -121,7 +123,7 @@ class Workload:
                          f"eps=1e-6, sample seed 0")
             self.host = host
             self.x = f32(host)
-            self.p = pk.plan(N, k, 1e-6, 1.0)
+            self.p = pk.plan(N, k, 1e-6, 1.0, **rule)
             self.kernel = "k_filter<f32>"
             self.ws = pk.workspace(self.p, pk.F32)
             self.out = (torch.empty(k, dtype=torch.float32, device="cuda"),
@@ -137,7 +139,7 @@ class Workload:
             self.host = bits
             self.x = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
             self.rows, self.es = True, 2
-            self.p = pk.plan_rows(D, k, 1e-6, 1.0)
+            self.p = pk.plan_rows(D, k, 1e-6, 1.0, **rule)
             self.kernel = "k_rows<bf16>"
             self.desc = (f"bf16 rows [4096, 131072] of ReLU(N(0,1)) (seed 3), per-row top-k k={k}, "
                          f"eps=1e-6, one row plan, sample seed 0")
@@ -156,7 +158,7 @@ class Workload:
             self.host = host.reshape(-1)
             self.x = f32(host).view(B, D)
             K = B * k_row
-            self.p = pk.plan(B * D, K, 1e-6, self.recall)
+            self.p = pk.plan(B * D, K, 1e-6, self.recall, **rule)
             self.kernel = "k_filter<f32>"
             self.desc = (f"BatchTopK select over fp32 [4096, 65536] N(-0.5,1) pre-activations with 1% "
                          f"hot columns +3 (seed 4), K=4096*64=262144, eps=1e-6, recall {self.recall}, "
@@ -172,9 +174,11 @@ class Workload:
         else:
             raise SystemExit(f"unknown workload {name}; choose from {', '.join(WORKLOADS)}")
         self.in_bytes = self.N * self.es
+        if lex:
+            self.desc += "; tie-exact filter on (key, -index) pairs"
 
     def key(self):
-        return f"{self.name}-k{self.k}"
+        return f"{self.name}-k{self.k}" + ("-lex" if self.lex else "")
 
 
 def cpu_baseline(w, budget_s=10.0):
@@ -219,6 +223,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-torch-baseline", action="store_true")
     ap.add_argument("--no-copy-probe", action="store_true")
+    ap.add_argument("--lexicographic", action="store_true",
+                    help="plan with the tie-exact filter rule on (key, -index) pairs")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -230,7 +236,7 @@ def main():
     import paper_2608_12573_amd as pk
     import workloads
 
-    w = Workload(args.workload, args.k, torch, pk, workloads)
+    w = Workload(args.workload, args.k, torch, pk, workloads, lex=args.lexicographic)
     lib = pk.lib()
     for _ in range(args.warmup):
         w.step()
@@ -291,7 +297,8 @@ def main():
         "dtype": "u16" if w.es == 2 else "u32",
         "data": "synthetic",
         "config": {"workload": w.desc, "N": w.N, "k": w.k, "eps": 1e-6, "recall": w.recall,
-                   "plan": {"S": w.p.S, "t": w.p.t, "M": w.p.M, "mode": w.p.mode}},
+                   "plan": {"S": w.p.S, "t": w.p.t, "M": w.p.M, "mode": w.p.mode,
+                            "lexicographic": int(w.p.lexicographic)}},
         "elements_per_s": round(w.N / (ms_per_step * 1e-3), 1),
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "kernel_ms": round(kern_ms, 5),

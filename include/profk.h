@@ -65,6 +65,8 @@ typedef struct {
   double eps_split;     /* eps_A = eps_split * eps, eps_B = the rest (Theorem 1): 0.5 */
   int32_t paper_literal;/* 1: t and M from Algorithm 1 verbatim (reporting only) */
   int32_t force_mode;   /* PROFK_FORCE_*: override the FILTER/DIRECT choice */
+  int32_t lexicographic;/* 1: tie-exact filter on (key, -index) pairs; 0: key >= tau
+                         * as in Sec. 3 (default).  Copied into the plan. */
 } profk_plan_opts_t;
 
 /* A plan: (S, t, M) for one (N, k, eps, recall). */
@@ -76,7 +78,13 @@ typedef struct {
   int64_t t;            /* threshold rank within the sample, 1-based */
   int64_t M;            /* buffer capacity */
   int32_t mode;         /* PROFK_MODE_* */
-  int32_t reserved;
+  int32_t lexicographic;/* 1: the threshold is the t-th largest sampled (key, -index)
+                         * pair (tau, -i_tau) and element i survives iff key > tau, or
+                         * key == tau and i <= i_tau.  Pairs never tie, so count is the
+                         * exact rank of the threshold and the eps bound of Theorem 1
+                         * holds for inputs with repeated values too (with key >= tau
+                         * it holds for distinct values).  The result is the same exact
+                         * top-k either way.  0: the paper's key >= tau. */
   double p_underflow;   /* Pr(count < k_req) = Pr(Bin(S, (k_req-1)/N) >= t) */
   double p_overflow;    /* Pr(count > M)     = Pr(Bin(S, M/N) <= t-1) */
 } profk_plan_t;
@@ -180,7 +188,9 @@ int profk_debug_filter(const profk_plan_t* plan, int32_t dtype,
                        void* stream);
 
 /* profk_topk with stages 1-2 replaced by a caller-given threshold key, to
- * drive the underflow and overflow paths on purpose. */
+ * drive the underflow and overflow paths on purpose.  A key alone names no
+ * threshold pair, so this entry point filters with key >= tau_key also for
+ * lexicographic plans. */
 int profk_topk_tau(const profk_plan_t* plan, int32_t dtype, const void* values,
                    int64_t N, int64_t k, uint32_t tau_key, void* out_vals,
                    int64_t* out_idx, void* ws, size_t ws_bytes, void* stream,

@@ -31,18 +31,19 @@ OK, EINVAL, EDTYPE, EWORKSPACE, ENULL, EHIP = 0, -1, -2, -3, -4, -5
 class PlanOpts(ctypes.Structure):
     _fields_ = [("S_min", ctypes.c_int32), ("S_max", ctypes.c_int32),
                 ("cost_ratio", ctypes.c_double), ("eps_split", ctypes.c_double),
-                ("paper_literal", ctypes.c_int32), ("force_mode", ctypes.c_int32)]
+                ("paper_literal", ctypes.c_int32), ("force_mode", ctypes.c_int32),
+                ("lexicographic", ctypes.c_int32)]
 
 
 class Plan(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("k", ctypes.c_int64),
                 ("eps", ctypes.c_double), ("recall", ctypes.c_double),
                 ("k_req", ctypes.c_int64), ("S", ctypes.c_int64), ("t", ctypes.c_int64),
-                ("M", ctypes.c_int64), ("mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("M", ctypes.c_int64), ("mode", ctypes.c_int32), ("lexicographic", ctypes.c_int32),
                 ("p_underflow", ctypes.c_double), ("p_overflow", ctypes.c_double)]
 
     def as_dict(self):
-        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+        return {name: getattr(self, name) for name, _ in self._fields_}
 
 
 INFO_DTYPE = np.dtype([("count", "<u8"), ("tau_key", "<u4"), ("status", "<i4"), ("n_valid", "<i8")])

@@ -24,7 +24,8 @@ bool plan_consistent(const profk_plan_t* p) {
   return p->N >= 1 && p->N <= static_cast<int64_t>(UINT32_MAX) && p->k >= 1 && p->k <= p->N &&
          p->k_req >= 1 && p->k_req <= p->k && p->S >= 1 && p->t >= 1 && p->t <= p->S &&
          p->S <= static_cast<int64_t>(UINT32_MAX) && p->M >= p->k && p->M <= p->N &&
-         (p->mode == PROFK_MODE_FILTER || p->mode == PROFK_MODE_DIRECT);
+         (p->mode == PROFK_MODE_FILTER || p->mode == PROFK_MODE_DIRECT) &&
+         (p->lexicographic == 0 || p->lexicographic == 1);
 }
 
 bool dtype_ok(int32_t dt) { return dt == PROFK_F32 || dt == PROFK_BF16; }
@@ -70,6 +71,7 @@ void profk_default_opts(profk_plan_opts_t* o) {
   o->eps_split = 0.5;
   o->paper_literal = 0;
   o->force_mode = PROFK_FORCE_AUTO;
+  o->lexicographic = 0;
 }
 
 void profk_default_row_opts(profk_plan_opts_t* o) {

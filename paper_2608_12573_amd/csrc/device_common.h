@@ -307,6 +307,54 @@ __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t k
   return block_select_kth<BS, kSelDigit>(visit, kk, nbits, prefix, sh.hist, sh.scratch());
 }
 
+// Index of the lexicographic threshold pair (Sec. 3 stage 2 taken on
+// (key, -index) pairs): with tau the t-th largest sampled key, the t-th
+// largest sampled pair is (tau, -i) where i is the r-th smallest index, with
+// multiplicity, among the draws whose key is tau, r = t - #draws above tau.
+// draws(f) must call f(key, index) once per draw, from any thread of the
+// block, identically on every call.  The indices of the tied draws are kept
+// in `list` (cap words of LDS) when they fit, otherwise the draws are
+// visited again on each select pass; `hist` is 2^DIGIT words of LDS.
+// Returns 0xFFFFFFFF when no draw carries tau (not for a tau taken from the
+// same draws).
+template <int BS, int DIGIT, class Draws>
+__device__ uint32_t tau_pair_index(Draws draws, uint32_t tau, uint32_t t, uint32_t* list, uint32_t cap,
+                                   uint32_t* hist, SelectScratch& scr, uint32_t* s_n) {
+  if (threadIdx.x == 0) *s_n = 0;
+  __syncthreads();
+  uint32_t above = 0;
+  draws([&](uint32_t key, uint32_t idx) {
+    if (key > tau) {
+      ++above;
+    } else if (key == tau) {
+      const uint32_t p = atomicAdd(s_n, 1u);
+      if (p < cap) list[p] = idx;
+    }
+  });
+  const uint32_t a = block_sum<BS>(above, scr.wsum);
+  __syncthreads();
+  const uint32_t ne = *s_n;
+  if (ne == 0 || a >= t) return 0xFFFFFFFFu;
+  const uint32_t r = min(t - a, ne);
+  SelectResult res;
+  if (ne <= cap) {
+    res = block_select_kth<BS, DIGIT>(
+        [&](auto f) {
+          for (uint32_t i = threadIdx.x; i < ne; i += BS) f(~list[i]);
+        },
+        r, 32, 0u, hist, scr);
+  } else {
+    res = block_select_kth<BS, DIGIT>(
+        [&](auto f) {
+          draws([&](uint32_t key, uint32_t idx) {
+            if (key == tau) f(~idx);
+          });
+        },
+        r, 32, 0u, hist, scr);
+  }
+  return ~res.kth;
+}
+
 // Top-t of up to 64*E keys held by one wave (E per lane, `valid` bits mark
 // which of a lane's slots hold keys): t rounds of a wave-wide max; the lowest
 // lane holding the maximum gives up one copy and stores it to out[round]

@@ -22,12 +22,17 @@ template <> struct Elem<0> { static constexpr int EPV = 4, ES = 4, KEYBITS = 32;
 template <> struct Elem<1> { static constexpr int EPV = 8, ES = 2, KEYBITS = 16; };
 
 // The transformed threshold of a key: survive iff transform(word) >= thr.
+// Under the lexicographic rule an element equal to the threshold survives
+// only when its index is at most `tie` (0xFFFFFFFF: every tie survives, the
+// paper's rule); the fast test below stays the superset key >= tau.
 template <int DT>
 struct Thresh {
   uint32_t flip;
   int thr;
   uint32_t neutral;  // a word that fails the fast test unless every word passes
-  __device__ __forceinline__ explicit Thresh(uint32_t tau) {
+  uint32_t tie;
+  __device__ __forceinline__ bool keep(int x, uint32_t i) const { return x >= thr && (x != thr || i <= tie); }
+  __device__ __forceinline__ explicit Thresh(uint32_t tau, uint32_t tie_idx = 0xFFFFFFFFu) : tie(tie_idx) {
     if (DT == 0) {
       const uint32_t tb = bits_from_key_f32(tau);
       flip = (tb >> 31) ? 0x7FFFFFFFu : 0u;
@@ -68,8 +73,11 @@ __device__ __forceinline__ bool tile_any(const u32x4 (&v)[U], const Thresh<DT>& 
 // vb + u*BS + lane_pos, valid when below vend; element e of a vector is
 // input element base + vector*EPV + e.  count() returns the lane's survivor
 // count; emit(f) calls f(key, index) for each survivor in element order.
-template <int DT, int U, int BS>
+// LEX: the lexicographic rule (ties at the threshold cut by index).
+template <int DT, int U, int BS, bool LEX = false>
 struct TileExact {
+  __device__ __forceinline__ bool keep(int x, uint32_t i) const { return LEX ? th.keep(x, i) : x >= th.thr; }
+
   const u32x4 (&v)[U];
   const Thresh<DT>& th;
   uint32_t vb, vend, pos, base;
@@ -78,15 +86,17 @@ struct TileExact {
     uint32_t cnt = 0;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const bool valid = vb + u * BS + pos < vend;
+      const uint32_t vi = vb + u * BS + pos;
+      const bool valid = vi < vend;
+      const uint32_t i0 = base + vi * Elem<DT>::EPV;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const uint32_t w = v[u][e] ^ th.flip;
         if (DT == 0) {
-          cnt += (valid && static_cast<int>(w) >= th.thr) ? 1u : 0u;
+          cnt += (valid && keep(static_cast<int>(w), i0 + e)) ? 1u : 0u;
         } else {
-          cnt += (valid && (static_cast<int>(w << 16) >> 16) >= th.thr) ? 1u : 0u;
-          cnt += (valid && (static_cast<int>(w) >> 16) >= th.thr) ? 1u : 0u;
+          cnt += (valid && keep(static_cast<int>(w << 16) >> 16, i0 + 2 * e)) ? 1u : 0u;
+          cnt += (valid && keep(static_cast<int>(w) >> 16, i0 + 2 * e + 1)) ? 1u : 0u;
         }
       }
     }
@@ -105,11 +115,11 @@ struct TileExact {
         const uint32_t raw = v[u][e];
         const uint32_t w = raw ^ th.flip;
         if (DT == 0) {
-          if (valid && static_cast<int>(w) >= th.thr) f(key_f32(raw), base + vi * EPV + e);
+          if (valid && keep(static_cast<int>(w), base + vi * EPV + e)) f(key_f32(raw), base + vi * EPV + e);
         } else {
-          if (valid && (static_cast<int>(w << 16) >> 16) >= th.thr)
+          if (valid && keep(static_cast<int>(w << 16) >> 16, base + vi * EPV + 2 * e))
             f(key_bf16(raw & 0xFFFFu), base + vi * EPV + 2 * e);
-          if (valid && (static_cast<int>(w) >> 16) >= th.thr)
+          if (valid && keep(static_cast<int>(w) >> 16, base + vi * EPV + 2 * e + 1))
             f(key_bf16(raw >> 16), base + vi * EPV + 2 * e + 1);
         }
       }
@@ -125,7 +135,7 @@ struct TileExact {
 // are the survivor flags (bf16: two per word, gathered into one mask per
 // vector with byte permutes).  emit() then visits each lane's set bits in a
 // short loop per vector, instead of one predicated branch per element.
-template <int DT, int U, int BS>
+template <int DT, int U, int BS, bool LEX = false>
 struct TileSparse {
   static constexpr int EPV = Elem<DT>::EPV;
   uint32_t m[U];  // survivor flags of vector u (bit layout: elem_of_bit)
@@ -166,6 +176,31 @@ struct TileSparse {
       }
       if (all) b = kAll;
       m[u] = vb + u * BS + pos < vend ? b : 0u;
+    }
+    if (LEX && th.tie != 0xFFFFFFFFu) {
+      // lexicographic rule: drop the survivors equal to the threshold whose
+      // index lies past the threshold pair's
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t i0 = base + (vb + u * BS + pos) * EPV;
+        uint32_t b = m[u], keep = m[u];
+        while (b) {
+          const uint32_t p = __builtin_ctz(b);
+          b &= b - 1;
+          const uint32_t e = elem_of_bit(p);
+          int x;
+          if (DT == 0) {
+            const uint32_t raw = (e & 2) ? ((e & 1) ? v[u][3] : v[u][2]) : ((e & 1) ? v[u][1] : v[u][0]);
+            x = static_cast<int>(raw ^ th.flip);
+          } else {
+            const uint32_t raw = (e & 4) ? ((e & 2) ? v[u][3] : v[u][2]) : ((e & 2) ? v[u][1] : v[u][0]);
+            const uint32_t w = raw ^ th.flip;
+            x = (e & 1) ? (static_cast<int>(w) >> 16) : (static_cast<int>(w << 16) >> 16);
+          }
+          if (!th.keep(x, i0 + e)) keep &= ~(1u << p);
+        }
+        m[u] = keep;
+      }
     }
   }
 

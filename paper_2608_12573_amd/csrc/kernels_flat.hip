@@ -7,6 +7,8 @@
 //                 local top-t sample keys (the t-th largest of the whole
 //                 sample is among the union of the blocks' top-t).
 //   k_select_tau  only when that union is large: one block picks tau.
+//   k_tau_index   lexicographic plans only: the sample blocks list the draws
+//                 that carry tau, and the last one picks the threshold pair.
 //   k_filter      persistent grid, one contiguous chunk per block, 16-byte
 //                 nontemporal loads.  When the union is small each block
 //                 first selects tau from it itself.  Survivors are staged in
@@ -35,6 +37,9 @@ __device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt, ui
   if (threadIdx.x == 0) {
     st->ticket = 0;
     st->status = 0;
+    st->tie_above = 0;
+    st->tie_n = 0;
+    st->tie_ticket = 0;
   }
 }
 
@@ -191,6 +196,77 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
   if (tid == 0) a.st->tau_key = r.kth;
 }
 
+// ------------------------------------------------------ stage 2, pairs ----
+// Lexicographic plans: once tau is in the call state, every sample block
+// draws its 1024 draws again (Philox words and gathers, as k_sample), counts
+// those above tau and lists the indices of those equal to it (one atomic
+// per block for each); the last block to finish takes i_tau, the
+// (t - above)-th smallest listed index, with multiplicity.
+struct TauIdxArgs {
+  const void* values;
+  uint64_t n, seed, row;
+  uint32_t S, t;
+  CallState* st;
+  uint32_t* list;  // S entries
+};
+
+template <int DT>
+__global__ __launch_bounds__(kSampBS) void k_tau_index(TauIdxArgs a) {
+  __shared__ uint32_t s_list[kSampPerBlock];
+  __shared__ SelectShared sel;
+  __shared__ uint32_t s_n, s_base, s_last;
+  const uint32_t tid = threadIdx.x, tau = a.st->tau_key;
+  const uint32_t j0 = blockIdx.x * kSampPerBlock;
+  if (tid == 0) s_n = 0;
+  __syncthreads();
+  uint32_t above = 0;
+  {
+    const U64x4 r = philox4x64_10(static_cast<uint64_t>(j0 / 4) + tid, a.row, 0, 0, a.seed, 0);
+    uint32_t raw[4], ix[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool in = j0 + 4 * tid + q < a.S;
+      ix[q] = in ? index_of_word(r.w[q], a.n) : 0u;
+      raw[q] = in ? load_raw<DT>(a.values, ix[q]) : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (j0 + 4 * tid + q >= a.S) continue;
+      const uint32_t key = key_of<DT>(raw[q]);
+      if (key > tau) ++above;
+      else if (key == tau) s_list[atomicAdd(&s_n, 1u)] = ix[q];
+    }
+  }
+  const uint32_t blk_above = block_sum<kSampBS>(above, sel.wsum);
+  __syncthreads();
+  const uint32_t nb = s_n;
+  if (tid == 0) {
+    if (blk_above) atomicAdd(&a.st->tie_above, blk_above);
+    s_base = nb ? atomicAdd(&a.st->tie_n, nb) : 0u;
+  }
+  __syncthreads();
+  for (uint32_t i = tid; i < nb; i += kSampBS) a.list[s_base + i] = s_list[i];
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) s_last = atomicAdd(&a.st->tie_ticket, 1u) == gridDim.x - 1 ? 1u : 0u;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  const uint32_t a_tot = a.st->tie_above, ne = a.st->tie_n;
+  uint32_t i_tau = 0xFFFFFFFFu;
+  if (ne > 0 && a_tot < a.t) {
+    const uint32_t r = min(a.t - a_tot, ne);
+    const uint32_t* list = a.list;
+    i_tau = ~block_select_kth<kSampBS>(
+                 [&](auto f) {
+                   for (uint32_t i = tid; i < ne; i += kSampBS) f(~list[i]);
+                 },
+                 r, 32, 0u, sel)
+                 .kth;
+  }
+  if (tid == 0) a.st->tau_idx = i_tau;
+}
+
 struct InitArgs {
   CallState* st;
   uint32_t* seg_cnt;
@@ -216,7 +292,7 @@ struct FilterArgs {
 };
 
 // The filter pass; the survival test is in filter_tile.h.
-template <int DT>
+template <int DT, bool LEX>
 __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   constexpr int EPV = Elem<DT>::EPV;
   constexpr int ES = Elem<DT>::ES;
@@ -323,7 +399,7 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     tau = a.st->tau_key;
   }
 
-  const Thresh<DT> th(tau);
+  const Thresh<DT> th(tau, LEX ? a.st->tau_idx : 0xFFFFFFFFu);
   uint32_t* const s_hist = s_pool;
   if (a.fhist)
     for (uint32_t i = tid; i < kLogBins; i += kFiltBS) s_hist[i] = 0;
@@ -370,7 +446,7 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     if (vb != vbeg) load_step(vb, th.neutral);
     if (__ballot(tile_any<DT, kFiltU>(v, th)) == 0) continue;
     // Rare path: exact per-element test, one slot reservation per wave.
-    const TileExact<DT, kFiltU, kFiltBS> tx{v, th, vb, vend, tid, a.head};
+    const TileExact<DT, kFiltU, kFiltBS, LEX> tx{v, th, vb, vend, tid, a.head};
     uint32_t slot, first_over, gbase;
     reserve(tx.count(), slot, first_over, gbase);
     tx.emit([&](uint32_t key, uint32_t idx) { store(slot++, first_over, gbase, key, idx); });
@@ -385,7 +461,7 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     if (lane < ns) {
       idx = lane < a.head ? lane : tail0 + (lane - a.head);
       key = key_of<DT>(load_raw<DT>(a.values, idx));
-      ok = key >= tau;
+      ok = LEX ? (key > tau || (key == tau && idx <= th.tie)) : key >= tau;
     }
     (void)EPV;
     if (__ballot(ok)) {
@@ -778,8 +854,8 @@ static int filter_blocks_per_cu(int dtype) {
   if (cached[d] == 0) {
     int n = 0;
     const hipError_t e = d == 0
-        ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0>, kFiltBS, 0)
-        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1>, kFiltBS, 0);
+        ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0, false>, kFiltBS, 0)
+        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1, false>, kFiltBS, 0);
     cached[d] = (e == hipSuccess && n > 0) ? (n < 4 ? n : 4) : 4;
   }
   return cached[d];
@@ -829,6 +905,7 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
     L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
   }
   L.off_fhist = take(static_cast<size_t>(kLogBins) * 4);
+  if (p.lexicographic) L.off_tie = take(static_cast<size_t>(S) * 4);
   L.bytes = off;
   return L;
 }
@@ -837,7 +914,7 @@ template <class T> static T* at(uint8_t* ws, size_t off) { return reinterpret_ca
 
 // union_keys null: the filter reads tau from the call state.
 template <int DT>
-static hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t* union_keys) {
+static hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t* union_keys, bool lex) {
   const FlatLayout& L = c.L;
   constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV;
   const uintptr_t addr = reinterpret_cast<uintptr_t>(c.values);
@@ -852,7 +929,8 @@ static hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t
                 at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max),
                 at<uint32_t>(c.ws, L.off_fhist)};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
-  hipLaunchKernelGGL(k_filter<DT>, dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  if (lex) hipLaunchKernelGGL((k_filter<DT, true>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  else hipLaunchKernelGGL((k_filter<DT, false>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
   return hipGetLastError();
 }
@@ -864,6 +942,7 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   CallState* st = at<CallState>(c.ws, L.off_state);
   uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
   const bool direct = p.mode == PROFK_MODE_DIRECT && !c.use_tau;
+  const bool lex = p.lexicographic && !direct && !c.use_tau;  // a caller's tau: the key rule
   uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
   const uint32_t* union_for_filter = nullptr;
   hipError_t e;
@@ -875,15 +954,20 @@ static hipError_t launch_flat_t(const FlatCall& c) {
     SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
                   L.tcap, uk, st, seg_cnt, fhist};
     hipLaunchKernelGGL(k_sample<DT>, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
-    if (L.union_n <= kFiltTauMax && static_cast<uint32_t>(p.t) <= kFiltTauInMaxT) {
+    if (!lex && L.union_n <= kFiltTauMax && static_cast<uint32_t>(p.t) <= kFiltTauInMaxT) {
       union_for_filter = uk;
     } else {
       TauArgs ta{uk, L.union_n, static_cast<uint32_t>(p.t), Elem<DT>::KEYBITS, st};
       hipLaunchKernelGGL(k_select_tau, dim3(1), dim3(kTauBS), 0, c.stream, ta);
+      if (lex) {
+        TauIdxArgs ti{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t), st,
+                      at<uint32_t>(c.ws, L.off_tie)};
+        hipLaunchKernelGGL(k_tau_index<DT>, dim3(L.G_s), dim3(kSampBS), 0, c.stream, ti);
+      }
     }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (!direct && (e = launch_filter<DT>(c, st, union_for_filter)) != hipSuccess) return e;
+  if (!direct && (e = launch_filter<DT>(c, st, union_for_filter, lex)) != hipSuccess) return e;
   if (L.big) {
     BigCall bc{DT, c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
                direct ? 1 : 0, seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
@@ -926,7 +1010,8 @@ hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* b
   (void)hipGetLastError();
   uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
   hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, InitArgs{st, seg_cnt, fhist, c.tau_key});
-  hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st, nullptr) : launch_filter<1>(c, st, nullptr);
+  hipError_t e = c.dtype == PROFK_F32 ? launch_filter<0>(c, st, nullptr, false)
+                                       : launch_filter<1>(c, st, nullptr, false);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_gather_buffer, dim3(1), dim3(1024), 0, c.stream, L.seg_cap, seg_cnt,
                      at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),

@@ -2,7 +2,8 @@
 // batch element).  One workgroup owns one row and runs all four stages in
 // LDS:
 //   1. draw S indices of the row (Philox counter word 1 = row);
-//   2. tau = t-th largest sampled key (radix select in LDS);
+//   2. tau = t-th largest sampled key (radix select in LDS); lexicographic
+//      plans also find the index of the threshold pair;
 //   3. stream the row once with 16-byte loads, appending survivors to an
 //      LDS buffer of capacity M and counting all of them; a buffer that
 //      holds them all is then histogrammed by log_bin(key - tau);
@@ -49,7 +50,7 @@ struct RowArgs {
 // distance below 2^16, so bf16 rows need only the first 1280.
 template <int DT> constexpr uint32_t row_log_bins() { return Elem<DT>::KEYBITS == 16 ? 1280u : kLogBins; }
 
-template <int DT>
+template <int DT, bool LEX>
 __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV, KB = Elem<DT>::KEYBITS;
   constexpr int kSelDigitRow = KB == 16 ? 8 : 11;  // sample select: 2 or 3 passes
@@ -68,7 +69,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   uint64_t* const comp = reinterpret_cast<uint64_t*>(smem + a.L.off_comp);
   uint64_t* const exch = reinterpret_cast<uint64_t*>(smem + a.L.off_a);      // after the buffer is done
   __shared__ SelectScratch scr;
-  __shared__ uint32_t s_cnt, s_counter, s_tau, s_wmax[NW];
+  __shared__ uint32_t s_cnt, s_counter, s_tau, s_tie_n, s_wmax[NW];
 
   const uint32_t r = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const char* row = static_cast<const char*>(a.values) + static_cast<size_t>(r) * a.row_stride * ES;
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
   if (!a.direct) {
     // 1. sample: the Philox words first, then all gathers in flight at once
     const bool fast = row_fast_tau(a.S, a.t);
-    uint32_t keys[8];
+    uint32_t keys[8], ids[8];
     uint32_t valid = 0;
     for (uint32_t blk0 = 0; 4 * blk0 < a.S; blk0 += 2 * kRowBS) {
       U64x4 rnd[2];
@@ -96,7 +97,8 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
           const uint32_t j = 4 * (blk0 + q * kRowBS + tid) + x;
-          raw[4 * q + x] = j < a.S ? load_raw<DT>(row, index_of_word(rnd[q].w[x], a.D)) : 0u;
+          ids[4 * q + x] = j < a.S ? index_of_word(rnd[q].w[x], a.D) : 0u;
+          raw[4 * q + x] = j < a.S ? load_raw<DT>(row, ids[4 * q + x]) : 0u;
         }
 #pragma unroll
       for (int q = 0; q < 2; ++q)
@@ -143,11 +145,41 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
                 a.t, KB, 0u, hist, scr)
                 .kth;
     }
+    uint32_t tie = 0xFFFFFFFFu;
+    if (LEX && fast) {
+      // the draws are still in registers
+      auto draws = [&](auto f) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if ((valid >> e) & 1u) f(keys[e], ids[e]);
+      };
+      tie = tau_pair_index<kRowBS, kDigit>(draws, tau, a.t, reinterpret_cast<uint32_t*>(smem + a.L.off_a),
+                                           a.L.off_b / 4u, hist, scr, &s_tie_n);
+    } else if (LEX) {
+      // the draws again (Philox words and gathers), for the tied draws' indices
+      auto draws = [&](auto f) {
+        for (uint32_t jb = tid; 4 * jb < a.S; jb += kRowBS) {
+          const U64x4 rr = philox4x64_10(jb, r, 0, 0, a.seed, 0);
+          uint32_t raw[4], ix[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const bool in = 4 * jb + q < a.S;
+            ix[q] = in ? index_of_word(rr.w[q], a.D) : 0u;
+            raw[q] = in ? load_raw<DT>(row, ix[q]) : 0u;
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (4 * jb + q < a.S) f(key_of<DT>(raw[q]), ix[q]);
+        }
+      };
+      tie = tau_pair_index<kRowBS, kDigit>(draws, tau, a.t, reinterpret_cast<uint32_t*>(smem + a.L.off_a),
+                                           a.L.off_b / 4u, hist, scr, &s_tie_n);
+    }
     for (uint32_t i = tid; i < NB; i += kRowBS) hist[i] = 0;
     __syncthreads();
 
     // 3. filter the row into the LDS buffer (which reuses the sample space)
-    const Thresh<DT> th(tau);
+    const Thresh<DT> th(tau, tie);
     uint32_t my_max = 0;
     auto reserve = [&](uint32_t cnt) {
       const uint32_t incl = wave_incl_sum(cnt);
@@ -176,7 +208,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
         if (vi < nvec) v[u] = __builtin_nontemporal_load(vec + vi);
         else v[u] = u32x4{th.neutral, th.neutral, th.neutral, th.neutral};
       }
-      const TileSparse<DT, kRowU, kRowBS> tx(v, th, vb, nvec, tid, head);
+      const TileSparse<DT, kRowU, kRowBS, LEX> tx(v, th, vb, nvec, tid, head);
       if (__ballot(tx.any()) == 0) continue;
       uint32_t slot = reserve(tx.count());
       tx.emit(v, [&](uint32_t key, uint32_t idx) { store(slot++, key, idx); });
@@ -190,7 +222,7 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
       if (lane < ns) {
         idx = lane < head ? lane : tail0 + (lane - head);
         key = key_of<DT>(load_raw<DT>(row, idx));
-        ok = key >= tau;
+        ok = LEX ? (key > tau || (key == tau && idx <= tie)) : key >= tau;
       }
       if (__ballot(ok)) {
         const uint32_t slot = reserve(ok ? 1u : 0u);
@@ -327,7 +359,8 @@ static hipError_t launch_rows_t(const RowCall& c) {
   RowArgs ra{c.values, c.row_stride, c.D, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.S),
              static_cast<uint32_t>(p.t), static_cast<uint32_t>(p.M), p.mode == PROFK_MODE_DIRECT ? 1 : 0,
              c.seed, c.out_vals, c.out_idx, c.info, c.L};
-  hipLaunchKernelGGL(k_rows<DT>, dim3(c.B), dim3(kRowBS), c.L.bytes, c.stream, ra);
+  if (p.lexicographic) hipLaunchKernelGGL((k_rows<DT, true>), dim3(c.B), dim3(kRowBS), c.L.bytes, c.stream, ra);
+  else hipLaunchKernelGGL((k_rows<DT, false>), dim3(c.B), dim3(kRowBS), c.L.bytes, c.stream, ra);
   return hipGetLastError();
 }
 

@@ -15,7 +15,11 @@ struct CallState {
   uint32_t tau_key;    // threshold key (stage 2)
   uint32_t ticket;     // last-block-done counter of the fallback
   uint32_t status;     // PROFK_STATUS_* of the call
-  uint32_t pad[61];
+  uint32_t tau_idx;    // lexicographic plans: index of the threshold pair
+  uint32_t tie_above;  // draws above tau (k_tau_index)
+  uint32_t tie_n;      // draws equal to tau, listed in the workspace
+  uint32_t tie_ticket; // last-block-done counter of k_tau_index
+  uint32_t pad[57];
 };
 
 // Launch geometry.
@@ -61,6 +65,7 @@ struct FlatLayout {
   size_t off_seg_key = 0, off_seg_idx = 0;
   size_t off_cand_key = 0, off_cand_idx = 0, off_cand_cnt = 0;
   size_t off_fhist = 0;                       // log-bin histogram of the candidates
+  size_t off_tie = 0;                         // lexicographic plans: indices of the draws equal to tau
   bool big = false;                           // k > kFinMaxK: multi-block refinement
   uint32_t G_big = 0;
   size_t off_big_state = 0, off_ghist = 0, off_staging = 0, off_runs = 0;

@@ -207,7 +207,7 @@ int make_plan(int64_t N, int64_t k, double eps, double recall,
   out->t = t;
   out->M = M;
   out->mode = mode;
-  out->reserved = 0;
+  out->lexicographic = o.lexicographic ? 1 : 0;
   out->p_underflow = plan_p_underflow(S, t, N, k_req);
   out->p_overflow = plan_p_overflow(S, t, N, M);
   return PROFK_OK;

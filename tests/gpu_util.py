@@ -61,6 +61,7 @@ def oracle_plan_of(p, opts=None, rows=False, **kw):
     o = opts if opts is not None else oplan.PlanOpts(**kw) if kw else (oplan.ROW_OPTS if rows else oplan.PlanOpts())
     q = oplan.plan(p.N, p.k, p.eps, p.recall, o)
     assert (q.S, q.t, q.M, q.k_req, q.mode) == (p.S, p.t, p.M, p.k_req, p.mode), (q, p.as_dict())
+    assert q.lexicographic == bool(p.lexicographic)
     return q
 
 
@@ -68,7 +69,8 @@ def plan_from_lib(p):
     """oracle Plan carrying exactly the library plan's numbers (used when a
     test edits a plan on purpose)."""
     return oplan.Plan(N=p.N, k=p.k, eps=p.eps, recall=p.recall, k_req=p.k_req, S=p.S, t=p.t, M=p.M,
-                      mode=p.mode, p_underflow=p.p_underflow, p_overflow=p.p_overflow)
+                      mode=p.mode, p_underflow=p.p_underflow, p_overflow=p.p_overflow,
+                      lexicographic=bool(p.lexicographic))
 
 
 def compare(vals, idx, info, ref, dtype):

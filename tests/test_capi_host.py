@@ -22,11 +22,12 @@ def test_library_exports_every_header_symbol():
 def _oracle_opts(o):
     return oplan.PlanOpts(S_min=o.S_min, S_max=o.S_max, cost_ratio=o.cost_ratio,
                           eps_split=o.eps_split, paper_literal=bool(o.paper_literal),
-                          force_mode=o.force_mode)
+                          force_mode=o.force_mode, lexicographic=bool(o.lexicographic))
 
 
 def _same(p, q):
     assert (p.N, p.k, p.k_req, p.S, p.t, p.M, p.mode) == (q.N, q.k, q.k_req, q.S, q.t, q.M, q.mode)
+    assert bool(p.lexicographic) == q.lexicographic
     assert p.p_underflow == pytest.approx(q.p_underflow, rel=1e-9, abs=1e-300)
     assert p.p_overflow == pytest.approx(q.p_overflow, rel=1e-9, abs=1e-300)
 
@@ -57,7 +58,7 @@ def test_row_planner_equals_oracle(D):
 
 
 def test_paper_literal_and_options_equal_oracle():
-    cases = [dict(paper_literal=1), dict(S_min=64, S_max=64, force_mode=pk.FORCE_FILTER),
+    cases = [dict(paper_literal=1), dict(S_min=64, S_max=64, force_mode=pk.FORCE_FILTER), dict(lexicographic=1),
              dict(cost_ratio=0.1), dict(eps_split=0.3), dict(S_min=131072, S_max=131072)]
     for kw, (N, k) in itertools.product(cases, [(2**20, 64), (2**28, 1024), (2**29, 64),
                                                 (10**6, 10), (2**28, 262144)]):
