@@ -32,7 +32,7 @@ constexpr int kFiltU = 8;                     // 16-byte loads in flight per lan
 constexpr int kFiltMaxBlocks = 1024;
 constexpr uint32_t kFiltTauMax = 2048;        // largest sample union a filter block selects from
 constexpr uint32_t kFiltTauWave = 4;          // union keys per lane when one wave selects tau
-constexpr uint32_t kFiltTauInMaxT = 8;        // largest t the filter blocks select tau for themselves
+constexpr uint32_t kFiltTauInMaxT = 32;       // largest t the filter blocks select tau for themselves
 constexpr uint32_t kStage = 1024;             // survivors a filter block stages in LDS
 constexpr int kSegs = 8;                      // candidate segments (one counter each)
 constexpr int kSegStride = 64;                // words between segment counters
