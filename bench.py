@@ -35,7 +35,7 @@ CSRC = os.path.join(ROOT, "paper_2608_12573_amd", "csrc")
 # Every source the filter kernel is compiled from: the committed counters
 # stand for this exact code and are dropped once any of these changes.
 FILTER_SRCS = ("kernels_flat.hip", "filter_tile.h", "device_common.h", "launch.h", "topk_block.h")
-WORKLOADS = ("c2", "c1", "c3a", "c3b", "c3c", "c3d", "c3d2", "c4", "c5", "c5r")
+WORKLOADS = ("c2", "c1", "c3a", "c3b", "c3c", "c3d", "c3d2", "c4", "c5", "c5r", "c5p")
 FLUSH_BYTES = 512 << 20
 
 
@@ -151,17 +151,18 @@ class Workload:
                                              info=self.info, seed=0)
             self.torch_ref = lambda: torch.topk(self.x, k, dim=1, sorted=True)
             self.N, self.k, self.B, self.D = B * D, k, B, D
-        elif name in ("c5", "c5r"):
-            B, D, k_row = 4096, 65536, 64
-            self.recall = 1.0 if name == "c5" else 0.95
+        elif name in ("c5", "c5r", "c5p"):
+            # c5p: the paper's SAE shape, [4096, 12288] with k = 32 per row
+            B, D, k_row = (4096, 12288, 32) if name == "c5p" else (4096, 65536, 64)
+            self.recall = 0.95 if name == "c5r" else 1.0
             host = wl.sae_preacts_f32(B=B, D=D, seed=4)
             self.host = host.reshape(-1)
             self.x = f32(host).view(B, D)
             K = B * k_row
             self.p = pk.plan(B * D, K, 1e-6, self.recall, **rule)
             self.kernel = "k_filter<f32>"
-            self.desc = (f"BatchTopK select over fp32 [4096, 65536] N(-0.5,1) pre-activations with 1% "
-                         f"hot columns +3 (seed 4), K=4096*64=262144, eps=1e-6, recall {self.recall}, "
+            self.desc = (f"BatchTopK select over fp32 [{B}, {D}] N(-0.5,1) pre-activations with 1% "
+                         f"hot columns +3 (seed 4), K={B}*{k_row}={B * k_row}, eps=1e-6, recall {self.recall}, "
                          f"sample seed 0")
             self.ws = pk.workspace(self.p, pk.F32)
             self.out = (torch.empty(K, dtype=torch.float32, device="cuda"),
