@@ -96,3 +96,25 @@ def special_f32(n, seed=5):
     neg_nan = g.random(n) < 0.05
     u[neg_nan] = np.uint32(0xFFC00001)
     return x
+
+
+def sae_model(B=4096, d_model=512, d_dict=12288, seed=6, hot_every=100):
+    """A synthetic BatchTopK SAE layer in the paper's shape (B x d_model
+    inputs, d_dict latents), as bf16 bit patterns and fp32 biases:
+      x      [B, d_model]       N(0, 1) activations;
+      W_enc  [d_dict, d_model]  N(0, 1/d_model) rows, so pre-activations are
+                                about N(0, 1);
+      b_enc  [d_dict]           -0.5, and +1.5 on every hot_every-th latent
+                                (frequently active latents);
+      W_dec  [d_dict, d_model]  unit-norm rows;
+      b_dec  [d_model]          N(0, 0.1)."""
+    g = rng(seed)
+    x = g.standard_normal((B, d_model), dtype=np.float32)
+    w_enc = g.standard_normal((d_dict, d_model), dtype=np.float32) / np.float32(np.sqrt(d_model))
+    b_enc = np.full(d_dict, -0.5, dtype=np.float32)
+    b_enc[::hot_every] = np.float32(1.5)
+    w_dec = g.standard_normal((d_dict, d_model), dtype=np.float32)
+    w_dec /= np.linalg.norm(w_dec, axis=1, keepdims=True).astype(np.float32)
+    b_dec = (g.standard_normal(d_model, dtype=np.float32) * np.float32(0.1)).astype(np.float32)
+    return dict(x=f32_to_bf16_bits(x), w_enc=f32_to_bf16_bits(w_enc), b_enc=b_enc,
+                w_dec=f32_to_bf16_bits(w_dec), b_dec=b_dec)
