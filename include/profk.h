@@ -187,6 +187,65 @@ int profk_debug_filter(const profk_plan_t* plan, int32_t dtype,
                        uint32_t* count_dev, void* ws, size_t ws_bytes,
                        void* stream);
 
+/* ---- BatchTopK SAE layer (Sec. 5, "Application: BatchTopK Sparse
+ * Autoencoders"; the encoder and decoder are those of the BatchTopK SAE the
+ * paper builds on) ----
+ *
+ * Latents z[b, j] = max(sum_m x[b, m] W_enc[j, m] + b_enc[j], +0.0): bf16
+ * inputs, fp32 sums (MFMA: each 16-product step and its accumulator are
+ * rounded once), fp32 bias; a non-positive or NaN pre-activation gives +0.0.
+ *
+ * profk_sae_encode_topk selects the K = B*k_row largest latents of the
+ * flattened [B, d_dict] matrix (flat index b*d_dict + j) with Prof-K inside
+ * the encoder GEMM: the S sampled latents are computed with the GEMM's own
+ * MFMA sequence (bit-identical values), and the filter runs in the GEMM's
+ * epilogue, so the latent matrix is never written to memory -- except by
+ * the exact fallback, which writes it to `ws` and selects from it.  The
+ * result is the exact top-K of the latents under the total order (value
+ * descending, then index ascending), sorted, as profk_batchtopk's.
+ *   plan   profk_plan(B*d_dict, B*k_row, eps, recall), key rule only
+ *          (lexicographic plans: PROFK_EINVAL).
+ *   x      bf16 [B, d_model] row-major, 16-byte aligned; d_model a multiple
+ *          of 64 (at most 65536).
+ *   w_enc  bf16 [d_dict, d_model] row-major (one row per latent), 16-byte
+ *          aligned.  b_enc: fp32 [d_dict].
+ *   out_vals fp32 [K], out_flat_idx int64 [K]; relaxed recall pads as
+ *          profk_topk does.  ws: profk_sae_workspace_size(plan, B, d_dict)
+ *          bytes (the vector path's workspace plus 4*B*d_dict bytes for the
+ *          fallback's latent matrix).
+ * Errors as profk_topk; B*d_dict < 2^32. */
+size_t profk_sae_workspace_size(const profk_plan_t* plan, int64_t B, int64_t d_dict);
+int profk_sae_encode_topk(const profk_plan_t* plan, const void* x, const void* w_enc,
+                          const float* b_enc, int64_t B, int64_t d_model, int64_t d_dict,
+                          int64_t k_row, uint64_t seed, float* out_vals, int64_t* out_flat_idx,
+                          void* ws, size_t ws_bytes, void* stream, profk_info_t* info_dev);
+
+/* The latent matrix itself, out = fp32 [B, d_dict] (the same values the
+ * fused path filters).  Same argument rules as profk_sae_encode_topk. */
+int profk_sae_encode_dense(const void* x, const void* w_enc, const float* b_enc, int64_t B,
+                           int64_t d_model, int64_t d_dict, float* out, void* stream);
+
+/* Sparse decode: out[b, :] = sum over the entries i < K with flat_idx[i] =
+ * b*d_dict + j of vals[i] * W_dec[j, :], plus b_dec.  Entries with a
+ * negative or out-of-range index (relaxed-recall padding) are skipped.  Each
+ * row's terms are summed in fp32 in ascending j, so the result does not
+ * depend on the order of the list.  w_dec: bf16 [d_dict, d_model]
+ * row-major; b_dec fp32 [d_model]; out fp32 [B, d_model]; d_dict <= 16384;
+ * ws: profk_sae_decode_workspace_size(B, K) bytes. */
+size_t profk_sae_decode_workspace_size(int64_t B, int64_t K);
+int profk_sae_decode(const float* vals, const int64_t* flat_idx, int64_t K, const void* w_dec,
+                     const float* b_dec, int64_t B, int64_t d_model, int64_t d_dict, float* out,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* Inspection: the keys of the S latents profk_sae_encode_topk samples for
+ * this plan and seed (draw j at keys_dev[j], S entries); ws as for
+ * profk_sae_encode_topk.  The draws' flat indices are
+ * profk_debug_sample_indices(seed, 0, S, B*d_dict). */
+int profk_debug_sae_sample(const profk_plan_t* plan, const void* x, const void* w_enc,
+                           const float* b_enc, int64_t B, int64_t d_model, int64_t d_dict,
+                           uint64_t seed, uint32_t* keys_dev, void* ws, size_t ws_bytes,
+                           void* stream);
+
 /* profk_topk with stages 1-2 replaced by a caller-given threshold key, to
  * drive the underflow and overflow paths on purpose.  A key alone names no
  * threshold pair, so this entry point filters with key >= tau_key also for

@@ -96,6 +96,15 @@ def lib():
         L.profk_status_string.restype = ctypes.c_char_p
         L.profk_last_hip_error.restype = ctypes.c_int
         L.profk_set_trace_events.argtypes = [vp, vp]
+        sz = ctypes.c_size_t
+        L.profk_sae_workspace_size.argtypes = [P(Plan), i64, i64]
+        L.profk_sae_workspace_size.restype = sz
+        L.profk_sae_encode_topk.argtypes = [P(Plan), vp, vp, vp, i64, i64, i64, i64, u64, vp, vp, vp, sz, vp, vp]
+        L.profk_sae_encode_dense.argtypes = [vp, vp, vp, i64, i64, i64, vp, vp]
+        L.profk_sae_decode_workspace_size.argtypes = [i64, i64]
+        L.profk_sae_decode_workspace_size.restype = sz
+        L.profk_sae_decode.argtypes = [vp, vp, i64, vp, vp, i64, i64, i64, vp, vp, sz, vp]
+        L.profk_debug_sae_sample.argtypes = [P(Plan), vp, vp, vp, i64, i64, i64, u64, vp, vp, sz, vp]
         _lib = L
     return _lib
 
@@ -276,3 +285,81 @@ def debug_filter(x, tau_key, p, ws=None):
     _check(lib().profk_debug_filter(ctypes.byref(p), dt, _ptr(x), x.numel(), tau_key, _ptr(bk), _ptr(bi),
                                     _ptr(cnt), _ptr(ws), ws.numel(), _stream()))
     return bk, bi, cnt
+
+
+# ------------------------------------------------------ BatchTopK SAE layer ---
+
+def _sae_shape(x, w_enc, b_enc):
+    torch = _torch()
+    if x.dim() != 2 or w_enc.dim() != 2 or x.shape[1] != w_enc.shape[1] or b_enc.shape != (w_enc.shape[0],):
+        raise ProfkError("x [B, d_model], w_enc [d_dict, d_model] and b_enc [d_dict] required")
+    if x.dtype != torch.bfloat16 or w_enc.dtype != torch.bfloat16 or b_enc.dtype != torch.float32:
+        raise ProfkError("x and w_enc must be bfloat16, b_enc float32")
+    if not (x.is_contiguous() and w_enc.is_contiguous() and b_enc.is_contiguous()):
+        raise ProfkError("x, w_enc and b_enc must be contiguous")
+    return x.shape[0], x.shape[1], w_enc.shape[0]
+
+
+def sae_workspace(p, B, d_dict, device="cuda"):
+    torch = _torch()
+    n = int(lib().profk_sae_workspace_size(ctypes.byref(p), B, d_dict))
+    if n == 0:
+        raise ProfkError("plan does not match the latent shape")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def sae_encode_topk(x, w_enc, b_enc, k_row, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None,
+                    info=None):
+    """BatchTopK over the SAE latents relu(x w_enc^T + b_enc), with Prof-K
+    fused into the encoder GEMM: (values fp32 [K], flat indices [K], info)."""
+    torch = _torch()
+    B, d_model, d_dict = _sae_shape(x, w_enc, b_enc)
+    K = B * k_row
+    p = p if p is not None else plan(B * d_dict, K, eps, recall)
+    ws = ws if ws is not None else sae_workspace(p, B, d_dict, x.device)
+    if out is None:
+        out = (torch.empty(K, dtype=torch.float32, device=x.device),
+               torch.empty(K, dtype=torch.int64, device=x.device))
+    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    _check(lib().profk_sae_encode_topk(ctypes.byref(p), _ptr(x), _ptr(w_enc), _ptr(b_enc), B, d_model, d_dict,
+                                       k_row, seed, _ptr(out[0]), _ptr(out[1]), _ptr(ws), ws.numel(),
+                                       _stream(), _ptr(info)))
+    return out[0], out[1], info
+
+
+def sae_encode_dense(x, w_enc, b_enc, out=None):
+    """The latent matrix relu(x w_enc^T + b_enc), fp32 [B, d_dict]."""
+    torch = _torch()
+    B, d_model, d_dict = _sae_shape(x, w_enc, b_enc)
+    out = out if out is not None else torch.empty((B, d_dict), dtype=torch.float32, device=x.device)
+    _check(lib().profk_sae_encode_dense(_ptr(x), _ptr(w_enc), _ptr(b_enc), B, d_model, d_dict, _ptr(out),
+                                        _stream()))
+    return out
+
+
+def sae_decode(vals, flat_idx, w_dec, b_dec, B, out=None, ws=None):
+    """x_hat fp32 [B, d_model] from selected latents (flat indices b*d_dict + j)."""
+    torch = _torch()
+    d_dict, d_model = w_dec.shape
+    K = vals.numel()
+    if w_dec.dtype != torch.bfloat16 or b_dec.dtype != torch.float32 or vals.dtype != torch.float32 or \
+            flat_idx.dtype != torch.int64 or flat_idx.numel() != K:
+        raise ProfkError("vals fp32 [K], flat_idx int64 [K], w_dec bf16 [d_dict, d_model], b_dec fp32 [d_model]")
+    out = out if out is not None else torch.empty((B, d_model), dtype=torch.float32, device=vals.device)
+    n = int(lib().profk_sae_decode_workspace_size(B, K))
+    ws = ws if ws is not None else torch.empty(max(n, 1), dtype=torch.uint8, device=vals.device)
+    _check(lib().profk_sae_decode(_ptr(vals), _ptr(flat_idx), K, _ptr(w_dec), _ptr(b_dec), B, d_model, d_dict,
+                                  _ptr(out), _ptr(ws), ws.numel(), _stream()))
+    return out
+
+
+def debug_sae_sample(x, w_enc, b_enc, p, seed=0, ws=None):
+    """The keys of the S latents the fused path samples (uint32 as int64)."""
+    torch = _torch()
+    B, d_model, d_dict = _sae_shape(x, w_enc, b_enc)
+    ws = ws if ws is not None else sae_workspace(p, B, d_dict, x.device)
+    keys = torch.empty(p.S, dtype=torch.int32, device=x.device)
+    _check(lib().profk_debug_sae_sample(ctypes.byref(p), _ptr(x), _ptr(w_enc), _ptr(b_enc), B, d_model, d_dict,
+                                        seed, _ptr(keys), _ptr(ws), ws.numel(), _stream()))
+    return keys.to(torch.int64) & 0xFFFFFFFF
+

@@ -59,6 +59,17 @@ int run_flat(const profk_plan_t* plan, int32_t dtype, const void* values, int64_
   return e == hipSuccess ? PROFK_OK : hip_fail(e);
 }
 
+int check_sae_shape(const void* x, const void* w_enc, const float* b_enc, int64_t B, int64_t d_model,
+                    int64_t d_dict) {
+  if (!x || !w_enc || !b_enc) return PROFK_ENULL;
+  if (B < 1 || d_model < 64 || d_model % 64 != 0 || d_dict < 1) return PROFK_EINVAL;
+  if (d_model > (1 << 16) || B > static_cast<int64_t>(UINT32_MAX) / d_dict) return PROFK_EINVAL;
+  if (reinterpret_cast<uintptr_t>(x) % 16 != 0 || reinterpret_cast<uintptr_t>(w_enc) % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(b_enc) % 4 != 0)
+    return PROFK_EINVAL;
+  return PROFK_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -125,6 +136,91 @@ int profk_batchtopk(const profk_plan_t* plan, int32_t dtype, const void* values,
   if (B > static_cast<int64_t>(UINT32_MAX) / D) return PROFK_EINVAL;
   return run_flat(plan, dtype, values, B * D, B * k_row, seed, 0, out_vals, out_flat_idx, ws, ws_bytes,
                   stream, info_dev, 0, 0);
+}
+
+// ---- BatchTopK SAE layer ----
+
+size_t profk_sae_workspace_size(const profk_plan_t* plan, int64_t B, int64_t d_dict) {
+  if (!plan || !plan_consistent(plan) || B < 1 || d_dict < 1 || plan->N != B * d_dict) return 0;
+  return profk::sae_layout(*plan, static_cast<uint32_t>(B), static_cast<uint32_t>(d_dict),
+                           profk::device_cu_count())
+      .bytes;
+}
+
+int profk_sae_encode_topk(const profk_plan_t* plan, const void* x, const void* w_enc, const float* b_enc,
+                          int64_t B, int64_t d_model, int64_t d_dict, int64_t k_row, uint64_t seed,
+                          float* out_vals, int64_t* out_flat_idx, void* ws, size_t ws_bytes, void* stream,
+                          profk_info_t* info_dev) {
+  if (!plan || !out_vals || !out_flat_idx || !ws) return PROFK_ENULL;
+  int rc = check_sae_shape(x, w_enc, b_enc, B, d_model, d_dict);
+  if (rc != PROFK_OK) return rc;
+  if (k_row < 1 || k_row > d_dict) return PROFK_EINVAL;
+  if (!plan_consistent(plan) || plan->N != B * d_dict || plan->k != B * k_row || plan->lexicographic)
+    return PROFK_EINVAL;
+  const profk::SaeLayout L = profk::sae_layout(*plan, static_cast<uint32_t>(B), static_cast<uint32_t>(d_dict),
+                                               profk::device_cu_count());
+  if (ws_bytes < L.bytes) return PROFK_EWORKSPACE;
+  profk::SaeCall c{plan, x, w_enc, b_enc, static_cast<uint32_t>(B), static_cast<uint32_t>(d_model),
+                   static_cast<uint32_t>(d_dict), static_cast<uint32_t>(B * k_row), seed, out_vals, out_flat_idx,
+                   static_cast<uint8_t*>(ws), L, static_cast<hipStream_t>(stream), info_dev, nullptr,
+                   g_ev_before, g_ev_after};
+  const hipError_t e = profk::launch_sae_topk(c);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
+int profk_sae_encode_dense(const void* x, const void* w_enc, const float* b_enc, int64_t B, int64_t d_model,
+                           int64_t d_dict, float* out, void* stream) {
+  if (!out) return PROFK_ENULL;
+  int rc = check_sae_shape(x, w_enc, b_enc, B, d_model, d_dict);
+  if (rc != PROFK_OK) return rc;
+  profk::SaeCall c{};
+  c.x = x;
+  c.w = w_enc;
+  c.bias = b_enc;
+  c.B = static_cast<uint32_t>(B);
+  c.d_model = static_cast<uint32_t>(d_model);
+  c.d_dict = static_cast<uint32_t>(d_dict);
+  c.stream = static_cast<hipStream_t>(stream);
+  const hipError_t e = profk::launch_sae_dense(c, out);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
+int profk_debug_sae_sample(const profk_plan_t* plan, const void* x, const void* w_enc, const float* b_enc,
+                           int64_t B, int64_t d_model, int64_t d_dict, uint64_t seed, uint32_t* keys_dev,
+                           void* ws, size_t ws_bytes, void* stream) {
+  if (!plan || !keys_dev || !ws) return PROFK_ENULL;
+  int rc = check_sae_shape(x, w_enc, b_enc, B, d_model, d_dict);
+  if (rc != PROFK_OK) return rc;
+  if (!plan_consistent(plan) || plan->N != B * d_dict || plan->mode != PROFK_MODE_FILTER) return PROFK_EINVAL;
+  const profk::SaeLayout L = profk::sae_layout(*plan, static_cast<uint32_t>(B), static_cast<uint32_t>(d_dict),
+                                               profk::device_cu_count());
+  if (ws_bytes < L.bytes) return PROFK_EWORKSPACE;
+  profk::SaeCall c{plan, x, w_enc, b_enc, static_cast<uint32_t>(B), static_cast<uint32_t>(d_model),
+                   static_cast<uint32_t>(d_dict), static_cast<uint32_t>(plan->k), seed, nullptr, nullptr,
+                   static_cast<uint8_t*>(ws), L, static_cast<hipStream_t>(stream), nullptr, keys_dev};
+  const hipError_t e = profk::launch_sae_sample(c);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
+size_t profk_sae_decode_workspace_size(int64_t B, int64_t K) {
+  if (B < 1 || K < 0 || B > static_cast<int64_t>(INT32_MAX) || K > static_cast<int64_t>(UINT32_MAX)) return 0;
+  return profk::sae_decode_workspace(static_cast<uint32_t>(B), static_cast<uint32_t>(K));
+}
+
+int profk_sae_decode(const float* vals, const int64_t* flat_idx, int64_t K, const void* w_dec,
+                     const float* b_dec, int64_t B, int64_t d_model, int64_t d_dict, float* out, void* ws,
+                     size_t ws_bytes, void* stream) {
+  if (!vals || !flat_idx || !w_dec || !b_dec || !out || !ws) return PROFK_ENULL;
+  if (K < 1 || B < 1 || d_model < 1 || d_dict < 1 || d_dict > static_cast<int64_t>(profk::sae_decode_max_dict()))
+    return PROFK_EINVAL;
+  if (B > static_cast<int64_t>(UINT32_MAX) / d_dict || K > B * d_dict || d_model > (1 << 16)) return PROFK_EINVAL;
+  if (reinterpret_cast<uintptr_t>(w_dec) % 2 != 0) return PROFK_EINVAL;
+  if (ws_bytes < profk_sae_decode_workspace_size(B, K)) return PROFK_EWORKSPACE;
+  profk::SaeDecodeCall c{vals, flat_idx, static_cast<uint32_t>(K), static_cast<uint32_t>(B),
+                         static_cast<uint32_t>(d_model), static_cast<uint32_t>(d_dict), w_dec, b_dec, out, ws,
+                         static_cast<hipStream_t>(stream)};
+  const hipError_t e = profk::launch_sae_decode(c);
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
 }
 
 int profk_topk_rows(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t B, int64_t D,

@@ -24,24 +24,10 @@
 #include "device_common.h"
 #include "filter_tile.h"
 #include "launch.h"
+#include "sample_union.h"
 #include "topk_block.h"
 
 namespace profk {
-
-// Clears the per-call counters; fhist (kLogBins words, or null) is the
-// refinement histogram the filter accumulates into.
-__device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt, uint32_t* fhist) {
-  if (threadIdx.x < kSegs) seg_cnt[threadIdx.x * kSegStride] = 0;
-  if (fhist)
-    for (uint32_t i = threadIdx.x; i < kLogBins; i += blockDim.x) fhist[i] = 0;
-  if (threadIdx.x == 0) {
-    st->ticket = 0;
-    st->status = 0;
-    st->tie_above = 0;
-    st->tie_n = 0;
-    st->tie_ticket = 0;
-  }
-}
 
 // ------------------------------------------------------------ stage 1 -----
 struct SampleArgs {
@@ -56,13 +42,8 @@ struct SampleArgs {
 
 template <int DT>
 __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
-  constexpr int NW = kSampBS / kWave;
-  __shared__ uint32_t keys[kSampPerBlock];
-  __shared__ uint32_t lists[NW][kWaveTopMax];
-  __shared__ uint32_t list_n[NW];
-  __shared__ SelectShared sel;
-  __shared__ uint32_t emitted;
-  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  __shared__ SampleUnionShared sh;
+  const uint32_t b = blockIdx.x, tid = threadIdx.x;
   if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist);
   const uint32_t j0 = b * kSampPerBlock;
   const uint32_t nb = min(static_cast<uint32_t>(kSampPerBlock), a.S - j0);
@@ -81,49 +62,7 @@ __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
       }
     }
   }
-  uint32_t* dst = a.union_keys + static_cast<size_t>(b) * a.tcap;
-  const uint32_t tl = min(a.t, nb);
-  if (a.t <= kWaveTopMax) {
-    // each wave keeps its top-tl draws, then wave 0 merges the NW lists
-    uint32_t last;
-    const uint32_t got = wave_top_t<4>(kv, valid, tl, lists[w], last);
-    if (lane == 0) list_n[w] = got;
-    __syncthreads();
-    if (w == 0) {
-      constexpr int E2 = NW * kWaveTopMax / kWave;
-      uint32_t v2[E2];
-      uint32_t valid2 = 0;
-#pragma unroll
-      for (int e = 0; e < E2; ++e) {
-        // concatenated list position c = lane + 64*e
-        uint32_t c = lane + kWave * e, li = 0;
-        v2[e] = 0;
-#pragma unroll
-        for (int i = 0; i < NW; ++i)
-          if (li == static_cast<uint32_t>(i) && c >= list_n[i]) { c -= list_n[i]; li = i + 1; }
-        if (li < NW) { v2[e] = lists[li][c]; valid2 |= 1u << e; }
-      }
-      wave_top_t<E2>(v2, valid2, tl, dst, last);
-    }
-    return;
-  }
-#pragma unroll
-  for (int q = 0; q < 4; ++q)
-    if ((valid >> q) & 1u) keys[4 * tid + q] = kv[q];
-  __syncthreads();
-  if (tl == nb) {
-    for (uint32_t j = tid; j < nb; j += kSampBS) dst[j] = keys[j];
-    return;
-  }
-  auto visit = [&](auto f) {
-    for (uint32_t j = tid; j < nb; j += kSampBS) f(keys[j]);
-  };
-  const SelectResult r = block_select_kth<kSampBS>(visit, tl, Elem<DT>::KEYBITS, 0u, sel);
-  if (tid == 0) emitted = 0;
-  __syncthreads();
-  for (uint32_t j = tid; j < nb; j += kSampBS)
-    if (keys[j] > r.kth) dst[atomicAdd(&emitted, 1u)] = keys[j];
-  for (uint32_t j = r.above + tid; j < tl; j += kSampBS) dst[j] = r.kth;
+  sample_block_top<Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
 }
 
 // ------------------------------------------------------------ stage 2 -----
@@ -935,6 +874,36 @@ static hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t
   return hipGetLastError();
 }
 
+// Stages 4 and 5 on the candidates the filter left in the workspace (G_f
+// workgroups wrote blk_max); the fallback reads c.values.
+template <int DT>
+static hipError_t launch_refine_t(const FlatCall& c, bool direct, uint32_t G_f) {
+  const FlatLayout& L = c.L;
+  const profk_plan_t& p = *c.plan;
+  CallState* st = at<CallState>(c.ws, L.off_state);
+  uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
+  uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
+  if (L.big) {
+    BigCall bc{DT, c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
+               direct ? 1 : 0, seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
+               at<uint32_t>(c.ws, L.off_blk_max), L.seg_cap, G_f, st, c.ws + L.off_big_state,
+               at<uint32_t>(c.ws, L.off_ghist), at<uint64_t>(c.ws, L.off_staging), at<uint64_t>(c.ws, L.off_runs),
+               fhist, at<uint32_t>(c.ws, L.off_boff), at<uint32_t>(c.ws, L.off_bcur),
+               at<uint32_t>(c.ws, L.off_blist),
+               L.G_big, c.out_vals, c.out_idx, c.info, c.stream};
+    return launch_big(bc);
+  }
+  FinishArgs fa{c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
+                direct ? 1 : 0, G_f, L.seg_cap,
+                seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
+                at<uint32_t>(c.ws, L.off_blk_max), st,
+                L.G_fb, L.chunk, at<uint32_t>(c.ws, L.off_cand_key), at<uint32_t>(c.ws, L.off_cand_idx),
+                at<uint32_t>(c.ws, L.off_cand_cnt), fhist,
+                c.out_vals, c.out_idx, c.info};
+  hipLaunchKernelGGL(k_finish<DT>, dim3(L.G_fb), dim3(kFinBS), 0, c.stream, fa);
+  return hipGetLastError();
+}
+
 template <int DT>
 static hipError_t launch_flat_t(const FlatCall& c) {
   const FlatLayout& L = c.L;
@@ -968,30 +937,23 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (!direct && (e = launch_filter<DT>(c, st, union_for_filter, lex)) != hipSuccess) return e;
-  if (L.big) {
-    BigCall bc{DT, c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
-               direct ? 1 : 0, seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
-               at<uint32_t>(c.ws, L.off_blk_max), L.seg_cap, L.G_f, st, c.ws + L.off_big_state,
-               at<uint32_t>(c.ws, L.off_ghist), at<uint64_t>(c.ws, L.off_staging), at<uint64_t>(c.ws, L.off_runs),
-               fhist, at<uint32_t>(c.ws, L.off_boff), at<uint32_t>(c.ws, L.off_bcur),
-               at<uint32_t>(c.ws, L.off_blist),
-               L.G_big, c.out_vals, c.out_idx, c.info, c.stream};
-    return launch_big(bc);
-  }
-  FinishArgs fa{c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
-                direct ? 1 : 0, L.G_f, L.seg_cap,
-                seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
-                at<uint32_t>(c.ws, L.off_blk_max), st,
-                L.G_fb, L.chunk, at<uint32_t>(c.ws, L.off_cand_key), at<uint32_t>(c.ws, L.off_cand_idx),
-                at<uint32_t>(c.ws, L.off_cand_cnt), at<uint32_t>(c.ws, L.off_fhist),
-                c.out_vals, c.out_idx, c.info};
-  hipLaunchKernelGGL(k_finish<DT>, dim3(L.G_fb), dim3(kFinBS), 0, c.stream, fa);
-  return hipGetLastError();
+  return launch_refine_t<DT>(c, direct, L.G_f);
 }
 
 hipError_t launch_flat(const FlatCall& c) {
   (void)hipGetLastError();  // report only errors of this call's launches
   return c.dtype == PROFK_F32 ? launch_flat_t<0>(c) : launch_flat_t<1>(c);
+}
+
+hipError_t launch_refine(const FlatCall& c, uint32_t G_f) {
+  return c.dtype == PROFK_F32 ? launch_refine_t<0>(c, false, G_f) : launch_refine_t<1>(c, false, G_f);
+}
+
+hipError_t launch_select_tau(const uint32_t* union_keys, uint32_t n, uint32_t t, int keybits, CallState* st,
+                             hipStream_t s) {
+  TauArgs ta{union_keys, n, t, keybits, st};
+  hipLaunchKernelGGL(k_select_tau, dim3(1), dim3(kTauBS), 0, s, ta);
+  return hipGetLastError();
 }
 
 hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t N, int64_t* out,

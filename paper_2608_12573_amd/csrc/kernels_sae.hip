@@ -1,0 +1,560 @@
+// The BatchTopK SAE layer with Prof-K in the encoder's epilogue (Sec. 5,
+// "Application: BatchTopK Sparse Autoencoders": the K = B*k largest of the
+// B x d_dict post-ReLU latents, flattened).
+//
+//   z[b, j] = relu(sum_m x[b, m] W_enc[j, m] + b_enc[j])     (bf16 inputs,
+//                                                             fp32 sums)
+//
+// The latent matrix is never written to HBM:
+//   k_sae_sample   stage 1: the S sampled latents, each computed with the same
+//                  MFMA sequence as the GEMM (so its value is the GEMM's, bit
+//                  for bit), and each sample workgroup's top-t of them;
+//   k_select_tau   stage 2 (shared with the vector path);
+//   k_sae_filter   the GEMM with stage 3 in its epilogue: survivors are
+//                  compacted exactly as the vector filter does it, so the
+//                  vector path's refinement (stage 4) runs unchanged;
+//   k_sae_dense    the GEMM with a dense epilogue: for the exact fallback only
+//                  (it returns at once when the filter's count is in range),
+//                  and as an inspection entry point.
+// Sparse decode (k_dec_*): x_hat[b, :] = sum over b's selected latents of
+// z W_dec[j, :] + b_dec, grouped by row and summed in ascending j, so the
+// result does not depend on the order the selection lists them in.
+//
+// GEMM shape: a workgroup of 4 waves computes a 128x128 tile of z, a wave a
+// 64x64 block as 2x2 v_mfma_f32_32x32x16_bf16 accumulators; d_model is
+// consumed in chunks of 64 staged through LDS (rows padded to 144 B).
+// One 32x32x16 step rounds once: the accumulator and its 16 products are
+// summed together before rounding to fp32.
+#include "device_common.h"
+#include "launch.h"
+#include "sample_union.h"
+
+namespace profk {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+
+constexpr int kSaeBS = 256;
+constexpr uint32_t kSaeBM = 128, kSaeBN = 128, kSaeBK = 64;
+constexpr uint32_t kSaeLd = kSaeBK + 8;  // LDS row stride in bf16 elements
+constexpr uint32_t kSaeMaxBlocks = 1024;
+
+struct SaeGemm {
+  const uint16_t* x;  // [B, d_model] bf16 bits, 16-byte aligned rows
+  const uint16_t* w;  // [d_dict, d_model]
+  const float* bias;  // [d_dict]
+  uint32_t B, d_model, d_dict;
+};
+
+struct alignas(16) SaeTileLds {
+  uint16_t a[kSaeBM * kSaeLd];
+  uint16_t b[kSaeBN * kSaeLd];
+};
+
+__device__ __forceinline__ float sae_relu(float pre) { return pre > 0.0f ? pre : 0.0f; }
+
+// acc[bm][bn] = this wave's 64x64 part of the product for the tile at (m0, n0).
+__device__ __forceinline__ void sae_tile_mma(const SaeGemm& g, uint32_t m0, uint32_t n0, SaeTileLds& sh,
+                                             f32x16 (&acc)[2][2]) {
+  const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const uint32_t wm = w >> 1, wn = w & 1;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  const uint32_t nchunk = g.d_model / kSaeBK;
+  // a 128 x 64 chunk is 1024 16-byte pieces: 4 per thread, 8 per row
+  u32x4v ra[4], rb[4];
+  auto gload = [&](uint32_t kc) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t id = q * kSaeBS + tid, row = id >> 3, seg = id & 7;
+      const uint32_t gm = m0 + row, gn = n0 + row;
+      const size_t col = static_cast<size_t>(kc) * kSaeBK + seg * 8;
+      ra[q] = gm < g.B ? *reinterpret_cast<const u32x4v*>(g.x + static_cast<size_t>(gm) * g.d_model + col)
+                       : u32x4v{0u, 0u, 0u, 0u};
+      rb[q] = gn < g.d_dict ? *reinterpret_cast<const u32x4v*>(g.w + static_cast<size_t>(gn) * g.d_model + col)
+                            : u32x4v{0u, 0u, 0u, 0u};
+    }
+  };
+  gload(0);
+  for (uint32_t kc = 0; kc < nchunk; ++kc) {
+    __syncthreads();  // every wave is done with the previous chunk
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t id = q * kSaeBS + tid, row = id >> 3, seg = id & 7;
+      *reinterpret_cast<u32x4v*>(&sh.a[row * kSaeLd + seg * 8]) = ra[q];
+      *reinterpret_cast<u32x4v*>(&sh.b[row * kSaeLd + seg * 8]) = rb[q];
+    }
+    __syncthreads();
+    if (kc + 1 < nchunk) gload(kc + 1);
+#pragma unroll
+    for (uint32_t ks = 0; ks < kSaeBK / 16; ++ks) {
+      const uint32_t kofs = ks * 16 + 8 * (lane >> 5);
+      bf16x8 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = *reinterpret_cast<const bf16x8*>(&sh.a[(wm * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
+        fb[i] = *reinterpret_cast<const bf16x8*>(&sh.b[(wn * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+// Tile-local row and column of accumulator element v of block (i, j).
+__device__ __forceinline__ uint32_t sae_row(uint32_t lane, uint32_t w, int i, int v) {
+  return (w >> 1) * 64 + i * 32 + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
+}
+__device__ __forceinline__ uint32_t sae_col(uint32_t lane, uint32_t w, int j) {
+  return (w & 1) * 64 + j * 32 + (lane & 31);
+}
+
+// ------------------------------------------------------------ stage 1 -----
+struct SaeSampleArgs {
+  SaeGemm g;
+  uint64_t seed;
+  uint32_t S, t, tcap;
+  uint32_t* union_keys;
+  CallState* st;
+  uint32_t* seg_cnt;
+  uint32_t* fhist;
+  uint32_t* sample_keys;  // optional: every draw's key (inspection)
+};
+
+// Draw j is word j%4 of Philox block j/4 (row 0) over the N = B*d_dict
+// flattened latents.  A wave takes 32 draws at a time: lane L and L+32 feed
+// draw L%32's input row and weight row to the MFMA, and the draw's latent is
+// the diagonal element (L%32, L%32) of the 32x32 result: the same sums, in
+// the same order, as the GEMM computes for that element.
+__global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
+  __shared__ SampleUnionShared sh;
+  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist);
+  const uint32_t j0 = b * kSampPerBlock;
+  const uint32_t nb = min(static_cast<uint32_t>(kSampPerBlock), a.S - j0);
+  const uint64_t N = static_cast<uint64_t>(a.g.B) * a.g.d_dict;
+  constexpr uint32_t kPerWave = kSampPerBlock / (kSampBS / kWave);
+  for (uint32_t grp = 0; grp < kPerWave / 32; ++grp) {
+    const uint32_t jl = w * kPerWave + grp * 32 + (lane & 31);
+    const bool in = jl < nb;
+    uint32_t r = 0, c = 0;
+    if (in) {
+      const uint64_t jg = static_cast<uint64_t>(j0) + jl;
+      const U64x4 p = philox4x64_10(jg >> 2, 0, 0, 0, a.seed, 0);
+      const uint64_t flat = index_of_word(p.w[jg & 3], N);
+      r = static_cast<uint32_t>(flat / a.g.d_dict);
+      c = static_cast<uint32_t>(flat % a.g.d_dict);
+    }
+    const uint16_t* xr = a.g.x + static_cast<size_t>(r) * a.g.d_model + 8 * (lane >> 5);
+    const uint16_t* wr = a.g.w + static_cast<size_t>(c) * a.g.d_model + 8 * (lane >> 5);
+    f32x16 acc{};
+    for (uint32_t k0 = 0; k0 < a.g.d_model; k0 += 16) {
+      bf16x8 fa = bf16x8{}, fb = bf16x8{};
+      if (in) {
+        fa = *reinterpret_cast<const bf16x8*>(xr + k0);
+        fb = *reinterpret_cast<const bf16x8*>(wr + k0);
+      }
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc, 0, 0, 0);
+    }
+    // element (i, i), i = lane % 32, is held by lane i + 32*((i>>2)&1) as
+    // accumulator 4*(i>>3) + (i&3)
+    const uint32_t i = lane & 31, v = 4 * (i >> 3) + (i & 3);
+    float d = acc[0];
+#pragma unroll
+    for (int q = 1; q < 16; ++q) d = v == static_cast<uint32_t>(q) ? acc[q] : d;
+    if (in && (lane >> 5) == ((i >> 2) & 1)) {
+      const uint32_t key = key_f32(__float_as_uint(sae_relu(d + a.g.bias[c])));
+      sh.keys[jl] = key;
+      if (a.sample_keys) a.sample_keys[j0 + jl] = key;
+    }
+  }
+  __syncthreads();
+  uint32_t kv[4];
+  uint32_t valid = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t j = 4 * tid + q;
+    kv[q] = j < nb ? sh.keys[j] : 0u;
+    if (j < nb) valid |= 1u << q;
+  }
+  __syncthreads();
+  sample_block_top<32>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
+}
+
+// ------------------------------------------------------------ stage 3 -----
+struct SaeFilterArgs {
+  SaeGemm g;
+  uint32_t tiles_n, tiles;
+  CallState* st;
+  uint32_t seg_cap;
+  uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
+  uint32_t* fhist;  // refinement histogram, zero on entry
+};
+
+// Persistent: workgroup b takes tiles b, b + G, ...  Survivors (key >= tau)
+// get workgroup-stage slots from a wave prefix sum (slots past the stage go
+// straight to the workgroup's candidate segment); at the end the stage is
+// appended with one atomic, the maximum key goes to blk_max[b] and the
+// non-empty log-bin counts to fhist -- the vector filter's outputs.
+__global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
+  __shared__ SaeTileLds tl;
+  __shared__ uint32_t s_skey[kStage], s_sidx[kStage];
+  __shared__ uint32_t s_hist[kLogBins];
+  __shared__ uint32_t s_cnt, s_base, s_wmax[kSaeBS / kWave];
+  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const uint32_t seg = b & (kSegs - 1);
+  const uint32_t tau = a.st->tau_key;
+  for (uint32_t i = tid; i < kLogBins; i += kSaeBS) s_hist[i] = 0;
+  if (tid == 0) s_cnt = 0;
+  uint32_t* const seg_counter = a.seg_cnt + seg * kSegStride;
+  uint32_t* const seg_key = a.seg_key + static_cast<size_t>(seg) * a.seg_cap;
+  uint32_t* const seg_idx = a.seg_idx + static_cast<size_t>(seg) * a.seg_cap;
+  uint32_t my_max = 0;
+  for (uint32_t tile = b; tile < a.tiles; tile += gridDim.x) {
+    const uint32_t m0 = (tile / a.tiles_n) * kSaeBM, n0 = (tile % a.tiles_n) * kSaeBN;
+    f32x16 acc[2][2];
+    sae_tile_mma(a.g, m0, n0, tl, acc);
+    // Epilogue, one 32x32 block of each wave at a time, staged in the wave's
+    // own 4 KB of the (now idle) tile buffers: relu(acc + bias), or a key-0
+    // marker outside the matrix; then lane L tests elements 16L..16L+15.
+    float* const stage = reinterpret_cast<float*>(&tl) + w * 1024;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        __syncthreads();  // the tile buffers (first block) or this wave's stage (later blocks) are free
+        const uint32_t c = n0 + sae_col(lane, w, j);
+        const float bias = c < a.g.d_dict ? a.g.bias[c] : 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const uint32_t rl = 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
+          const bool ok = c < a.g.d_dict && m0 + sae_row(lane, w, i, v) < a.g.B;
+          stage[rl * 32 + (lane & 31)] = ok ? sae_relu(acc[i][j][v] + bias) : __uint_as_float(0xFFFFFFFFu);
+        }
+        __syncthreads();
+        const uint32_t r0 = m0 + (w >> 1) * 64 + i * 32, c0 = n0 + (w & 1) * 64 + j * 32;
+        uint32_t cnt = 0;
+        for (uint32_t q = 0; q < 16; ++q) cnt += key_f32(__float_as_uint(stage[lane * 16 + q])) >= tau ? 1u : 0u;
+        if (__ballot(cnt != 0) == 0) continue;
+        // one stage reservation per wave
+        const uint32_t incl = wave_incl_sum(cnt);
+        const uint32_t total = __shfl(incl, kWave - 1, kWave);
+        uint32_t base = 0;
+        if (lane == 0) base = atomicAdd(&s_cnt, total);
+        base = __shfl(base, 0, kWave);
+        const uint32_t n_in = base < kStage ? min(total, kStage - base) : 0u;
+        uint32_t gbase = 0;
+        if (total - n_in) {
+          if (lane == 0) gbase = atomicAdd(seg_counter, total - n_in);
+          gbase = __shfl(gbase, 0, kWave);
+        }
+        const uint32_t first_over = base + n_in;
+        uint32_t slot = base + incl - cnt;
+        for (uint32_t q = 0; q < 16 && cnt; ++q) {
+          const uint32_t e = lane * 16 + q;
+          const uint32_t key = key_f32(__float_as_uint(stage[e]));
+          if (key < tau) continue;
+          --cnt;
+          const uint32_t idx = (r0 + e / 32) * a.g.d_dict + c0 + e % 32;
+          my_max = max(my_max, key);
+          atomicAdd(&s_hist[log_bin(key - tau)], 1u);
+          if (slot < kStage) {
+            s_skey[slot] = key;
+            s_sidx[slot] = idx;
+          } else {
+            const uint32_t gp = gbase + (slot - first_over);
+            if (gp < a.seg_cap) {
+              seg_key[gp] = key;
+              seg_idx[gp] = idx;
+            }
+          }
+          ++slot;
+        }
+      }
+  }
+  const uint32_t wm = wave_max_u32(my_max);
+  if (lane == 0) s_wmax[w] = wm;
+  __syncthreads();
+  const uint32_t n_st = min(s_cnt, kStage);
+  if (tid == 0) {
+    s_base = n_st ? atomicAdd(seg_counter, n_st) : 0u;
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < kSaeBS / kWave; ++i) m = max(m, s_wmax[i]);
+    a.blk_max[b] = m;
+  }
+  __syncthreads();
+  for (uint32_t i = tid; i < n_st; i += kSaeBS) {
+    const uint32_t gp = s_base + i;
+    if (gp < a.seg_cap) {
+      seg_key[gp] = s_skey[i];
+      seg_idx[gp] = s_sidx[i];
+    }
+  }
+  if (s_cnt) {
+    for (uint32_t i = tid; i < kLogBins; i += kSaeBS) {
+      const uint32_t c = s_hist[i];
+      if (c) atomicAdd(&a.fhist[i], c);
+    }
+  }
+}
+
+// ------------------------------------------------------------- dense ------
+struct SaeDenseArgs {
+  SaeGemm g;
+  uint32_t tiles_n;
+  float* out;               // [B, d_dict]
+  const uint32_t* seg_cnt;  // null: always write; else only when the count is outside [k_req, M]
+  uint32_t k_req, M;
+};
+
+__global__ __launch_bounds__(kSaeBS) void k_sae_dense(SaeDenseArgs a) {
+  __shared__ SaeTileLds tl;
+  if (a.seg_cnt) {
+    uint32_t total = 0;
+#pragma unroll
+    for (int x = 0; x < kSegs; ++x) total += a.seg_cnt[x * kSegStride];
+    if (total >= a.k_req && total <= a.M) return;  // filtered: the candidates suffice
+  }
+  const uint32_t lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const uint32_t m0 = (blockIdx.x / a.tiles_n) * kSaeBM, n0 = (blockIdx.x % a.tiles_n) * kSaeBN;
+  f32x16 acc[2][2];
+  sae_tile_mma(a.g, m0, n0, tl, acc);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const uint32_t c = n0 + sae_col(lane, w, j);
+    if (c >= a.g.d_dict) continue;
+    const float bias = a.g.bias[c];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const uint32_t r = m0 + sae_row(lane, w, i, v);
+        if (r < a.g.B) a.out[static_cast<size_t>(r) * a.g.d_dict + c] = sae_relu(acc[i][j][v] + bias);
+      }
+  }
+}
+
+// ------------------------------------------------------------ decode ------
+// Selected latents grouped by row: counts, offsets, a scatter, then one
+// workgroup per row places its entries by latent index in LDS and sums them
+// in ascending index order.
+constexpr uint32_t kDecMaxDict = 16384;  // LDS per row: one float and one flag per latent
+constexpr int kDecBS = 256;
+
+struct DecArgs {
+  const float* vals;
+  const int64_t* idx;  // flat b*d_dict + j; -1 (padding) and out-of-range entries are skipped
+  uint32_t K, B, d_model, d_dict;
+  const uint16_t* w;   // W_dec [d_dict, d_model] bf16 bits
+  const float* bias;   // b_dec [d_model]
+  float* out;          // [B, d_model]
+  uint32_t* row_cnt;   // [B + 1]
+  uint32_t* row_off;   // [B + 1]
+  uint32_t* row_fill;  // [B]
+  uint32_t* grouped;   // [K] positions into vals/idx
+};
+
+__global__ void k_dec_clear(DecArgs a) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i <= a.B; i += gridDim.x * blockDim.x) {
+    a.row_cnt[i] = 0;
+    if (i < a.B) a.row_fill[i] = 0;
+  }
+}
+
+__global__ void k_dec_count(DecArgs a) {
+  const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= a.K) return;
+  const int64_t f = a.idx[e];
+  if (f >= 0 && static_cast<uint64_t>(f) < static_cast<uint64_t>(a.B) * a.d_dict)
+    atomicAdd(&a.row_cnt[static_cast<uint64_t>(f) / a.d_dict], 1u);
+}
+
+__global__ __launch_bounds__(1024) void k_dec_scan(DecArgs a) {
+  __shared__ uint32_t wsum[20];
+  __shared__ uint32_t s_carry;
+  if (threadIdx.x == 0) s_carry = 0;
+  __syncthreads();
+  for (uint32_t base = 0; base < a.B; base += 1024) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t v = i < a.B ? a.row_cnt[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_excl_sum<1024>(v, wsum, &tot);
+    if (i < a.B) a.row_off[i] = s_carry + ex;
+    __syncthreads();
+    if (threadIdx.x == 0) s_carry += tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) a.row_off[a.B] = s_carry;
+}
+
+__global__ void k_dec_scatter(DecArgs a) {
+  const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= a.K) return;
+  const int64_t f = a.idx[e];
+  if (f < 0 || static_cast<uint64_t>(f) >= static_cast<uint64_t>(a.B) * a.d_dict) return;  // padding or out of range
+  const uint32_t r = static_cast<uint32_t>(static_cast<uint64_t>(f) / a.d_dict);
+  a.grouped[a.row_off[r] + atomicAdd(&a.row_fill[r], 1u)] = e;
+}
+
+__global__ __launch_bounds__(kDecBS) void k_dec_rows(DecArgs a) {
+  __shared__ float s_val[kDecMaxDict];
+  __shared__ uint32_t s_has[kDecMaxDict / 32];
+  __shared__ uint32_t s_list[kDecMaxDict];
+  __shared__ uint32_t wsum[20];
+  const uint32_t r = blockIdx.x, tid = threadIdx.x;
+  const uint32_t nw = (a.d_dict + 31) / 32;
+  for (uint32_t i = tid; i < nw; i += kDecBS) s_has[i] = 0;
+  __syncthreads();
+  const uint32_t e0 = a.row_off[r], e1 = a.row_off[r + 1];
+  for (uint32_t p = e0 + tid; p < e1; p += kDecBS) {
+    const uint32_t e = a.grouped[p];
+    const uint32_t j = static_cast<uint32_t>(static_cast<uint64_t>(a.idx[e]) % a.d_dict);
+    s_val[j] = a.vals[e];
+    atomicOr(&s_has[j >> 5], 1u << (j & 31));
+  }
+  __syncthreads();
+  // the row's latent indices, ascending: a prefix sum over the flag words
+  uint32_t n_list = 0;
+  for (uint32_t base = 0; base < nw; base += kDecBS) {
+    const uint32_t i = base + tid;
+    const uint32_t word = i < nw ? s_has[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_excl_sum<kDecBS>(__popc(word), wsum, &tot);
+    uint32_t pos = n_list + ex, rest = word;
+    while (rest) {
+      const uint32_t bit = __builtin_ctz(rest);
+      rest &= rest - 1;
+      s_list[pos++] = i * 32 + bit;
+    }
+    n_list += tot;
+    __syncthreads();
+  }
+  for (uint32_t d = tid; d < a.d_model; d += kDecBS) {
+    float acc = 0.0f;
+    for (uint32_t q = 0; q < n_list; ++q) {
+      const uint32_t j = s_list[q];
+      const uint32_t bits = static_cast<uint32_t>(a.w[static_cast<size_t>(j) * a.d_model + d]) << 16;
+      acc = fmaf(s_val[j], __uint_as_float(bits), acc);
+    }
+    a.out[static_cast<size_t>(r) * a.d_model + d] = acc + a.bias[d];
+  }
+}
+
+// ------------------------------------------------------------- host -------
+static uint32_t cdiv_s(uint64_t a, uint64_t b) { return static_cast<uint32_t>((a + b - 1) / b); }
+
+SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int num_cus) {
+  SaeLayout S;
+  S.flat = flat_layout(plan, PROFK_F32, num_cus);
+  const uint32_t tiles = cdiv_s(B, kSaeBM) * cdiv_s(d_dict, kSaeBN);
+  S.G = tiles < kSaeMaxBlocks ? tiles : kSaeMaxBlocks;
+  if (S.G > S.flat.G_f) S.G = S.flat.G_f;  // blk_max holds G_f entries
+  S.off_dense = (S.flat.bytes + 255) & ~static_cast<size_t>(255);
+  S.bytes = S.off_dense + static_cast<size_t>(B) * d_dict * 4;
+  return S;
+}
+
+static SaeGemm gemm_of(const SaeCall& c) {
+  return SaeGemm{static_cast<const uint16_t*>(c.x), static_cast<const uint16_t*>(c.w), c.bias, c.B, c.d_model,
+                 c.d_dict};
+}
+
+hipError_t launch_sae_dense(const SaeCall& c, float* out) {
+  (void)hipGetLastError();
+  const uint32_t tn = cdiv_s(c.d_dict, kSaeBN), tiles = cdiv_s(c.B, kSaeBM) * tn;
+  SaeDenseArgs da{gemm_of(c), tn, out, nullptr, 0, 0};
+  hipLaunchKernelGGL(k_sae_dense, dim3(tiles), dim3(kSaeBS), 0, c.stream, da);
+  return hipGetLastError();
+}
+
+hipError_t launch_sae_topk(const SaeCall& c) {
+  (void)hipGetLastError();
+  const profk_plan_t& p = *c.plan;
+  const FlatLayout& L = c.L.flat;
+  uint8_t* ws = c.ws;
+  float* dense = reinterpret_cast<float*>(ws + c.L.off_dense);
+  const uint32_t N = c.B * c.d_dict;
+  FlatCall fc{};
+  fc.plan = c.plan;
+  fc.dtype = PROFK_F32;
+  fc.values = dense;
+  fc.n = N;
+  fc.k = c.K;
+  fc.seed = c.seed;
+  fc.row = 0;
+  fc.out_vals = c.out_vals;
+  fc.out_idx = c.out_idx;
+  fc.ws = ws;
+  fc.L = L;
+  fc.stream = c.stream;
+  fc.info = c.info;
+  if (p.mode == PROFK_MODE_DIRECT) {
+    // no sampling pays off: the dense latents, then the exact selection
+    hipError_t e = launch_sae_dense(c, dense);
+    if (e != hipSuccess) return e;
+    return launch_flat(fc);
+  }
+  CallState* st = reinterpret_cast<CallState*>(ws + L.off_state);
+  uint32_t* seg_cnt = reinterpret_cast<uint32_t*>(ws + L.off_segcnt);
+  uint32_t* fhist = reinterpret_cast<uint32_t*>(ws + L.off_fhist);
+  uint32_t* uk = reinterpret_cast<uint32_t*>(ws + L.off_union);
+  const SaeGemm g = gemm_of(c);
+  SaeSampleArgs sa{g, c.seed, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t), L.tcap, uk, st, seg_cnt,
+                   fhist, c.sample_keys};
+  hipLaunchKernelGGL(k_sae_sample, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if ((e = launch_select_tau(uk, L.union_n, static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess) return e;
+  const uint32_t tn = cdiv_s(c.d_dict, kSaeBN), tiles = cdiv_s(c.B, kSaeBM) * tn;
+  SaeFilterArgs fa{g, tn, tiles, st, L.seg_cap, seg_cnt,
+                   reinterpret_cast<uint32_t*>(ws + L.off_seg_key), reinterpret_cast<uint32_t*>(ws + L.off_seg_idx),
+                   reinterpret_cast<uint32_t*>(ws + L.off_blk_max), fhist};
+  if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
+  hipLaunchKernelGGL(k_sae_filter, dim3(c.L.G), dim3(kSaeBS), 0, c.stream, fa);
+  if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
+  // the dense latents only when the candidates do not suffice (exact fallback)
+  SaeDenseArgs da{g, tn, dense, seg_cnt, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M)};
+  hipLaunchKernelGGL(k_sae_dense, dim3(tiles), dim3(kSaeBS), 0, c.stream, da);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_refine(fc, c.L.G);
+}
+
+hipError_t launch_sae_sample(const SaeCall& c) {
+  (void)hipGetLastError();
+  const FlatLayout& L = c.L.flat;
+  SaeSampleArgs sa{gemm_of(c), c.seed, static_cast<uint32_t>(c.plan->S), static_cast<uint32_t>(c.plan->t), L.tcap,
+                   reinterpret_cast<uint32_t*>(c.ws + L.off_union), reinterpret_cast<CallState*>(c.ws + L.off_state),
+                   reinterpret_cast<uint32_t*>(c.ws + L.off_segcnt), reinterpret_cast<uint32_t*>(c.ws + L.off_fhist),
+                   c.sample_keys};
+  hipLaunchKernelGGL(k_sae_sample, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
+  return hipGetLastError();
+}
+
+size_t sae_decode_workspace(uint32_t B, uint32_t K) {
+  return (static_cast<size_t>(B) * 3 + 2 + K) * 4 + 256;
+}
+
+hipError_t launch_sae_decode(const SaeDecodeCall& c) {
+  (void)hipGetLastError();
+  uint32_t* ws = static_cast<uint32_t*>(c.ws);
+  DecArgs a{c.vals, c.idx, c.K, c.B, c.d_model, c.d_dict, static_cast<const uint16_t*>(c.w), c.bias, c.out,
+            ws, ws + (c.B + 1), ws + 2 * (c.B + 1), ws + 2 * (c.B + 1) + c.B};
+  const uint32_t gk = cdiv_s(c.K, 256);
+  hipLaunchKernelGGL(k_dec_clear, dim3(cdiv_s(c.B + 1, 256)), dim3(256), 0, c.stream, a);
+  if (gk) hipLaunchKernelGGL(k_dec_count, dim3(gk), dim3(256), 0, c.stream, a);
+  hipLaunchKernelGGL(k_dec_scan, dim3(1), dim3(1024), 0, c.stream, a);
+  if (gk) hipLaunchKernelGGL(k_dec_scatter, dim3(gk), dim3(256), 0, c.stream, a);
+  hipLaunchKernelGGL(k_dec_rows, dim3(c.B), dim3(kDecBS), 0, c.stream, a);
+  return hipGetLastError();
+}
+
+uint32_t sae_decode_max_dict() { return kDecMaxDict; }
+
+}  // namespace profk

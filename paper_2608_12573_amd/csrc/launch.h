@@ -95,6 +95,11 @@ struct FlatCall {
 };
 
 hipError_t launch_flat(const FlatCall& c);
+// Refinement of the candidates a filter left in c.ws by G_f workgroups
+// (the fallback reads c.values), and tau from a stage-1 union into st.
+hipError_t launch_refine(const FlatCall& c, uint32_t G_f);
+hipError_t launch_select_tau(const uint32_t* union_keys, uint32_t n, uint32_t t, int keybits, CallState* st,
+                             hipStream_t s);
 
 struct BigCall {
   int dtype;
@@ -147,6 +152,53 @@ struct RowCall {
 };
 
 hipError_t launch_rows(const RowCall& c);
+
+// BatchTopK SAE encoder with the filter in its GEMM epilogue.  The
+// workspace is the vector path's (same plan) followed by a dense fp32
+// [B, d_dict] latent buffer that only the exact fallback writes.
+struct SaeLayout {
+  FlatLayout flat;
+  uint32_t G = 0;  // filter workgroups (persistent)
+  size_t off_dense = 0, bytes = 0;
+};
+
+SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int num_cus);
+
+struct SaeCall {
+  const profk_plan_t* plan;
+  const void* x;     // bf16 [B, d_model]
+  const void* w;     // bf16 [d_dict, d_model]
+  const float* bias; // [d_dict]
+  uint32_t B, d_model, d_dict, K;
+  uint64_t seed;
+  float* out_vals;
+  int64_t* out_idx;
+  uint8_t* ws;
+  SaeLayout L;
+  hipStream_t stream;
+  profk_info_t* info;
+  uint32_t* sample_keys;  // optional: the S sampled latents' keys
+  hipEvent_t ev_before = nullptr, ev_after = nullptr;  // around the fused filter launch
+};
+
+hipError_t launch_sae_topk(const SaeCall& c);
+hipError_t launch_sae_sample(const SaeCall& c);  // stage 1 only, with c.sample_keys
+hipError_t launch_sae_dense(const SaeCall& c, float* out);
+
+struct SaeDecodeCall {
+  const float* vals;
+  const int64_t* idx;
+  uint32_t K, B, d_model, d_dict;
+  const void* w;      // bf16 [d_dict, d_model]
+  const float* bias;  // [d_model]
+  float* out;         // [B, d_model]
+  void* ws;
+  hipStream_t stream;
+};
+
+size_t sae_decode_workspace(uint32_t B, uint32_t K);
+uint32_t sae_decode_max_dict();
+hipError_t launch_sae_decode(const SaeDecodeCall& c);
 
 // Inspection helpers.
 hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t N,
