@@ -35,7 +35,8 @@ CSRC = os.path.join(ROOT, "paper_2608_12573_amd", "csrc")
 # Every source the filter kernel is compiled from: the committed counters
 # stand for this exact code and are dropped once any of these changes.
 FILTER_SRCS = ("kernels_flat.hip", "filter_tile.h", "device_common.h", "launch.h", "topk_block.h")
-WORKLOADS = ("c2", "c1", "c3a", "c3b", "c3c", "c3d", "c3d2", "c4", "c5", "c5r", "c5p")
+WORKLOADS = ("c2", "c1", "c3a", "c3b", "c3c", "c3d", "c3d2", "c4", "c5", "c5r", "c5p", "sae")
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 FLUSH_BYTES = 512 << 20
 
 
@@ -94,6 +95,7 @@ class Workload:
     def __init__(self, name, k_arg, torch, pk, wl, lex=False):
         self.name = name
         self.lex = lex
+        self.flops = None   # set for a matrix-core workload
         rule = dict(lexicographic=1) if lex else {}
         self.rows = False
         self.es = 4
@@ -172,6 +174,44 @@ class Workload:
                                              out=self.out, info=self.info, seed=0)
             self.torch_ref = lambda: torch.topk(self.x.view(-1), K, sorted=True)
             self.N, self.k = B * D, K
+        elif name == "sae":
+            # the paper's BatchTopK SAE shape, with the selection fused into
+            # the encoder GEMM: the B x d_dict latents are never written
+            B, d_model, d_dict, k_row = 4096, 512, 12288, 32
+            m = wl.sae_model(B=B, d_model=d_model, d_dict=d_dict, seed=6)
+            bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+            self.sx, self.sw, self.sb = bf(m["x"]), bf(m["w_enc"]), torch.from_numpy(m["b_enc"]).cuda()
+            self.host = None
+            self.x = self.sx
+            K = B * k_row
+            self.p = pk.plan(B * d_dict, K, 1e-6, 1.0, **rule)
+            self.kernel = "k_sae_filter (bf16 MFMA GEMM + filter epilogue)"
+            self.desc = (f"BatchTopK SAE encoder: bf16 x [{B}, {d_model}] (N(0,1)) times W_enc [{d_dict}, {d_model}] "
+                         f"(N(0,1/d_model)), fp32 bias -0.5 (+1.5 on every 100th latent), ReLU, top K={B}*{k_row}="
+                         f"{K} of the flattened latents, eps=1e-6, sample seed 0 (seed 6 model)")
+            self.ws = pk.sae_workspace(self.p, B, d_dict)
+            self.out = (torch.empty(K, dtype=torch.float32, device="cuda"),
+                        torch.empty(K, dtype=torch.int64, device="cuda"))
+            self.info = torch.empty(pk.INFO_BYTES, dtype=torch.uint8, device="cuda")
+            self.step = lambda: pk.sae_encode_topk(self.sx, self.sw, self.sb, k_row, p=self.p, ws=self.ws,
+                                                   out=self.out, info=self.info, seed=0)
+            self.dense = torch.empty((B, d_dict), dtype=torch.float32, device="cuda")
+            self.p_flat = pk.plan(B * d_dict, K)
+            self.ws_flat = pk.workspace(self.p_flat, pk.F32)
+            self.out_flat = (torch.empty(K, dtype=torch.float32, device="cuda"),
+                             torch.empty(K, dtype=torch.int64, device="cuda"))
+
+            def unfused():
+                pk.sae_encode_dense(self.sx, self.sw, self.sb, out=self.dense)
+                return pk.batchtopk(self.dense, k_row, p=self.p_flat, ws=self.ws_flat, out=self.out_flat, seed=0)
+            self.unfused = unfused
+
+            def torch_ref():
+                z = torch.relu(torch.matmul(self.sx, self.sw.t()).float() + self.sb)
+                return torch.topk(z.view(-1), K, sorted=True)
+            self.torch_ref = torch_ref
+            self.N, self.k, self.es = B * d_dict, K, 4
+            self.flops = 2 * B * d_model * d_dict
         else:
             raise SystemExit(f"unknown workload {name}; choose from {', '.join(WORKLOADS)}")
         self.in_bytes = self.N * self.es
@@ -283,6 +323,16 @@ def main():
         kern_bytes = w.in_bytes + count * 8  # one read of the input, (key, index) per survivor
     value = w.in_bytes / (ms_per_step * 1e-3) / 1e9
     achieved = kern_bytes / (kern_ms * 1e-3) / 1e9
+    if w.flops:
+        roofline = {"bound": "mfma", "achieved": round(w.flops / (kern_ms * 1e-3) / 1e12, 1),
+                    "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(w.flops / (kern_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                    "traffic": None, "kernel": w.kernel, "algorithmic_flops_per_launch": w.flops}
+    else:
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                    "traffic": counters_traffic(w.key()), "kernel": w.kernel,
+                    "algorithmic_bytes_per_launch": kern_bytes}
 
     line = {
         "metric": "effective GB/s and elements/s at N=2^28 fp32, k=1024; % of HBM peak",
@@ -306,11 +356,28 @@ def main():
         "kernel_pct_hbm_peak": round(100 * w.in_bytes / (kern_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
         "count": count,
         "status": status,
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": counters_traffic(w.key()), "kernel": w.kernel,
-                     "algorithmic_bytes_per_launch": kern_bytes},
+        "roofline": roofline,
     }
+    if w.flops:
+        # the latent matrix a dense pipeline would write and then read
+        line["metric"] = "BatchTopK SAE encoder + selection: effective GB/s of fp32 latents; MFMA roofline"
+        line["dtype"] = "bf16"
+        for key in ("pct_hbm_peak", "kernel_pct_hbm_peak"):
+            line.pop(key)
+        line["step_tflops"] = round(w.flops / (ms_per_step * 1e-3) / 1e12, 1)
+        for _ in range(2):
+            w.unfused()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(5):
+            w.unfused()
+        stop.record()
+        torch.cuda.synchronize()
+        u_ms = start.elapsed_time(stop) / 5
+        line["unfused"] = {"what": "profk_sae_encode_dense (the same GEMM, latents written) + profk_batchtopk",
+                           "ms": round(u_ms, 4), "values_equal": bool(torch.equal(w.out_flat[0], w.out[0])),
+                           "indices_equal": bool(torch.equal(w.out_flat[1], w.out[1])),
+                           "speedup_of_fused": round(u_ms / ms_per_step, 3)}
 
     if args.cold:
         flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
@@ -339,9 +406,12 @@ def main():
         line["torch_topk"] = {"ms": round(t_ms, 4), "GB/s": round(w.in_bytes / (t_ms * 1e-3) / 1e9, 1),
                               "values_equal": bool(torch.equal(tv, w.out[0])),
                               "speedup_vs_torch": round(t_ms / ms_per_step, 3)}
+        if w.flops:
+            line["torch_topk"]["what"] = ("torch.matmul (bf16 output) + bias + relu + torch.topk; its latents "
+                                          "are rounded to bf16, so values differ")
         del tv, ti
 
-    if not args.no_copy_probe:
+    if not args.no_copy_probe and not w.flops:
         # A plain device-to-device copy of the same input: the practical
         # streaming ceiling on this GPU, and the reference kernel that scales
         # the FETCH_SIZE / WRITE_SIZE counters into bytes.
@@ -360,7 +430,7 @@ def main():
                               "GB/s": round(2 * w.in_bytes / (c_ms * 1e-3) / 1e9, 1)}
         del dst
 
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not w.flops:
         line["cpu_baseline"] = cpu_baseline(w)
 
     print(json.dumps(line), flush=True)

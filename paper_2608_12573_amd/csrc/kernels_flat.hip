@@ -42,7 +42,8 @@ struct SampleArgs {
 
 template <int DT>
 __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
-  __shared__ SampleUnionShared sh;
+  static_assert(kSampPerBlock == 4 * kSampBS, "four draws per thread");
+  __shared__ SampleUnionShared<kSampBS> sh;
   const uint32_t b = blockIdx.x, tid = threadIdx.x;
   if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist);
   const uint32_t j0 = b * kSampPerBlock;
@@ -62,7 +63,8 @@ __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
       }
     }
   }
-  sample_block_top<Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
+  sample_block_top<kSampBS, Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap,
+                                                sh);
 }
 
 // ------------------------------------------------------------ stage 2 -----

@@ -116,75 +116,85 @@ __device__ __forceinline__ uint32_t sae_col(uint32_t lane, uint32_t w, int j) {
 }
 
 // ------------------------------------------------------------ stage 1 -----
+// k_sae_sample: every draw's latent key, into skeys[S].  k_sae_union: each
+// workgroup of 1024 threads takes 4096 of them and keeps its top-t (the
+// union stays small enough for one workgroup to select tau from in LDS even
+// when t is in the hundreds).
+constexpr int kSaeUnionBS = 1024;
+constexpr uint32_t kSaeUnionPer = 4 * kSaeUnionBS;
+
 struct SaeSampleArgs {
   SaeGemm g;
   uint64_t seed;
-  uint32_t S, t, tcap;
-  uint32_t* union_keys;
+  uint32_t S;
+  uint32_t* skeys;
   CallState* st;
   uint32_t* seg_cnt;
   uint32_t* fhist;
-  uint32_t* sample_keys;  // optional: every draw's key (inspection)
 };
 
 // Draw j is word j%4 of Philox block j/4 (row 0) over the N = B*d_dict
-// flattened latents.  A wave takes 32 draws at a time: lane L and L+32 feed
-// draw L%32's input row and weight row to the MFMA, and the draw's latent is
-// the diagonal element (L%32, L%32) of the 32x32 result: the same sums, in
-// the same order, as the GEMM computes for that element.
+// flattened latents.  Each wave takes 32 draws: lanes L and L+32 feed draw
+// L%32's input row and weight row to the MFMA, and the draw's latent is the
+// diagonal element (L%32, L%32) of the 32x32 result -- the same sums, in the
+// same order, as the GEMM computes for that element.
 __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
-  __shared__ SampleUnionShared sh;
-  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-  if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist);
-  const uint32_t j0 = b * kSampPerBlock;
-  const uint32_t nb = min(static_cast<uint32_t>(kSampPerBlock), a.S - j0);
-  const uint64_t N = static_cast<uint64_t>(a.g.B) * a.g.d_dict;
-  constexpr uint32_t kPerWave = kSampPerBlock / (kSampBS / kWave);
-  for (uint32_t grp = 0; grp < kPerWave / 32; ++grp) {
-    const uint32_t jl = w * kPerWave + grp * 32 + (lane & 31);
-    const bool in = jl < nb;
-    uint32_t r = 0, c = 0;
-    if (in) {
-      const uint64_t jg = static_cast<uint64_t>(j0) + jl;
-      const U64x4 p = philox4x64_10(jg >> 2, 0, 0, 0, a.seed, 0);
-      const uint64_t flat = index_of_word(p.w[jg & 3], N);
-      r = static_cast<uint32_t>(flat / a.g.d_dict);
-      c = static_cast<uint32_t>(flat % a.g.d_dict);
-    }
-    const uint16_t* xr = a.g.x + static_cast<size_t>(r) * a.g.d_model + 8 * (lane >> 5);
-    const uint16_t* wr = a.g.w + static_cast<size_t>(c) * a.g.d_model + 8 * (lane >> 5);
-    f32x16 acc{};
-    for (uint32_t k0 = 0; k0 < a.g.d_model; k0 += 16) {
-      bf16x8 fa = bf16x8{}, fb = bf16x8{};
-      if (in) {
-        fa = *reinterpret_cast<const bf16x8*>(xr + k0);
-        fb = *reinterpret_cast<const bf16x8*>(wr + k0);
-      }
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc, 0, 0, 0);
-    }
-    // element (i, i), i = lane % 32, is held by lane i + 32*((i>>2)&1) as
-    // accumulator 4*(i>>3) + (i&3)
-    const uint32_t i = lane & 31, v = 4 * (i >> 3) + (i & 3);
-    float d = acc[0];
-#pragma unroll
-    for (int q = 1; q < 16; ++q) d = v == static_cast<uint32_t>(q) ? acc[q] : d;
-    if (in && (lane >> 5) == ((i >> 2) & 1)) {
-      const uint32_t key = key_f32(__float_as_uint(sae_relu(d + a.g.bias[c])));
-      sh.keys[jl] = key;
-      if (a.sample_keys) a.sample_keys[j0 + jl] = key;
-    }
+  const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  if (blockIdx.x == 0) reset_state(a.st, a.seg_cnt, a.fhist);
+  const uint32_t j = (blockIdx.x * (kSampBS / kWave) + w) * 32 + (lane & 31);
+  const bool in = j < a.S;
+  uint32_t r = 0, c = 0;
+  if (in) {
+    const U64x4 p = philox4x64_10(j >> 2, 0, 0, 0, a.seed, 0);
+    const uint64_t flat = index_of_word(p.w[j & 3], static_cast<uint64_t>(a.g.B) * a.g.d_dict);
+    r = static_cast<uint32_t>(flat / a.g.d_dict);
+    c = static_cast<uint32_t>(flat % a.g.d_dict);
   }
-  __syncthreads();
+  const uint16_t* xr = a.g.x + static_cast<size_t>(r) * a.g.d_model + 8 * (lane >> 5);
+  const uint16_t* wr = a.g.w + static_cast<size_t>(c) * a.g.d_model + 8 * (lane >> 5);
+  f32x16 acc{};
+  constexpr uint32_t kBatch = 8;  // k-steps whose loads are issued together
+  for (uint32_t k0 = 0; k0 < a.g.d_model; k0 += 16 * kBatch) {
+    bf16x8 fa[kBatch], fb[kBatch];
+#pragma unroll
+    for (uint32_t s = 0; s < kBatch; ++s) {
+      const bool ok = in && k0 + 16 * s < a.g.d_model;
+      fa[s] = ok ? *reinterpret_cast<const bf16x8*>(xr + k0 + 16 * s) : bf16x8{};
+      fb[s] = ok ? *reinterpret_cast<const bf16x8*>(wr + k0 + 16 * s) : bf16x8{};
+    }
+#pragma unroll
+    for (uint32_t s = 0; s < kBatch; ++s)
+      if (k0 + 16 * s < a.g.d_model) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s], fb[s], acc, 0, 0, 0);
+  }
+  // element (i, i), i = lane % 32, is held by lane i + 32*((i>>2)&1) as
+  // accumulator 4*(i>>3) + (i&3)
+  const uint32_t i = lane & 31, v = 4 * (i >> 3) + (i & 3);
+  float d = acc[0];
+#pragma unroll
+  for (int q = 1; q < 16; ++q) d = v == static_cast<uint32_t>(q) ? acc[q] : d;
+  if (in && (lane >> 5) == ((i >> 2) & 1)) a.skeys[j] = key_f32(__float_as_uint(sae_relu(d + a.g.bias[c])));
+}
+
+struct SaeUnionArgs {
+  const uint32_t* skeys;
+  uint32_t S, t, tcap;
+  uint32_t* union_keys;
+};
+
+__global__ __launch_bounds__(kSaeUnionBS) void k_sae_union(SaeUnionArgs a) {
+  __shared__ SampleUnionShared<kSaeUnionBS> sh;
+  const uint32_t b = blockIdx.x, tid = threadIdx.x;
+  const uint32_t j0 = b * kSaeUnionPer;
+  const uint32_t nb = min(kSaeUnionPer, a.S - j0);
   uint32_t kv[4];
   uint32_t valid = 0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const uint32_t j = 4 * tid + q;
-    kv[q] = j < nb ? sh.keys[j] : 0u;
+    kv[q] = j < nb ? a.skeys[j0 + j] : 0u;
     if (j < nb) valid |= 1u << q;
   }
-  __syncthreads();
-  sample_block_top<32>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
+  sample_block_top<kSaeUnionBS, 32>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
 }
 
 // ------------------------------------------------------------ stage 3 -----
@@ -223,12 +233,14 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
     // Epilogue, one 32x32 block of each wave at a time, staged in the wave's
     // own 4 KB of the (now idle) tile buffers: relu(acc + bias), or a key-0
     // marker outside the matrix; then lane L tests elements 16L..16L+15.
+    // (A wave's LDS operations execute in order, so its own stage needs no
+    // barrier between blocks; the one below frees the tile buffers.)
     float* const stage = reinterpret_cast<float*>(&tl) + w * 1024;
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        __syncthreads();  // the tile buffers (first block) or this wave's stage (later blocks) are free
         const uint32_t c = n0 + sae_col(lane, w, j);
         const float bias = c < a.g.d_dict ? a.g.bias[c] : 0.0f;
 #pragma unroll
@@ -237,7 +249,6 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
           const bool ok = c < a.g.d_dict && m0 + sae_row(lane, w, i, v) < a.g.B;
           stage[rl * 32 + (lane & 31)] = ok ? sae_relu(acc[i][j][v] + bias) : __uint_as_float(0xFFFFFFFFu);
         }
-        __syncthreads();
         const uint32_t r0 = m0 + (w >> 1) * 64 + i * 32, c0 = n0 + (w & 1) * 64 + j * 32;
         uint32_t cnt = 0;
         for (uint32_t q = 0; q < 16; ++q) cnt += key_f32(__float_as_uint(stage[lane * 16 + q])) >= tau ? 1u : 0u;
@@ -456,7 +467,13 @@ SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int 
   const uint32_t tiles = cdiv_s(B, kSaeBM) * cdiv_s(d_dict, kSaeBN);
   S.G = tiles < kSaeMaxBlocks ? tiles : kSaeMaxBlocks;
   if (S.G > S.flat.G_f) S.G = S.flat.G_f;  // blk_max holds G_f entries
-  S.off_dense = (S.flat.bytes + 255) & ~static_cast<size_t>(255);
+  const uint32_t Sn = static_cast<uint32_t>(plan.S), t = static_cast<uint32_t>(plan.t);
+  S.G_u = cdiv_s(Sn, kSaeUnionPer);
+  S.tcap_u = t < kSaeUnionPer ? t : kSaeUnionPer;
+  const uint32_t last_nb = Sn - (S.G_u - 1) * kSaeUnionPer;
+  S.union_n_u = (S.G_u - 1) * S.tcap_u + (t < last_nb ? t : last_nb);  // fits the vector path's union area
+  S.off_skeys = (S.flat.bytes + 255) & ~static_cast<size_t>(255);
+  S.off_dense = (S.off_skeys + static_cast<size_t>(Sn) * 4 + 255) & ~static_cast<size_t>(255);
   S.bytes = S.off_dense + static_cast<size_t>(B) * d_dict * 4;
   return S;
 }
@@ -506,12 +523,14 @@ hipError_t launch_sae_topk(const SaeCall& c) {
   uint32_t* fhist = reinterpret_cast<uint32_t*>(ws + L.off_fhist);
   uint32_t* uk = reinterpret_cast<uint32_t*>(ws + L.off_union);
   const SaeGemm g = gemm_of(c);
-  SaeSampleArgs sa{g, c.seed, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t), L.tcap, uk, st, seg_cnt,
-                   fhist, c.sample_keys};
-  hipLaunchKernelGGL(k_sae_sample, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_sae_sample(c);
   if (e != hipSuccess) return e;
-  if ((e = launch_select_tau(uk, L.union_n, static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess) return e;
+  SaeUnionArgs ua{reinterpret_cast<const uint32_t*>(ws + c.L.off_skeys), static_cast<uint32_t>(p.S),
+                  static_cast<uint32_t>(p.t), c.L.tcap_u, uk};
+  hipLaunchKernelGGL(k_sae_union, dim3(c.L.G_u), dim3(kSaeUnionBS), 0, c.stream, ua);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_select_tau(uk, c.L.union_n_u, static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess)
+    return e;
   const uint32_t tn = cdiv_s(c.d_dict, kSaeBN), tiles = cdiv_s(c.B, kSaeBM) * tn;
   SaeFilterArgs fa{g, tn, tiles, st, L.seg_cap, seg_cnt,
                    reinterpret_cast<uint32_t*>(ws + L.off_seg_key), reinterpret_cast<uint32_t*>(ws + L.off_seg_idx),
@@ -529,11 +548,11 @@ hipError_t launch_sae_topk(const SaeCall& c) {
 hipError_t launch_sae_sample(const SaeCall& c) {
   (void)hipGetLastError();
   const FlatLayout& L = c.L.flat;
-  SaeSampleArgs sa{gemm_of(c), c.seed, static_cast<uint32_t>(c.plan->S), static_cast<uint32_t>(c.plan->t), L.tcap,
-                   reinterpret_cast<uint32_t*>(c.ws + L.off_union), reinterpret_cast<CallState*>(c.ws + L.off_state),
-                   reinterpret_cast<uint32_t*>(c.ws + L.off_segcnt), reinterpret_cast<uint32_t*>(c.ws + L.off_fhist),
-                   c.sample_keys};
-  hipLaunchKernelGGL(k_sae_sample, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
+  uint32_t* skeys = c.sample_keys ? c.sample_keys : reinterpret_cast<uint32_t*>(c.ws + c.L.off_skeys);
+  const uint32_t S = static_cast<uint32_t>(c.plan->S);
+  SaeSampleArgs sa{gemm_of(c), c.seed, S, skeys, reinterpret_cast<CallState*>(c.ws + L.off_state),
+                   reinterpret_cast<uint32_t*>(c.ws + L.off_segcnt), reinterpret_cast<uint32_t*>(c.ws + L.off_fhist)};
+  hipLaunchKernelGGL(k_sae_sample, dim3(cdiv_s(S, 32 * (kSampBS / kWave))), dim3(kSampBS), 0, c.stream, sa);
   return hipGetLastError();
 }
 

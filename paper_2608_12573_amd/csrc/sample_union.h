@@ -1,8 +1,8 @@
 // Stage 1 of Sec. 3, the per-workgroup half of the threshold: a sample
-// workgroup of kSampBS threads holds kSampPerBlock draws, 4 per thread
-// (draw 4*tid + q in kv[q]), and keeps its own top-t of them.  The t-th
-// largest key of the whole sample (with multiplicity) is among the union of
-// the workgroups' lists, so stage 2 selects from that union only.
+// workgroup of BS threads holds up to 4*BS draws, 4 per thread (draw
+// 4*tid + q in kv[q]), and keeps its own top-t of them.  The t-th largest
+// key of the whole sample (with multiplicity) is among the union of the
+// workgroups' lists, so stage 2 selects from that union only.
 #pragma once
 
 #include "device_common.h"
@@ -25,20 +25,22 @@ __device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt, ui
   }
 }
 
+template <int BS>
 struct SampleUnionShared {
-  uint32_t keys[kSampPerBlock];
-  uint32_t lists[kSampBS / kWave][kWaveTopMax];
-  uint32_t list_n[kSampBS / kWave];
+  uint32_t keys[4 * BS];
+  uint32_t lists[BS / kWave][kWaveTopMax];
+  uint32_t list_n[BS / kWave];
   SelectShared sel;
   uint32_t emitted;
 };
 
 // Writes the workgroup's top-min(t, nb) draws to dst (nb: draws it holds,
 // valid bit q of `valid` for kv[q]).  Every thread of the workgroup calls it.
-template <int KEYBITS>
+template <int BS, int KEYBITS>
 __device__ __forceinline__ void sample_block_top(uint32_t (&kv)[4], uint32_t valid, uint32_t nb, uint32_t t,
-                                                 uint32_t* dst, SampleUnionShared& sh) {
-  constexpr int NW = kSampBS / kWave;
+                                                 uint32_t* dst, SampleUnionShared<BS>& sh) {
+  constexpr int NW = BS / kWave;
+  static_assert(NW * kWaveTopMax % kWave == 0, "union of the wave lists");
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const uint32_t tl = min(t, nb);
   if (t <= kWaveTopMax) {
@@ -70,18 +72,18 @@ __device__ __forceinline__ void sample_block_top(uint32_t (&kv)[4], uint32_t val
     if ((valid >> q) & 1u) sh.keys[4 * tid + q] = kv[q];
   __syncthreads();
   if (tl == nb) {
-    for (uint32_t j = tid; j < nb; j += kSampBS) dst[j] = sh.keys[j];
+    for (uint32_t j = tid; j < nb; j += BS) dst[j] = sh.keys[j];
     return;
   }
   auto visit = [&](auto f) {
-    for (uint32_t j = tid; j < nb; j += kSampBS) f(sh.keys[j]);
+    for (uint32_t j = tid; j < nb; j += BS) f(sh.keys[j]);
   };
-  const SelectResult r = block_select_kth<kSampBS>(visit, tl, KEYBITS, 0u, sh.sel);
+  const SelectResult r = block_select_kth<BS>(visit, tl, KEYBITS, 0u, sh.sel);
   if (tid == 0) sh.emitted = 0;
   __syncthreads();
-  for (uint32_t j = tid; j < nb; j += kSampBS)
+  for (uint32_t j = tid; j < nb; j += BS)
     if (sh.keys[j] > r.kth) dst[atomicAdd(&sh.emitted, 1u)] = sh.keys[j];
-  for (uint32_t j = r.above + tid; j < tl; j += kSampBS) dst[j] = r.kth;
+  for (uint32_t j = r.above + tid; j < tl; j += BS) dst[j] = r.kth;
 }
 
 }  // namespace profk
