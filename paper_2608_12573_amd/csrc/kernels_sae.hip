@@ -35,10 +35,18 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 
-constexpr int kSaeBS = 256;
-constexpr uint32_t kSaeBM = 128, kSaeBN = 128, kSaeBK = 64;
+// GEMM tiling: a workgroup of 8 waves computes a 256 x 128 tile of z (waves
+// in a 4 x 2 grid, 64 x 64 each as 2 x 2 32x32 MFMA accumulators); d_model
+// is consumed in chunks of 64, double-buffered in LDS (rows padded to 144 B)
+// with one barrier per chunk: the next chunk's global loads are in flight,
+// and then written to the other buffer, while this chunk's MFMAs run.
+constexpr int kSaeBS = 512;
+constexpr uint32_t kSaeBM = 256, kSaeBN = 128, kSaeBK = 64;
 constexpr uint32_t kSaeLd = kSaeBK + 8;  // LDS row stride in bf16 elements
 constexpr uint32_t kSaeMaxBlocks = 1024;
+constexpr int kSaeApieces = kSaeBM * kSaeBK / 8 / kSaeBS;  // 16-byte pieces per thread and chunk
+constexpr int kSaeBpieces = kSaeBN * kSaeBK / 8 / kSaeBS;
+static_assert(kSaeBS / kWave == (kSaeBM / 64) * (kSaeBN / 64), "one wave per 64 x 64 block");
 
 struct SaeGemm {
   const uint16_t* x;  // [B, d_model] bf16 bits, 16-byte aligned rows
@@ -48,13 +56,14 @@ struct SaeGemm {
 };
 
 struct alignas(16) SaeTileLds {
-  uint16_t a[kSaeBM * kSaeLd];
-  uint16_t b[kSaeBN * kSaeLd];
+  uint16_t a[2][kSaeBM * kSaeLd];
+  uint16_t b[2][kSaeBN * kSaeLd];
 };
 
 __device__ __forceinline__ float sae_relu(float pre) { return pre > 0.0f ? pre : 0.0f; }
 
-// acc[bm][bn] = this wave's 64x64 part of the product for the tile at (m0, n0).
+// acc[i][j] = this wave's 64x64 part of the product for the tile at (m0, n0).
+// Ends with a barrier, after which the tile buffers are free.
 __device__ __forceinline__ void sae_tile_mma(const SaeGemm& g, uint32_t m0, uint32_t n0, SaeTileLds& sh,
                                              f32x16 (&acc)[2][2]) {
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
@@ -64,39 +73,47 @@ __device__ __forceinline__ void sae_tile_mma(const SaeGemm& g, uint32_t m0, uint
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
   const uint32_t nchunk = g.d_model / kSaeBK;
-  // a 128 x 64 chunk is 1024 16-byte pieces: 4 per thread, 8 per row
-  u32x4v ra[4], rb[4];
-  auto gload = [&](uint32_t kc) {
+  // piece id = q * kSaeBS + tid is row id / 8, 16-byte segment id % 8 of the
+  // chunk.  Two register sets hold the chunks in flight: chunk c + 2 is
+  // loaded while chunk c is computed and stored to LDS after chunk c + 1 is.
+  u32x4v ra[2][kSaeApieces], rb[2][kSaeBpieces];
+  auto gload = [&](uint32_t kc, u32x4v (&xa)[kSaeApieces], u32x4v (&xb)[kSaeBpieces]) {
+    const size_t col = static_cast<size_t>(kc) * kSaeBK;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t id = q * kSaeBS + tid, row = id >> 3, seg = id & 7;
-      const uint32_t gm = m0 + row, gn = n0 + row;
-      const size_t col = static_cast<size_t>(kc) * kSaeBK + seg * 8;
-      ra[q] = gm < g.B ? *reinterpret_cast<const u32x4v*>(g.x + static_cast<size_t>(gm) * g.d_model + col)
+    for (int q = 0; q < kSaeApieces; ++q) {
+      const uint32_t id = q * kSaeBS + tid, gm = m0 + (id >> 3);
+      xa[q] = gm < g.B ? *reinterpret_cast<const u32x4v*>(g.x + static_cast<size_t>(gm) * g.d_model + col + (id & 7) * 8)
                        : u32x4v{0u, 0u, 0u, 0u};
-      rb[q] = gn < g.d_dict ? *reinterpret_cast<const u32x4v*>(g.w + static_cast<size_t>(gn) * g.d_model + col)
-                            : u32x4v{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int q = 0; q < kSaeBpieces; ++q) {
+      const uint32_t id = q * kSaeBS + tid, gn = n0 + (id >> 3);
+      xb[q] = gn < g.d_dict
+                  ? *reinterpret_cast<const u32x4v*>(g.w + static_cast<size_t>(gn) * g.d_model + col + (id & 7) * 8)
+                  : u32x4v{0u, 0u, 0u, 0u};
     }
   };
-  gload(0);
-  for (uint32_t kc = 0; kc < nchunk; ++kc) {
-    __syncthreads();  // every wave is done with the previous chunk
+  auto lstore = [&](uint32_t buf, const u32x4v (&xa)[kSaeApieces], const u32x4v (&xb)[kSaeBpieces]) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t id = q * kSaeBS + tid, row = id >> 3, seg = id & 7;
-      *reinterpret_cast<u32x4v*>(&sh.a[row * kSaeLd + seg * 8]) = ra[q];
-      *reinterpret_cast<u32x4v*>(&sh.b[row * kSaeLd + seg * 8]) = rb[q];
+    for (int q = 0; q < kSaeApieces; ++q) {
+      const uint32_t id = q * kSaeBS + tid;
+      *reinterpret_cast<u32x4v*>(&sh.a[buf][(id >> 3) * kSaeLd + (id & 7) * 8]) = xa[q];
     }
-    __syncthreads();
-    if (kc + 1 < nchunk) gload(kc + 1);
+#pragma unroll
+    for (int q = 0; q < kSaeBpieces; ++q) {
+      const uint32_t id = q * kSaeBS + tid;
+      *reinterpret_cast<u32x4v*>(&sh.b[buf][(id >> 3) * kSaeLd + (id & 7) * 8]) = xb[q];
+    }
+  };
+  auto compute = [&](uint32_t buf) {
 #pragma unroll
     for (uint32_t ks = 0; ks < kSaeBK / 16; ++ks) {
       const uint32_t kofs = ks * 16 + 8 * (lane >> 5);
       bf16x8 fa[2], fb[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        fa[i] = *reinterpret_cast<const bf16x8*>(&sh.a[(wm * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
-        fb[i] = *reinterpret_cast<const bf16x8*>(&sh.b[(wn * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
+        fa[i] = *reinterpret_cast<const bf16x8*>(&sh.a[buf][(wm * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
+        fb[i] = *reinterpret_cast<const bf16x8*>(&sh.b[buf][(wn * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -104,8 +121,53 @@ __device__ __forceinline__ void sae_tile_mma(const SaeGemm& g, uint32_t m0, uint
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
+  };
+  __syncthreads();  // the previous tile's epilogue is done with the buffers
+  gload(0, ra[0], rb[0]);
+  lstore(0, ra[0], rb[0]);
+  if (nchunk > 1) gload(1, ra[1], rb[1]);
+  __syncthreads();
+  // chunk kc is in LDS buffer kc % 2; register set s holds chunk kc + 1 on
+  // entry to an even (s = 1) or odd (s = 0) step
+  for (uint32_t kc = 0; kc < nchunk; kc += 2) {
+    if (kc + 2 < nchunk) gload(kc + 2, ra[0], rb[0]);
+    compute(0);
+    if (kc + 1 < nchunk) lstore(1, ra[1], rb[1]);  // buffer 1 was last read before the previous barrier
+    __syncthreads();
+    if (kc + 1 >= nchunk) break;
+    if (kc + 3 < nchunk) gload(kc + 3, ra[1], rb[1]);
+    compute(1);
+    if (kc + 2 < nchunk) lstore(0, ra[0], rb[0]);  // buffer 0 was read before the barrier above
+    __syncthreads();
   }
 }
+
+// XCD-aware tile order.  Workgroups are dispatched to the 8 XCDs round-robin
+// (workgroup b runs on XCD b % 8), each XCD with its own L2.  The grid is a
+// multiple of V = min(8, grid) workgroups; group x = b % V owns the column
+// tiles [nlo, nlo + nx) -- a slice of W_enc that stays in its XCD's L2 --
+// and walks all row tiles; its workgroups (b / V = 0, 1, ...) take the
+// group's tiles in row-major order with stride grid / V, so consecutive tiles
+// of an XCD share their row block of x.  Every column tile has one owner.
+constexpr uint32_t kXcds = 8;
+
+struct XcdTiles {
+  uint32_t nlo, nx, count;  // the group's column tiles [nlo, nlo + nx), tiles in all
+  uint32_t first, stride;   // this workgroup's first tile of the group, and the step
+  __device__ __forceinline__ XcdTiles(uint32_t tiles_m, uint32_t tiles_n) {
+    const uint32_t V = gridDim.x < kXcds ? gridDim.x : kXcds;
+    const uint32_t x = blockIdx.x % V;
+    nlo = tiles_n * x / V;
+    nx = tiles_n * (x + 1) / V - nlo;
+    count = tiles_m * nx;
+    first = blockIdx.x / V;
+    stride = gridDim.x / V;
+  }
+  __device__ __forceinline__ void tile(uint32_t t, uint32_t& m0, uint32_t& n0) const {
+    m0 = (t / nx) * kSaeBM;
+    n0 = (nlo + t % nx) * kSaeBN;
+  }
+};
 
 // Tile-local row and column of accumulator element v of block (i, j).
 __device__ __forceinline__ uint32_t sae_row(uint32_t lane, uint32_t w, int i, int v) {
@@ -137,11 +199,17 @@ struct SaeSampleArgs {
 // flattened latents.  Each wave takes 32 draws: lanes L and L+32 feed draw
 // L%32's input row and weight row to the MFMA, and the draw's latent is the
 // diagonal element (L%32, L%32) of the 32x32 result -- the same sums, in the
-// same order, as the GEMM computes for that element.
+// same order, as the GEMM computes for that element.  The 32 rows are staged
+// through the wave's own LDS one 64-wide chunk at a time, 8 lanes per
+// 128-byte row piece, so the loads are coalesced rather than one 16-byte
+// line per lane.
 __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
+  constexpr int NW = kSampBS / kWave;
+  __shared__ __align__(16) uint16_t s_x[NW][32 * kSaeLd];
+  __shared__ __align__(16) uint16_t s_w[NW][32 * kSaeLd];
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   if (blockIdx.x == 0) reset_state(a.st, a.seg_cnt, a.fhist);
-  const uint32_t j = (blockIdx.x * (kSampBS / kWave) + w) * 32 + (lane & 31);
+  const uint32_t j = (blockIdx.x * NW + w) * 32 + (lane & 31);
   const bool in = j < a.S;
   uint32_t r = 0, c = 0;
   if (in) {
@@ -150,21 +218,42 @@ __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
     r = static_cast<uint32_t>(flat / a.g.d_dict);
     c = static_cast<uint32_t>(flat % a.g.d_dict);
   }
-  const uint16_t* xr = a.g.x + static_cast<size_t>(r) * a.g.d_model + 8 * (lane >> 5);
-  const uint16_t* wr = a.g.w + static_cast<size_t>(c) * a.g.d_model + 8 * (lane >> 5);
-  f32x16 acc{};
-  constexpr uint32_t kBatch = 8;  // k-steps whose loads are issued together
-  for (uint32_t k0 = 0; k0 < a.g.d_model; k0 += 16 * kBatch) {
-    bf16x8 fa[kBatch], fb[kBatch];
+  // piece s*64 + lane of a chunk: row (s*64 + lane) / 8, 16-byte segment lane % 8
+  uint32_t pr[4], pc[4];
+  bool pin[4];
 #pragma unroll
-    for (uint32_t s = 0; s < kBatch; ++s) {
-      const bool ok = in && k0 + 16 * s < a.g.d_model;
-      fa[s] = ok ? *reinterpret_cast<const bf16x8*>(xr + k0 + 16 * s) : bf16x8{};
-      fb[s] = ok ? *reinterpret_cast<const bf16x8*>(wr + k0 + 16 * s) : bf16x8{};
+  for (int s = 0; s < 4; ++s) {
+    const int row = (s * kWave + static_cast<int>(lane)) >> 3;
+    pr[s] = __shfl(r, row, kWave);
+    pc[s] = __shfl(c, row, kWave);
+    pin[s] = __shfl(in ? 1 : 0, row, kWave) != 0;
+  }
+  const uint32_t seg = lane & 7;
+  f32x16 acc{};
+  for (uint32_t k0 = 0; k0 < a.g.d_model; k0 += kSaeBK) {
+    u32x4v vx[4], vw[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      vx[s] = pin[s] ? *reinterpret_cast<const u32x4v*>(a.g.x + static_cast<size_t>(pr[s]) * a.g.d_model + k0 + seg * 8)
+                     : u32x4v{0u, 0u, 0u, 0u};
+      vw[s] = pin[s] ? *reinterpret_cast<const u32x4v*>(a.g.w + static_cast<size_t>(pc[s]) * a.g.d_model + k0 + seg * 8)
+                     : u32x4v{0u, 0u, 0u, 0u};
+    }
+    // (the wave's previous chunk was read by this wave's own earlier LDS
+    // reads, which complete in order before these writes)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const uint32_t row = (s * kWave + lane) >> 3;
+      *reinterpret_cast<u32x4v*>(&s_x[w][row * kSaeLd + seg * 8]) = vx[s];
+      *reinterpret_cast<u32x4v*>(&s_w[w][row * kSaeLd + seg * 8]) = vw[s];
     }
 #pragma unroll
-    for (uint32_t s = 0; s < kBatch; ++s)
-      if (k0 + 16 * s < a.g.d_model) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s], fb[s], acc, 0, 0, 0);
+    for (uint32_t ks = 0; ks < kSaeBK / 16; ++ks) {
+      const uint32_t kofs = ks * 16 + 8 * (lane >> 5);
+      const bf16x8 fa = *reinterpret_cast<const bf16x8*>(&s_x[w][(lane & 31) * kSaeLd + kofs]);
+      const bf16x8 fb = *reinterpret_cast<const bf16x8*>(&s_w[w][(lane & 31) * kSaeLd + kofs]);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc, 0, 0, 0);
+    }
   }
   // element (i, i), i = lane % 32, is held by lane i + 32*((i>>2)&1) as
   // accumulator 4*(i>>3) + (i&3)
@@ -200,7 +289,7 @@ __global__ __launch_bounds__(kSaeUnionBS) void k_sae_union(SaeUnionArgs a) {
 // ------------------------------------------------------------ stage 3 -----
 struct SaeFilterArgs {
   SaeGemm g;
-  uint32_t tiles_n, tiles;
+  uint32_t tiles_m, tiles_n;
   CallState* st;
   uint32_t seg_cap;
   uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
@@ -226,68 +315,82 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
   uint32_t* const seg_key = a.seg_key + static_cast<size_t>(seg) * a.seg_cap;
   uint32_t* const seg_idx = a.seg_idx + static_cast<size_t>(seg) * a.seg_cap;
   uint32_t my_max = 0;
-  for (uint32_t tile = b; tile < a.tiles; tile += gridDim.x) {
-    const uint32_t m0 = (tile / a.tiles_n) * kSaeBM, n0 = (tile % a.tiles_n) * kSaeBN;
+  const XcdTiles xt(a.tiles_m, a.tiles_n);
+  for (uint32_t tl_i = xt.first; tl_i < xt.count; tl_i += xt.stride) {
+    uint32_t m0, n0;
+    xt.tile(tl_i, m0, n0);
     f32x16 acc[2][2];
     sae_tile_mma(a.g, m0, n0, tl, acc);
-    // Epilogue, one 32x32 block of each wave at a time, staged in the wave's
-    // own 4 KB of the (now idle) tile buffers: relu(acc + bias), or a key-0
-    // marker outside the matrix; then lane L tests elements 16L..16L+15.
-    // (A wave's LDS operations execute in order, so its own stage needs no
-    // barrier between blocks; the one below frees the tile buffers.)
-    float* const stage = reinterpret_cast<float*>(&tl) + w * 1024;
-    __syncthreads();
+    // Epilogue, per half (i) of the wave's 64 x 64 block: the survivor bits of
+    // the lane's 32 latents (bit 16j + v for accumulator v of block (i, j))
+    // come from the registers; a wave with survivors stages its 32 latents
+    // per lane in its own 8 KB of the (now idle) tile buffers and each lane
+    // reads back only its survivors.  (sae_tile_mma ended with a barrier; a
+    // wave's LDS operations execute in order.)
+    float* const stage = reinterpret_cast<float*>(&tl) + w * (32 * kWave);
+    static_assert(kSaeBS / kWave * 32 * kWave * 4 <= sizeof(SaeTileLds), "epilogue stage");
+    float bias[2];
+    bool colok[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t c = n0 + sae_col(lane, w, j);
+      colok[j] = c < a.g.d_dict;
+      bias[j] = colok[j] ? a.g.bias[c] : 0.0f;
+    }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const uint32_t c = n0 + sae_col(lane, w, j);
-        const float bias = c < a.g.d_dict ? a.g.bias[c] : 0.0f;
+    for (int i = 0; i < 2; ++i) {
+      float z[32];
+      uint32_t m = 0;
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const uint32_t rl = 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
-          const bool ok = c < a.g.d_dict && m0 + sae_row(lane, w, i, v) < a.g.B;
-          stage[rl * 32 + (lane & 31)] = ok ? sae_relu(acc[i][j][v] + bias) : __uint_as_float(0xFFFFFFFFu);
+          z[16 * j + v] = sae_relu(acc[i][j][v] + bias[j]);
+          const bool ok = colok[j] && m0 + sae_row(lane, w, i, v) < a.g.B &&
+                          key_f32(__float_as_uint(z[16 * j + v])) >= tau;
+          m |= (ok ? 1u : 0u) << (16 * j + v);
         }
-        const uint32_t r0 = m0 + (w >> 1) * 64 + i * 32, c0 = n0 + (w & 1) * 64 + j * 32;
-        uint32_t cnt = 0;
-        for (uint32_t q = 0; q < 16; ++q) cnt += key_f32(__float_as_uint(stage[lane * 16 + q])) >= tau ? 1u : 0u;
-        if (__ballot(cnt != 0) == 0) continue;
-        // one stage reservation per wave
-        const uint32_t incl = wave_incl_sum(cnt);
-        const uint32_t total = __shfl(incl, kWave - 1, kWave);
-        uint32_t base = 0;
-        if (lane == 0) base = atomicAdd(&s_cnt, total);
-        base = __shfl(base, 0, kWave);
-        const uint32_t n_in = base < kStage ? min(total, kStage - base) : 0u;
-        uint32_t gbase = 0;
-        if (total - n_in) {
-          if (lane == 0) gbase = atomicAdd(seg_counter, total - n_in);
-          gbase = __shfl(gbase, 0, kWave);
-        }
-        const uint32_t first_over = base + n_in;
-        uint32_t slot = base + incl - cnt;
-        for (uint32_t q = 0; q < 16 && cnt; ++q) {
-          const uint32_t e = lane * 16 + q;
-          const uint32_t key = key_f32(__float_as_uint(stage[e]));
-          if (key < tau) continue;
-          --cnt;
-          const uint32_t idx = (r0 + e / 32) * a.g.d_dict + c0 + e % 32;
-          my_max = max(my_max, key);
-          atomicAdd(&s_hist[log_bin(key - tau)], 1u);
-          if (slot < kStage) {
-            s_skey[slot] = key;
-            s_sidx[slot] = idx;
-          } else {
-            const uint32_t gp = gbase + (slot - first_over);
-            if (gp < a.seg_cap) {
-              seg_key[gp] = key;
-              seg_idx[gp] = idx;
-            }
-          }
-          ++slot;
-        }
+      const uint32_t cnt = __popc(m);
+      if (__ballot(cnt != 0) == 0) continue;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        *reinterpret_cast<float4*>(&stage[lane * 32 + 4 * q]) =
+            make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+      // one stage reservation per wave
+      const uint32_t incl = wave_incl_sum(cnt);
+      const uint32_t total = __shfl(incl, kWave - 1, kWave);
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(&s_cnt, total);
+      base = __shfl(base, 0, kWave);
+      const uint32_t n_in = base < kStage ? min(total, kStage - base) : 0u;
+      uint32_t gbase = 0;
+      if (total - n_in) {
+        if (lane == 0) gbase = atomicAdd(seg_counter, total - n_in);
+        gbase = __shfl(gbase, 0, kWave);
       }
+      const uint32_t first_over = base + n_in;
+      uint32_t slot = base + incl - cnt;
+      while (m) {
+        const uint32_t bit = __builtin_ctz(m);
+        m &= m - 1;
+        const uint32_t key = key_f32(__float_as_uint(stage[lane * 32 + bit]));
+        const int j = static_cast<int>(bit >> 4), v = static_cast<int>(bit & 15);
+        const uint32_t idx = (m0 + sae_row(lane, w, i, v)) * a.g.d_dict + n0 + sae_col(lane, w, j);
+        my_max = max(my_max, key);
+        atomicAdd(&s_hist[log_bin(key - tau)], 1u);
+        if (slot < kStage) {
+          s_skey[slot] = key;
+          s_sidx[slot] = idx;
+        } else {
+          const uint32_t gp = gbase + (slot - first_over);
+          if (gp < a.seg_cap) {
+            seg_key[gp] = key;
+            seg_idx[gp] = idx;
+          }
+        }
+        ++slot;
+      }
+    }
   }
   const uint32_t wm = wave_max_u32(my_max);
   if (lane == 0) s_wmax[w] = wm;
@@ -319,7 +422,7 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
 // ------------------------------------------------------------- dense ------
 struct SaeDenseArgs {
   SaeGemm g;
-  uint32_t tiles_n;
+  uint32_t tiles_m, tiles_n;
   float* out;               // [B, d_dict]
   const uint32_t* seg_cnt;  // null: always write; else only when the count is outside [k_req, M]
   uint32_t k_req, M;
@@ -334,21 +437,25 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_dense(SaeDenseArgs a) {
     if (total >= a.k_req && total <= a.M) return;  // filtered: the candidates suffice
   }
   const uint32_t lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
-  const uint32_t m0 = (blockIdx.x / a.tiles_n) * kSaeBM, n0 = (blockIdx.x % a.tiles_n) * kSaeBN;
-  f32x16 acc[2][2];
-  sae_tile_mma(a.g, m0, n0, tl, acc);
+  const XcdTiles xt(a.tiles_m, a.tiles_n);
+  for (uint32_t tl_i = xt.first; tl_i < xt.count; tl_i += xt.stride) {
+    uint32_t m0, n0;
+    xt.tile(tl_i, m0, n0);
+    f32x16 acc[2][2];
+    sae_tile_mma(a.g, m0, n0, tl, acc);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const uint32_t c = n0 + sae_col(lane, w, j);
-    if (c >= a.g.d_dict) continue;
-    const float bias = a.g.bias[c];
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t c = n0 + sae_col(lane, w, j);
+      if (c >= a.g.d_dict) continue;
+      const float bias = a.g.bias[c];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const uint32_t r = m0 + sae_row(lane, w, i, v);
-        if (r < a.g.B) a.out[static_cast<size_t>(r) * a.g.d_dict + c] = sae_relu(acc[i][j][v] + bias);
-      }
+        for (int v = 0; v < 16; ++v) {
+          const uint32_t r = m0 + sae_row(lane, w, i, v);
+          if (r < a.g.B) a.out[static_cast<size_t>(r) * a.g.d_dict + c] = sae_relu(acc[i][j][v] + bias);
+        }
+    }
   }
 }
 
@@ -461,12 +568,21 @@ __global__ __launch_bounds__(kDecBS) void k_dec_rows(DecArgs a) {
 // ------------------------------------------------------------- host -------
 static uint32_t cdiv_s(uint64_t a, uint64_t b) { return static_cast<uint32_t>((a + b - 1) / b); }
 
+// Persistent GEMM grid: one workgroup per CU (the LDS of a 256 x 128 tile,
+// double-buffered, allows one), a multiple of the XCD count when there are
+// enough tiles.
+static uint32_t sae_grid(uint32_t tiles) {
+  const uint32_t cus = static_cast<uint32_t>(device_cu_count());
+  uint32_t g = cus < kSaeMaxBlocks ? cus : kSaeMaxBlocks;
+  if (tiles < g) g = tiles;
+  return g >= kXcds ? g / kXcds * kXcds : g;
+}
+
 SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int num_cus) {
   SaeLayout S;
   S.flat = flat_layout(plan, PROFK_F32, num_cus);
-  const uint32_t tiles = cdiv_s(B, kSaeBM) * cdiv_s(d_dict, kSaeBN);
-  S.G = tiles < kSaeMaxBlocks ? tiles : kSaeMaxBlocks;
-  if (S.G > S.flat.G_f) S.G = S.flat.G_f;  // blk_max holds G_f entries
+  S.G = sae_grid(cdiv_s(B, kSaeBM) * cdiv_s(d_dict, kSaeBN));
+  if (S.G > S.flat.G_f) S.G = S.flat.G_f >= kXcds ? S.flat.G_f / kXcds * kXcds : S.flat.G_f;  // blk_max: G_f entries
   const uint32_t Sn = static_cast<uint32_t>(plan.S), t = static_cast<uint32_t>(plan.t);
   S.G_u = cdiv_s(Sn, kSaeUnionPer);
   S.tcap_u = t < kSaeUnionPer ? t : kSaeUnionPer;
@@ -485,9 +601,9 @@ static SaeGemm gemm_of(const SaeCall& c) {
 
 hipError_t launch_sae_dense(const SaeCall& c, float* out) {
   (void)hipGetLastError();
-  const uint32_t tn = cdiv_s(c.d_dict, kSaeBN), tiles = cdiv_s(c.B, kSaeBM) * tn;
-  SaeDenseArgs da{gemm_of(c), tn, out, nullptr, 0, 0};
-  hipLaunchKernelGGL(k_sae_dense, dim3(tiles), dim3(kSaeBS), 0, c.stream, da);
+  const uint32_t tm = cdiv_s(c.B, kSaeBM), tn = cdiv_s(c.d_dict, kSaeBN);
+  SaeDenseArgs da{gemm_of(c), tm, tn, out, nullptr, 0, 0};
+  hipLaunchKernelGGL(k_sae_dense, dim3(sae_grid(tm * tn)), dim3(kSaeBS), 0, c.stream, da);
   return hipGetLastError();
 }
 
@@ -531,16 +647,16 @@ hipError_t launch_sae_topk(const SaeCall& c) {
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_select_tau(uk, c.L.union_n_u, static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess)
     return e;
-  const uint32_t tn = cdiv_s(c.d_dict, kSaeBN), tiles = cdiv_s(c.B, kSaeBM) * tn;
-  SaeFilterArgs fa{g, tn, tiles, st, L.seg_cap, seg_cnt,
+  const uint32_t tm = cdiv_s(c.B, kSaeBM), tn = cdiv_s(c.d_dict, kSaeBN);
+  SaeFilterArgs fa{g, tm, tn, st, L.seg_cap, seg_cnt,
                    reinterpret_cast<uint32_t*>(ws + L.off_seg_key), reinterpret_cast<uint32_t*>(ws + L.off_seg_idx),
                    reinterpret_cast<uint32_t*>(ws + L.off_blk_max), fhist};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
   hipLaunchKernelGGL(k_sae_filter, dim3(c.L.G), dim3(kSaeBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
   // the dense latents only when the candidates do not suffice (exact fallback)
-  SaeDenseArgs da{g, tn, dense, seg_cnt, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M)};
-  hipLaunchKernelGGL(k_sae_dense, dim3(tiles), dim3(kSaeBS), 0, c.stream, da);
+  SaeDenseArgs da{g, tm, tn, dense, seg_cnt, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M)};
+  hipLaunchKernelGGL(k_sae_dense, dim3(sae_grid(tm * tn)), dim3(kSaeBS), 0, c.stream, da);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_refine(fc, c.L.G);
 }
