@@ -286,6 +286,35 @@ __global__ __launch_bounds__(kSaeUnionBS) void k_sae_union(SaeUnionArgs a) {
   sample_block_top<kSaeUnionBS, 32>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
 }
 
+// ------------------------------------------------------- thresholds ------
+// A latent relu(acc + b_enc[j]) survives iff its key is >= tau.  With tau
+// above the key of +0 that is fl(acc + b_enc[j]) >= tau as floats (relu
+// lifts nothing to a positive value), and since fl(acc + b) does not decrease
+// as acc grows, it is acc >= thr[j] for the smallest float thr[j] that passes
+// (NaN when none does): one compare per latent in the filter's epilogue.
+// thr[j] is found by bisection over the floats in key order (-0 and +0 pass
+// alike, so the float compare agrees with the key order).
+__device__ __forceinline__ bool sae_passes(uint32_t akey, float b, float tf) {
+  return __uint_as_float(bits_from_key_f32(akey)) + b >= tf;
+}
+
+__global__ void k_sae_thresholds(const CallState* st, const float* bias, uint32_t d_dict, float* thr) {
+  const uint32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= d_dict) return;
+  const float tf = __uint_as_float(bits_from_key_f32(st->tau_key));
+  const float b = bias[j];
+  uint32_t lo = key_f32(0xFF800000u), hi = key_f32(0x7F800000u);  // -inf, +inf
+  if (!sae_passes(hi, b, tf)) {
+    thr[j] = __uint_as_float(0x7FC00000u);
+    return;
+  }
+  while (lo < hi) {  // the smallest passing key in [lo, hi]
+    const uint32_t mid = lo + (hi - lo) / 2;
+    if (sae_passes(mid, b, tf)) hi = mid; else lo = mid + 1;
+  }
+  thr[j] = __uint_as_float(bits_from_key_f32(lo));
+}
+
 // ------------------------------------------------------------ stage 3 -----
 struct SaeFilterArgs {
   SaeGemm g;
@@ -293,125 +322,156 @@ struct SaeFilterArgs {
   CallState* st;
   uint32_t seg_cap;
   uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
-  uint32_t* fhist;  // refinement histogram, zero on entry
+  uint32_t* fhist;   // refinement histogram, zero on entry
+  const float* thr;  // [d_dict] from k_sae_thresholds
 };
 
-// Persistent: workgroup b takes tiles b, b + G, ...  Survivors (key >= tau)
-// get workgroup-stage slots from a wave prefix sum (slots past the stage go
-// straight to the workgroup's candidate segment); at the end the stage is
-// appended with one atomic, the maximum key goes to blk_max[b] and the
-// non-empty log-bin counts to fhist -- the vector filter's outputs.
+constexpr uint32_t kSaeSlice = kStage / (kSaeBS / kWave);  // survivors a wave stages in LDS
+
+
+
+// Persistent: workgroup b takes its XCD group's tiles (XcdTiles).  Each
+// wave stages survivors (key, index) in its own slice of the workgroup stage
+// with a wave-uniform fill count, so the common path takes no atomics; a
+// slice is appended to the workgroup's candidate segment (one atomic) when it
+// is half full at a tile's start, and at the end.  The log-bin counts and the
+// maximum key are taken from the slice as it is appended.
+//
+// Per latent of a full tile, the fast epilogue costs one compare against the
+// column threshold and a wave-uniform branch; the body runs only for
+// accumulator elements with a survivor in the wave.  A tile whose survivors
+// do not fit the slice, a tile cut by the last row, and every tile when tau
+// is at most key(+0) (all latents survive) go through the general epilogue: the accumulators pass through LDS and each
+// element's survivors are appended to the segment directly.
 __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
   __shared__ SaeTileLds tl;
   __shared__ uint32_t s_skey[kStage], s_sidx[kStage];
   __shared__ uint32_t s_hist[kLogBins];
-  __shared__ uint32_t s_cnt, s_base, s_wmax[kSaeBS / kWave];
+  __shared__ uint32_t s_wmax[kSaeBS / kWave];
   const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const uint32_t seg = b & (kSegs - 1);
   const uint32_t tau = a.st->tau_key;
-  for (uint32_t i = tid; i < kLogBins; i += kSaeBS) s_hist[i] = 0;
-  if (tid == 0) s_cnt = 0;
+  const bool all = tau <= 0x80000000u;  // tau <= key(+0): every latent survives
+  for (uint32_t i = tid; i < kLogBins; i += kSaeBS) s_hist[i] = 0;  // visible after the first tile's barrier
   uint32_t* const seg_counter = a.seg_cnt + seg * kSegStride;
   uint32_t* const seg_key = a.seg_key + static_cast<size_t>(seg) * a.seg_cap;
   uint32_t* const seg_idx = a.seg_idx + static_cast<size_t>(seg) * a.seg_cap;
+  uint32_t* const wkey = s_skey + w * kSaeSlice;
+  uint32_t* const widx = s_sidx + w * kSaeSlice;
+  uint32_t wcnt = 0;  // wave-uniform fill of the wave's slice
   uint32_t my_max = 0;
+  // one survivor's log-bin count and maximum
+  auto note = [&](uint32_t key) {
+    atomicAdd(&s_hist[log_bin(key - tau)], 1u);
+    my_max = max(my_max, key);
+  };
+  // the wave's n staged survivors to the segment (a wave's LDS operations
+  // execute in program order, so the slice reads see its writes)
+  auto flush = [&](uint32_t n) {
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(seg_counter, n);
+    base = __shfl(base, 0, kWave);
+    for (uint32_t q = lane; q < n; q += kWave) {
+      const uint32_t key = wkey[q], gp = base + q;
+      note(key);
+      if (gp < a.seg_cap) {
+        seg_key[gp] = key;
+        seg_idx[gp] = widx[q];
+      }
+    }
+  };
+  float* const stage = reinterpret_cast<float*>(&tl) + w * (32 * kWave);
+  static_assert(kSaeBS / kWave * 32 * kWave * 4 <= sizeof(SaeTileLds), "epilogue stage");
   const XcdTiles xt(a.tiles_m, a.tiles_n);
   for (uint32_t tl_i = xt.first; tl_i < xt.count; tl_i += xt.stride) {
     uint32_t m0, n0;
     xt.tile(tl_i, m0, n0);
-    f32x16 acc[2][2];
-    sae_tile_mma(a.g, m0, n0, tl, acc);
-    // Epilogue, per half (i) of the wave's 64 x 64 block: the survivor bits of
-    // the lane's 32 latents (bit 16j + v for accumulator v of block (i, j))
-    // come from the registers; a wave with survivors stages its 32 latents
-    // per lane in its own 8 KB of the (now idle) tile buffers and each lane
-    // reads back only its survivors.  (sae_tile_mma ended with a barrier; a
-    // wave's LDS operations execute in order.)
-    float* const stage = reinterpret_cast<float*>(&tl) + w * (32 * kWave);
-    static_assert(kSaeBS / kWave * 32 * kWave * 4 <= sizeof(SaeTileLds), "epilogue stage");
-    float bias[2];
-    bool colok[2];
+    // the lane's two columns: threshold, bias (loaded ahead of the MFMAs)
+    float thr[2], bias[2];
+    bool pass_all[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const uint32_t c = n0 + sae_col(lane, w, j);
-      colok[j] = c < a.g.d_dict;
-      bias[j] = colok[j] ? a.g.bias[c] : 0.0f;
+      const bool colok = c < a.g.d_dict;
+      thr[j] = colok ? a.thr[c] : __uint_as_float(0x7FC00000u);
+      bias[j] = colok ? a.g.bias[c] : 0.0f;
+      pass_all[j] = all && colok;
     }
+    if (wcnt > kSaeSlice / 2) {
+      flush(wcnt);
+      wcnt = 0;
+    }
+    f32x16 acc[2][2];
+    sae_tile_mma(a.g, m0, n0, tl, acc);
+    const uint32_t wcnt0 = wcnt;
+    if (!all && m0 + kSaeBM <= a.g.B) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float av = acc[i][j][v];
+            const bool ok = av >= thr[j];
+            const uint64_t s = __ballot(ok);
+            if (s == 0) continue;
+            if (ok) {
+              const uint32_t pos =
+                  wcnt + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(s >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(s), 0u));
+              if (pos < kSaeSlice) {
+                wkey[pos] = key_f32(__float_as_uint(sae_relu(av + bias[j])));
+                widx[pos] = (m0 + sae_row(lane, w, i, v)) * a.g.d_dict + n0 + sae_col(lane, w, j);
+              }
+            }
+            wcnt += static_cast<uint32_t>(__popcll(s));
+          }
+      if (wcnt <= kSaeSlice) continue;
+      wcnt = wcnt0;  // the slice overflowed: drop this tile's entries, redo it below
+    }
+    // General epilogue, per half i: the lane's 32 accumulators through the
+    // wave's 8 KB of the (idle) tile buffers; element e = 16 j + v.
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      float z[32];
-      uint32_t m = 0;
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          z[16 * j + v] = sae_relu(acc[i][j][v] + bias[j]);
-          const bool ok = colok[j] && m0 + sae_row(lane, w, i, v) < a.g.B &&
-                          key_f32(__float_as_uint(z[16 * j + v])) >= tau;
-          m |= (ok ? 1u : 0u) << (16 * j + v);
-        }
-      const uint32_t cnt = __popc(m);
-      if (__ballot(cnt != 0) == 0) continue;
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
+      for (int q = 0; q < 8; ++q) {
+        const f32x16& src = acc[i][q >> 2];
+        const int v0 = 4 * (q & 3);
         *reinterpret_cast<float4*>(&stage[lane * 32 + 4 * q]) =
-            make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
-      // one stage reservation per wave
-      const uint32_t incl = wave_incl_sum(cnt);
-      const uint32_t total = __shfl(incl, kWave - 1, kWave);
-      uint32_t base = 0;
-      if (lane == 0) base = atomicAdd(&s_cnt, total);
-      base = __shfl(base, 0, kWave);
-      const uint32_t n_in = base < kStage ? min(total, kStage - base) : 0u;
-      uint32_t gbase = 0;
-      if (total - n_in) {
-        if (lane == 0) gbase = atomicAdd(seg_counter, total - n_in);
-        gbase = __shfl(gbase, 0, kWave);
+            make_float4(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3]);
       }
-      const uint32_t first_over = base + n_in;
-      uint32_t slot = base + incl - cnt;
-      while (m) {
-        const uint32_t bit = __builtin_ctz(m);
-        m &= m - 1;
-        const uint32_t key = key_f32(__float_as_uint(stage[lane * 32 + bit]));
-        const int j = static_cast<int>(bit >> 4), v = static_cast<int>(bit & 15);
-        const uint32_t idx = (m0 + sae_row(lane, w, i, v)) * a.g.d_dict + n0 + sae_col(lane, w, j);
-        my_max = max(my_max, key);
-        atomicAdd(&s_hist[log_bin(key - tau)], 1u);
-        if (slot < kStage) {
-          s_skey[slot] = key;
-          s_sidx[slot] = idx;
-        } else {
-          const uint32_t gp = gbase + (slot - first_over);
+      for (uint32_t e = 0; e < 32; ++e) {
+        const uint32_t j = e >> 4, v = e & 15;
+        const float av = stage[lane * 32 + e];
+        const uint32_t r = m0 + (w >> 1) * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        const bool ok = (j ? pass_all[1] || av >= thr[1] : pass_all[0] || av >= thr[0]) && r < a.g.B;
+        const uint64_t s = __ballot(ok);
+        if (s == 0) continue;
+        uint32_t base = 0;
+        if (lane == 0) base = atomicAdd(seg_counter, static_cast<uint32_t>(__popcll(s)));
+        base = __shfl(base, 0, kWave);
+        if (ok) {
+          const uint32_t gp = base + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(s >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(s), 0u));
+          const uint32_t key = key_f32(__float_as_uint(sae_relu(av + (j ? bias[1] : bias[0]))));
+          note(key);
           if (gp < a.seg_cap) {
             seg_key[gp] = key;
-            seg_idx[gp] = idx;
+            seg_idx[gp] = r * a.g.d_dict + n0 + (w & 1) * 64 + j * 32 + (lane & 31);
           }
         }
-        ++slot;
       }
     }
   }
+  if (wcnt) flush(wcnt);
   const uint32_t wm = wave_max_u32(my_max);
   if (lane == 0) s_wmax[w] = wm;
   __syncthreads();
-  const uint32_t n_st = min(s_cnt, kStage);
-  if (tid == 0) {
-    s_base = n_st ? atomicAdd(seg_counter, n_st) : 0u;
-    uint32_t m = 0;
+  uint32_t m = 0;
 #pragma unroll
-    for (int i = 0; i < kSaeBS / kWave; ++i) m = max(m, s_wmax[i]);
-    a.blk_max[b] = m;
-  }
-  __syncthreads();
-  for (uint32_t i = tid; i < n_st; i += kSaeBS) {
-    const uint32_t gp = s_base + i;
-    if (gp < a.seg_cap) {
-      seg_key[gp] = s_skey[i];
-      seg_idx[gp] = s_sidx[i];
-    }
-  }
-  if (s_cnt) {
+  for (int i = 0; i < kSaeBS / kWave; ++i) m = max(m, s_wmax[i]);
+  if (tid == 0) a.blk_max[b] = m;
+  if (m) {  // survivors' keys are >= key(+0) > 0
     for (uint32_t i = tid; i < kLogBins; i += kSaeBS) {
       const uint32_t c = s_hist[i];
       if (c) atomicAdd(&a.fhist[i], c);
@@ -441,19 +501,24 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_dense(SaeDenseArgs a) {
   for (uint32_t tl_i = xt.first; tl_i < xt.count; tl_i += xt.stride) {
     uint32_t m0, n0;
     xt.tile(tl_i, m0, n0);
+    float bias[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t c = n0 + sae_col(lane, w, j);
+      bias[j] = c < a.g.d_dict ? a.g.bias[c] : 0.0f;
+    }
     f32x16 acc[2][2];
     sae_tile_mma(a.g, m0, n0, tl, acc);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const uint32_t c = n0 + sae_col(lane, w, j);
       if (c >= a.g.d_dict) continue;
-      const float bias = a.g.bias[c];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const uint32_t r = m0 + sae_row(lane, w, i, v);
-          if (r < a.g.B) a.out[static_cast<size_t>(r) * a.g.d_dict + c] = sae_relu(acc[i][j][v] + bias);
+          if (r < a.g.B) a.out[static_cast<size_t>(r) * a.g.d_dict + c] = sae_relu(acc[i][j][v] + bias[j]);
         }
     }
   }
@@ -589,7 +654,8 @@ SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int 
   const uint32_t last_nb = Sn - (S.G_u - 1) * kSaeUnionPer;
   S.union_n_u = (S.G_u - 1) * S.tcap_u + (t < last_nb ? t : last_nb);  // fits the vector path's union area
   S.off_skeys = (S.flat.bytes + 255) & ~static_cast<size_t>(255);
-  S.off_dense = (S.off_skeys + static_cast<size_t>(Sn) * 4 + 255) & ~static_cast<size_t>(255);
+  S.off_thr = (S.off_skeys + static_cast<size_t>(Sn) * 4 + 255) & ~static_cast<size_t>(255);
+  S.off_dense = (S.off_thr + static_cast<size_t>(d_dict) * 4 + 255) & ~static_cast<size_t>(255);
   S.bytes = S.off_dense + static_cast<size_t>(B) * d_dict * 4;
   return S;
 }
@@ -647,10 +713,13 @@ hipError_t launch_sae_topk(const SaeCall& c) {
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_select_tau(uk, c.L.union_n_u, static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess)
     return e;
+  float* thr = reinterpret_cast<float*>(ws + c.L.off_thr);
+  hipLaunchKernelGGL(k_sae_thresholds, dim3(cdiv_s(c.d_dict, 256)), dim3(256), 0, c.stream, st, c.bias, c.d_dict,
+                     thr);
   const uint32_t tm = cdiv_s(c.B, kSaeBM), tn = cdiv_s(c.d_dict, kSaeBN);
   SaeFilterArgs fa{g, tm, tn, st, L.seg_cap, seg_cnt,
                    reinterpret_cast<uint32_t*>(ws + L.off_seg_key), reinterpret_cast<uint32_t*>(ws + L.off_seg_idx),
-                   reinterpret_cast<uint32_t*>(ws + L.off_blk_max), fhist};
+                   reinterpret_cast<uint32_t*>(ws + L.off_blk_max), fhist, thr};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
   hipLaunchKernelGGL(k_sae_filter, dim3(c.L.G), dim3(kSaeBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
