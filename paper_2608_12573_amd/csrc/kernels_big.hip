@@ -6,15 +6,15 @@
 // candidates spread over small buckets takes the bucket path:
 //   k_bkt_plan     status; bucket offsets in descending bucket order from
 //                  the filter's histogram of log_bin(key - tau), and the
-//                  bucket b* holding rank k;
+//                  bucket b* holding rank k; when the bucket path does not
+//                  apply, the radix path's state instead;
 //   k_bkt_scatter  every candidate of a bucket >= b* into its bucket's range
 //                  of the staging array;
 //   k_bkt_sort     one block per bucket sorts it in LDS and writes the
 //                  outputs at the bucket's offset.
 // Every other call (a fallback, DIRECT, or a bucket larger than kBktCap)
-// takes the radix path, whose kernels return at once after a bucket call:
-//   k_big_begin    status from the candidate counts; the source is the
-//                  candidate segments, or the whole input on fallback.
+// takes the radix path, whose kernels return at once after a bucket call
+// (its source is the candidate segments, or the whole input on fallback):
 //   k_big_pass     one radix digit per launch: block histograms are merged
 //                  into a global histogram and the last block (ticket) picks
 //                  the digit holding rank k.  Key digits first, then, if the
@@ -137,6 +137,55 @@ __device__ __forceinline__ void load_segn(const BigArgs& a, uint32_t* segn) {
   __syncthreads();
 }
 
+// ---------------------------------------------------------------- begin ---
+// The radix path's state, from the call's status (run by k_bkt_plan's
+// workgroup of 1024 when the bucket path does not apply).
+template <int DT>
+__device__ __forceinline__ void big_begin(const BigArgs& a, uint32_t status, uint32_t total, uint32_t* wsum) {
+  constexpr int KB = Elem<DT>::KEYBITS;
+  const uint32_t tid = threadIdx.x;
+  BigState* s = a.bs;
+  for (uint32_t i = tid; i < kBigBins; i += 1024) a.ghist[i] = 0;
+  const uint32_t key_max = KB == 32 ? 0xFFFFFFFFu : 0xFFFFu;
+  uint32_t lo = 0, hi = key_max;
+  if (status == PROFK_STATUS_FILTERED) {
+    lo = a.st->tau_key;
+    hi = max(lo, block_max<1024>(tid < a.G_f ? a.blk_max[tid] : 0u, wsum));
+  }
+  if (tid == 0) {
+    const bool filtered = status == PROFK_STATUS_FILTERED;
+    s->mode = kModeRadix;
+    s->status = status;
+    s->total = total;
+    s->tau = a.direct ? 0u : a.st->tau_key;
+    s->from_input = filtered ? 0u : 1u;
+    s->n_src = filtered ? total : a.n;
+    s->kk = filtered ? min(a.k, total) : a.k;
+    s->prefix = lo;
+    s->krem = s->kk;
+    s->above = 0;
+    s->equal = 0;
+    s->hi = KB - shared_prefix_bits(lo, hi, KB);
+    s->kstar = lo;
+    s->cut = 0;
+    s->iprefix = 0;
+    s->ikrem = 0;
+    s->ihi = 0;
+    s->istar = 0xFFFFFFFFu;
+    s->ticket = 0;
+    s->out_count = 0;
+    if (s->hi == 0) {
+      // every candidate carries the same key: only the index cut is left
+      s->equal = s->n_src;
+      if (s->kk < s->n_src) {
+        s->cut = 1;
+        s->ikrem = s->kk;
+        s->ihi = 32;
+      }
+    }
+  }
+}
+
 // ----------------------------------------------------------- bucket path ---
 template <int DT>
 __global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
@@ -157,7 +206,7 @@ __global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
   }
   if (status != PROFK_STATUS_FILTERED) {
-    if (tid == 0) s->mode = kModeRadix;
+    big_begin<DT>(a, status, total, fs.wsum);
     return;
   }
   const uint32_t kk = min(a.k, total);
@@ -203,8 +252,12 @@ __global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
   }
   big = block_max<1024>(big, fs.wsum);
   const bool bucket = big <= kBktCap;
+  if (!bucket) {
+    big_begin<DT>(a, status, total, fs.wsum);
+    return;
+  }
   if (tid == 0) {
-    s->mode = bucket ? kModeBucket : kModeRadix;
+    s->mode = kModeBucket;
     s->bstar = bstar;
     s->nlist = nlist;
     s->status = status;
@@ -214,7 +267,6 @@ __global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
     s->from_input = 0;
     s->kk = kk;
   }
-  if (!bucket) return;
   for (uint32_t p = kk + tid; p < a.k; p += 1024) {  // relaxed recall: padding
     if (DT == 0) static_cast<uint32_t*>(a.out_vals)[p] = 0xFF800000u;
     else static_cast<uint16_t*>(a.out_vals)[p] = 0xFF80u;
@@ -373,67 +425,6 @@ __global__ __launch_bounds__(kSortBS) void k_bkt_sort(BigArgs a) {
       }
     }
     __syncthreads();  // the next bucket reuses the LDS
-  }
-}
-
-// ---------------------------------------------------------------- begin ---
-template <int DT>
-__global__ __launch_bounds__(1024) void k_big_begin(BigArgs a) {
-  constexpr int KB = Elem<DT>::KEYBITS;
-  __shared__ uint32_t wsum[20];
-  __shared__ uint32_t s_total;
-  const uint32_t tid = threadIdx.x;
-  BigState* s = a.bs;
-  if (s->mode == kModeBucket) return;
-  for (uint32_t i = tid; i < kBigBins; i += 1024) a.ghist[i] = 0;
-  uint32_t status = PROFK_STATUS_DIRECT, total = 0;
-  if (!a.direct) {
-    if (tid == 0) {
-      uint32_t t = 0;
-      for (int x = 0; x < kSegs; ++x) t += a.seg_cnt[x * kSegStride];
-      s_total = t;
-    }
-    __syncthreads();
-    total = s_total;
-    status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
-                             : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
-  }
-  const uint32_t key_max = KB == 32 ? 0xFFFFFFFFu : 0xFFFFu;
-  uint32_t lo = 0, hi = key_max;
-  if (status == PROFK_STATUS_FILTERED) {
-    lo = a.st->tau_key;
-    hi = max(lo, block_max<1024>(tid < a.G_f ? a.blk_max[tid] : 0u, wsum));
-  }
-  if (tid == 0) {
-    const bool filtered = status == PROFK_STATUS_FILTERED;
-    s->status = status;
-    s->total = total;
-    s->tau = a.direct ? 0u : a.st->tau_key;
-    s->from_input = filtered ? 0u : 1u;
-    s->n_src = filtered ? total : a.n;
-    s->kk = filtered ? min(a.k, total) : a.k;
-    s->prefix = lo;
-    s->krem = s->kk;
-    s->above = 0;
-    s->equal = 0;
-    s->hi = KB - shared_prefix_bits(lo, hi, KB);
-    s->kstar = lo;
-    s->cut = 0;
-    s->iprefix = 0;
-    s->ikrem = 0;
-    s->ihi = 0;
-    s->istar = 0xFFFFFFFFu;
-    s->ticket = 0;
-    s->out_count = 0;
-    if (s->hi == 0) {
-      // every candidate carries the same key: only the index cut is left
-      s->equal = s->n_src;
-      if (s->kk < s->n_src) {
-        s->cut = 1;
-        s->ikrem = s->kk;
-        s->ihi = 32;
-      }
-    }
   }
 }
 
@@ -710,7 +701,6 @@ static hipError_t launch_big_t(const BigCall& c) {
   hipLaunchKernelGGL(k_bkt_plan<DT>, dim3(1), dim3(1024), 0, c.stream, a);
   hipLaunchKernelGGL(k_bkt_scatter<DT>, dim3(c.G_big), dim3(kScatBS), 0, c.stream, a);
   hipLaunchKernelGGL(k_bkt_sort<DT>, dim3(kBktSortBlocks), dim3(kSortBS), 0, c.stream, a);
-  hipLaunchKernelGGL(k_big_begin<DT>, dim3(1), dim3(1024), 0, c.stream, a);
   const uint32_t key_passes = cdiv_u(KB, kBigDigit);
   for (uint32_t p = 0; p < key_passes; ++p)
     hipLaunchKernelGGL((k_big_pass<DT, 0>), dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);

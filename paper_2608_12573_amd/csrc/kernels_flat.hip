@@ -122,13 +122,21 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
   auto gload = [&](uint32_t i) { return a.keys[i]; };
   SelectResult r;
   if (a.n <= kTauCache) {
-    for_items<kTauBS, 8>(a.n, gload, [&](uint32_t i, uint32_t v) { cache[i] = v; });
-    __syncthreads();
+    uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+    for_items<kTauBS, 8>(a.n, gload, [&](uint32_t i, uint32_t v) {
+      cache[i] = v;
+      mn = min(mn, v);
+      mx = max(mx, v);
+    });
+    // The high bits all keys share need no digit pass, and the first pass
+    // then spreads the keys over its bins instead of piling them into a few.
+    mx = block_max<kTauBS>(mx, sel.wsum);
+    mn = ~block_max<kTauBS>(~mn, sel.wsum);
     r = block_select_kth<kTauBS>(
         [&](auto f) {
           for (uint32_t i = tid; i < a.n; i += kTauBS) f(cache[i]);
         },
-        a.t, a.keybits, 0u, sel);
+        a.t, a.keybits - shared_prefix_bits(mn, mx, a.keybits), mn, sel);
   } else {
     r = block_select_kth<kTauBS>(
         [&](auto f) { for_items<kTauBS, 8>(a.n, gload, [&](uint32_t, uint32_t v) { f(v); }); },
