@@ -184,7 +184,7 @@ class Workload:
             self.host = None
             self.x = self.sx
             K = B * k_row
-            self.p = pk.plan(B * d_dict, K, 1e-6, 1.0, **rule)
+            self.p = pk.plan_sae(B, d_dict, k_row, 1e-6, 1.0, **rule)
             self.kernel = "k_sae_filter (bf16 MFMA GEMM + filter epilogue)"
             self.desc = (f"BatchTopK SAE encoder: bf16 x [{B}, {d_model}] (N(0,1)) times W_enc [{d_dict}, {d_model}] "
                          f"(N(0,1/d_model)), fp32 bias -0.5 (+1.5 on every 100th latent), ReLU, top K={B}*{k_row}="

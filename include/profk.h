@@ -107,6 +107,15 @@ void profk_default_opts(profk_plan_opts_t* opts);
  * "Optimal Sample Size", leaves the ratio to a benchmark of the hardware). */
 void profk_default_row_opts(profk_plan_opts_t* opts);
 
+/* Defaults for profk_sae_encode_topk plans (N = B * d_dict, k = B * k_row):
+ * the flat defaults with cost ratio 1/64.  A draw of the fused SAE path is
+ * a d_model-long dot product on the matrix cores (two row reads), far
+ * dearer than the flat path's one gathered element, so Algorithm 1's S*
+ * falls to S_min; the measured fused step at the paper's shape (B = 4096,
+ * d_model = 512, d_dict = 12288, k = 32) is fastest there (Sec. 4,
+ * "Optimal Sample Size", leaves the ratio to a benchmark of the hardware). */
+void profk_default_sae_opts(profk_plan_opts_t* opts);
+
 /* Parameter selection, host only, pure and thread-safe (Algorithm 1 for S;
  * t and M as the smallest integers whose exact binomial failure tails stay
  * within eps_A and eps_B -- the design goal of Sec. 3 and Theorem 1).

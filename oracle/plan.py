@@ -65,6 +65,10 @@ class PlanOpts:
 
 
 ROW_OPTS = PlanOpts(S_min=256, cost_ratio=0.5)
+# The fused SAE path: a draw is a d_model-long dot product, not one gathered
+# element, so tau_B / tau_A is measured far below 1 (Sec. 4, "Optimal Sample
+# Size", leaves the ratio to a benchmark of the hardware).
+SAE_OPTS = PlanOpts(cost_ratio=1.0 / 64.0)
 
 
 @dataclass(frozen=True)

@@ -79,6 +79,7 @@ def lib():
         P = ctypes.POINTER
         L.profk_default_opts.argtypes = [P(PlanOpts)]
         L.profk_default_row_opts.argtypes = [P(PlanOpts)]
+        L.profk_default_sae_opts.argtypes = [P(PlanOpts)]
         L.profk_plan.argtypes = [i64, i64, dbl, dbl, P(PlanOpts), P(Plan)]
         L.profk_plan_rows.argtypes = [i64, i64, dbl, dbl, P(PlanOpts), P(Plan)]
         L.profk_workspace_size.argtypes = [P(Plan), i32, i64]
@@ -125,9 +126,12 @@ def _check(rc):
         raise ProfkError(msg)
 
 
-def opts(flat=True, **kw):
+def opts(flat=True, sae=False, **kw):
     o = PlanOpts()
-    (lib().profk_default_opts if flat else lib().profk_default_row_opts)(ctypes.byref(o))
+    if sae:
+        lib().profk_default_sae_opts(ctypes.byref(o))
+    else:
+        (lib().profk_default_opts if flat else lib().profk_default_row_opts)(ctypes.byref(o))
     for key, val in kw.items():
         setattr(o, key, val)
     return o
@@ -137,6 +141,15 @@ def plan(N, k, eps=1e-6, recall=1.0, **kw):
     """profk_plan: (S, t, M) for N values and top-k."""
     p = Plan()
     _check(lib().profk_plan(N, k, eps, recall, ctypes.byref(opts(True, **kw)), ctypes.byref(p)))
+    return p
+
+
+def plan_sae(B, d_dict, k_row, eps=1e-6, recall=1.0, **kw):
+    """profk_plan for the fused SAE path (N = B*d_dict, K = B*k_row) with
+    profk_default_sae_opts."""
+    p = Plan()
+    _check(lib().profk_plan(B * d_dict, B * k_row, eps, recall, ctypes.byref(opts(True, sae=True, **kw)),
+                            ctypes.byref(p)))
     return p
 
 
@@ -315,7 +328,7 @@ def sae_encode_topk(x, w_enc, b_enc, k_row, eps=1e-6, recall=1.0, seed=0, p=None
     torch = _torch()
     B, d_model, d_dict = _sae_shape(x, w_enc, b_enc)
     K = B * k_row
-    p = p if p is not None else plan(B * d_dict, K, eps, recall)
+    p = p if p is not None else plan_sae(B, d_dict, k_row, eps, recall)
     ws = ws if ws is not None else sae_workspace(p, B, d_dict, x.device)
     if out is None:
         out = (torch.empty(K, dtype=torch.float32, device=x.device),

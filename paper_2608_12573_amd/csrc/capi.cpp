@@ -102,6 +102,15 @@ int profk_plan(int64_t N, int64_t k, double eps, double recall, const profk_plan
   return profk::make_plan(N, k, eps, recall, o, out);
 }
 
+void profk_default_sae_opts(profk_plan_opts_t* o) {
+  profk_default_opts(o);
+  if (!o) return;
+  // tau_B / tau_A measured for the fused SAE path on MI355X: a draw is a
+  // d_model-long dot product on the matrix cores with two row reads, not a
+  // single gathered element, so fewer draws and a larger buffer are faster.
+  o->cost_ratio = 1.0 / 64.0;
+}
+
 int profk_plan_rows(int64_t D, int64_t k, double eps, double recall, const profk_plan_opts_t* opts,
                     profk_plan_t* out) {
   profk_plan_opts_t o;

@@ -57,6 +57,14 @@ def test_row_planner_equals_oracle(D):
             _same(p, q)
 
 
+@pytest.mark.parametrize("B,d_dict,k_row", [(4096, 12288, 32), (4096, 65536, 64), (256, 2048, 8), (64, 512, 4)])
+def test_sae_planner_equals_oracle(B, d_dict, k_row):
+    for eps, recall in ((1e-6, 1.0), (1e-3, 0.95)):
+        p = pk.plan_sae(B, d_dict, k_row, eps, recall)
+        q = oplan.plan(B * d_dict, B * k_row, eps, recall, oplan.SAE_OPTS)
+        _same(p, q)
+
+
 def test_paper_literal_and_options_equal_oracle():
     cases = [dict(paper_literal=1), dict(S_min=64, S_max=64, force_mode=pk.FORCE_FILTER), dict(lexicographic=1),
              dict(cost_ratio=0.1), dict(eps_split=0.3), dict(S_min=131072, S_max=131072)]

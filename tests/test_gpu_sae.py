@@ -102,6 +102,19 @@ def test_sae_encode_topk(B, d_model, d_dict, k_row):
     assert np.array_equal(vals.cpu().numpy().view(np.uint32), dense[order].view(np.uint32))
 
 
+def test_sae_encode_topk_default_plan():
+    # the binding's default plan (profk_default_sae_opts: the sample floor)
+    B, d_model, d_dict, k_row = 512, 256, 4096, 16
+    m = workloads.sae_model(B=B, d_model=d_model, d_dict=d_dict, seed=19)
+    g = _dev(m)
+    p = pk.plan_sae(B, d_dict, k_row)
+    note(f"sae default plan S={p.S} t={p.t} M={p.M} mode={p.mode}")
+    vals, idx, info = pk.sae_encode_topk(g["x"], g["w_enc"], g["b_enc"], k_row, seed=1)
+    assert int(pk.read_info(info)[0]["status"]) in (0, 3)
+    z = osae.encode(m["x"], m["w_enc"], m["b_enc"])
+    _check_selection(vals.cpu().numpy().astype(np.float64), idx.cpu().numpy(), z, _tol(m), B * k_row)
+
+
 def test_sae_encode_topk_fallback():
     # a 64-draw sample with a small buffer overflows: the dense latents are
     # written to the workspace and selected exactly
