@@ -10,6 +10,7 @@
 //                  MFMA sequence as the GEMM (so its value is the GEMM's, bit
 //                  for bit), and each sample workgroup's top-t of them;
 //   k_select_tau   stage 2 (shared with the vector path);
+//   k_sae_thresholds  each column's accumulator threshold for tau;
 //   k_sae_filter   the GEMM with stage 3 in its epilogue: survivors are
 //                  compacted exactly as the vector filter does it, so the
 //                  vector path's refinement (stage 4) runs unchanged;
@@ -20,11 +21,8 @@
 // z W_dec[j, :] + b_dec, grouped by row and summed in ascending j, so the
 // result does not depend on the order the selection lists them in.
 //
-// GEMM shape: a workgroup of 4 waves computes a 128x128 tile of z, a wave a
-// 64x64 block as 2x2 v_mfma_f32_32x32x16_bf16 accumulators; d_model is
-// consumed in chunks of 64 staged through LDS (rows padded to 144 B).
-// One 32x32x16 step rounds once: the accumulator and its 16 products are
-// summed together before rounding to fp32.
+// One 32x32x16 MFMA step rounds once: the accumulator and its 16 products
+// are summed together before rounding to fp32.
 #include "device_common.h"
 #include "launch.h"
 #include "sample_union.h"
@@ -76,21 +74,21 @@ __device__ __forceinline__ void sae_tile_mma(const SaeGemm& g, uint32_t m0, uint
   // piece id = q * kSaeBS + tid is row id / 8, 16-byte segment id % 8 of the
   // chunk.  Two register sets hold the chunks in flight: chunk c + 2 is
   // loaded while chunk c is computed and stored to LDS after chunk c + 1 is.
+  // Rows past B and columns past d_dict load the last row or column instead
+  // (no branch around a load, so the loads' waits stay exact): they only
+  // feed accumulators of rows and columns the epilogues skip.
   u32x4v ra[2][kSaeApieces], rb[2][kSaeBpieces];
   auto gload = [&](uint32_t kc, u32x4v (&xa)[kSaeApieces], u32x4v (&xb)[kSaeBpieces]) {
     const size_t col = static_cast<size_t>(kc) * kSaeBK;
 #pragma unroll
     for (int q = 0; q < kSaeApieces; ++q) {
-      const uint32_t id = q * kSaeBS + tid, gm = m0 + (id >> 3);
-      xa[q] = gm < g.B ? *reinterpret_cast<const u32x4v*>(g.x + static_cast<size_t>(gm) * g.d_model + col + (id & 7) * 8)
-                       : u32x4v{0u, 0u, 0u, 0u};
+      const uint32_t id = q * kSaeBS + tid, gm = min(m0 + (id >> 3), g.B - 1);
+      xa[q] = *reinterpret_cast<const u32x4v*>(g.x + static_cast<size_t>(gm) * g.d_model + col + (id & 7) * 8);
     }
 #pragma unroll
     for (int q = 0; q < kSaeBpieces; ++q) {
-      const uint32_t id = q * kSaeBS + tid, gn = n0 + (id >> 3);
-      xb[q] = gn < g.d_dict
-                  ? *reinterpret_cast<const u32x4v*>(g.w + static_cast<size_t>(gn) * g.d_model + col + (id & 7) * 8)
-                  : u32x4v{0u, 0u, 0u, 0u};
+      const uint32_t id = q * kSaeBS + tid, gn = min(n0 + (id >> 3), g.d_dict - 1);
+      xb[q] = *reinterpret_cast<const u32x4v*>(g.w + static_cast<size_t>(gn) * g.d_model + col + (id & 7) * 8);
     }
   };
   auto lstore = [&](uint32_t buf, const u32x4v (&xa)[kSaeApieces], const u32x4v (&xb)[kSaeBpieces]) {
@@ -127,19 +125,44 @@ __device__ __forceinline__ void sae_tile_mma(const SaeGemm& g, uint32_t m0, uint
   lstore(0, ra[0], rb[0]);
   if (nchunk > 1) gload(1, ra[1], rb[1]);
   __syncthreads();
-  // chunk kc is in LDS buffer kc % 2; register set s holds chunk kc + 1 on
-  // entry to an even (s = 1) or odd (s = 0) step
-  for (uint32_t kc = 0; kc < nchunk; kc += 2) {
-    if (kc + 2 < nchunk) gload(kc + 2, ra[0], rb[0]);
+  // Chunk c is in LDS buffer c % 2 and register set c % 2.  The steady loop
+  // has no branch around its loads, so the compiler's waits before each LDS
+  // store cover that set's loads only and chunk c + 2 stays in flight; the
+  // last one to three chunks are peeled off.
+  // (sched_barrier keeps the compiler from sinking the loads below the
+  // MFMAs, which would shorten their lead to under one chunk.)
+  uint32_t kc = 0;
+  for (; kc + 3 < nchunk; kc += 2) {
+    gload(kc + 2, ra[0], rb[0]);
+    __builtin_amdgcn_sched_barrier(0);
     compute(0);
-    if (kc + 1 < nchunk) lstore(1, ra[1], rb[1]);  // buffer 1 was last read before the previous barrier
+    lstore(1, ra[1], rb[1]);  // buffer 1 was last read before the previous barrier
     __syncthreads();
-    if (kc + 1 >= nchunk) break;
-    if (kc + 3 < nchunk) gload(kc + 3, ra[1], rb[1]);
+    gload(kc + 3, ra[1], rb[1]);
+    __builtin_amdgcn_sched_barrier(0);
     compute(1);
-    if (kc + 2 < nchunk) lstore(0, ra[0], rb[0]);  // buffer 0 was read before the barrier above
+    lstore(0, ra[0], rb[0]);  // buffer 0 was read before the barrier above
     __syncthreads();
   }
+  if (kc + 2 < nchunk) {  // chunks kc, kc + 1, kc + 2
+    gload(kc + 2, ra[0], rb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(0);
+    lstore(1, ra[1], rb[1]);
+    __syncthreads();
+    compute(1);
+    lstore(0, ra[0], rb[0]);
+    __syncthreads();
+    compute(0);
+  } else if (kc + 1 < nchunk) {  // chunks kc, kc + 1
+    compute(0);
+    lstore(1, ra[1], rb[1]);
+    __syncthreads();
+    compute(1);
+  } else {  // chunk kc
+    compute(0);
+  }
+  __syncthreads();
 }
 
 // XCD-aware tile order.  Workgroups are dispatched to the 8 XCDs round-robin
@@ -391,10 +414,11 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
     bool pass_all[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const uint32_t c = n0 + sae_col(lane, w, j);
+      const uint32_t c = n0 + sae_col(lane, w, j), cc = min(c, a.g.d_dict - 1);
       const bool colok = c < a.g.d_dict;
-      thr[j] = colok ? a.thr[c] : __uint_as_float(0x7FC00000u);
-      bias[j] = colok ? a.g.bias[c] : 0.0f;
+      const float th = a.thr[cc], bi = a.g.bias[cc];  // unconditional loads, then the column check
+      thr[j] = colok ? th : __uint_as_float(0x7FC00000u);
+      bias[j] = colok ? bi : 0.0f;
       pass_all[j] = all && colok;
     }
     if (wcnt > kSaeSlice / 2) {
@@ -503,10 +527,7 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_dense(SaeDenseArgs a) {
     xt.tile(tl_i, m0, n0);
     float bias[2];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t c = n0 + sae_col(lane, w, j);
-      bias[j] = c < a.g.d_dict ? a.g.bias[c] : 0.0f;
-    }
+    for (int j = 0; j < 2; ++j) bias[j] = a.g.bias[min(n0 + sae_col(lane, w, j), a.g.d_dict - 1)];
     f32x16 acc[2][2];
     sae_tile_mma(a.g, m0, n0, tl, acc);
 #pragma unroll
