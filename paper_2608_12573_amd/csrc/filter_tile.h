@@ -69,72 +69,18 @@ __device__ __forceinline__ bool tile_any(const u32x4 (&v)[U], const Thresh<DT>& 
   return mx >= th.thr;
 }
 
-// Exact pass over a lane's tile.  Vector u of the lane is tile vector
-// vb + u*BS + lane_pos, valid when below vend; element e of a vector is
-// input element base + vector*EPV + e.  count() returns the lane's survivor
-// count; emit(f) calls f(key, index) for each survivor in element order.
+// Exact pass over a lane's tile, taken when some lane of the wave holds a
+// survivor.  Vector u of the lane is tile vector vb + u*BS + pos, valid when
+// below vend; element e of a vector is input element base + vector*EPV + e.
+// The survivor bits of each vector are formed with packed arithmetic: with
+// thr1 = thr - 1, the saturating difference thr1 - w is negative iff
+// w >= thr, so its sign bits are the survivor flags (bf16: two per word,
+// gathered into one mask per vector with byte permutes).  emit() then visits
+// each lane's set bits in a short loop per vector instead of one predicated
+// branch per element, which matters where survivors are common (a row of the
+// per-row path keeps about M/D of its elements, 0.5 % of a 131072-wide bf16
+// row, so nearly every wave holds a few in every tile).
 // LEX: the lexicographic rule (ties at the threshold cut by index).
-template <int DT, int U, int BS, bool LEX = false>
-struct TileExact {
-  __device__ __forceinline__ bool keep(int x, uint32_t i) const { return LEX ? th.keep(x, i) : x >= th.thr; }
-
-  const u32x4 (&v)[U];
-  const Thresh<DT>& th;
-  uint32_t vb, vend, pos, base;
-
-  __device__ __forceinline__ uint32_t count() const {
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t vi = vb + u * BS + pos;
-      const bool valid = vi < vend;
-      const uint32_t i0 = base + vi * Elem<DT>::EPV;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t w = v[u][e] ^ th.flip;
-        if (DT == 0) {
-          cnt += (valid && keep(static_cast<int>(w), i0 + e)) ? 1u : 0u;
-        } else {
-          cnt += (valid && keep(static_cast<int>(w << 16) >> 16, i0 + 2 * e)) ? 1u : 0u;
-          cnt += (valid && keep(static_cast<int>(w) >> 16, i0 + 2 * e + 1)) ? 1u : 0u;
-        }
-      }
-    }
-    return cnt;
-  }
-
-  template <class F>
-  __device__ __forceinline__ void emit(F f) const {
-    constexpr int EPV = Elem<DT>::EPV;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t vi = vb + u * BS + pos;
-      const bool valid = vi < vend;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t raw = v[u][e];
-        const uint32_t w = raw ^ th.flip;
-        if (DT == 0) {
-          if (valid && keep(static_cast<int>(w), base + vi * EPV + e)) f(key_f32(raw), base + vi * EPV + e);
-        } else {
-          if (valid && keep(static_cast<int>(w << 16) >> 16, base + vi * EPV + 2 * e))
-            f(key_bf16(raw & 0xFFFFu), base + vi * EPV + 2 * e);
-          if (valid && keep(static_cast<int>(w) >> 16, base + vi * EPV + 2 * e + 1))
-            f(key_bf16(raw >> 16), base + vi * EPV + 2 * e + 1);
-        }
-      }
-    }
-  }
-};
-
-// The same exact pass for tiles in which survivors are common (a row of
-// the per-row path keeps about M/D of its elements, 0.5 % at C4 shape, so
-// nearly every wave holds a few in every tile).  The survivor bits of each
-// vector are formed with packed arithmetic: with thr1 = thr - 1, the
-// saturating difference thr1 - w is negative iff w >= thr, so its sign bits
-// are the survivor flags (bf16: two per word, gathered into one mask per
-// vector with byte permutes).  emit() then visits each lane's set bits in a
-// short loop per vector, instead of one predicated branch per element.
 template <int DT, int U, int BS, bool LEX = false>
 struct TileSparse {
   static constexpr int EPV = Elem<DT>::EPV;

@@ -150,7 +150,9 @@ __device__ __forceinline__ void big_begin(const BigArgs& a, uint32_t status, uin
   uint32_t lo = 0, hi = key_max;
   if (status == PROFK_STATUS_FILTERED) {
     lo = a.st->tau_key;
-    hi = max(lo, block_max<1024>(tid < a.G_f ? a.blk_max[tid] : 0u, wsum));
+    uint32_t bm = 0;
+    for (uint32_t i = tid; i < a.G_f; i += 1024) bm = max(bm, a.blk_max[i]);
+    hi = max(lo, block_max<1024>(bm, wsum));
   }
   if (tid == 0) {
     const bool filtered = status == PROFK_STATUS_FILTERED;

@@ -246,25 +246,39 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   constexpr int EPV = Elem<DT>::EPV;
   constexpr int ES = Elem<DT>::ES;
   __shared__ uint32_t s_skey[kStage], s_sidx[kStage];
-  // the sample union and the select histogram while tau is chosen, then the
-  // block's log-bin histogram of its survivors
-  __shared__ __align__(16) uint32_t s_pool[kFiltTauMax + kSelBins];
-  __shared__ SelectScratch s_scr;
-  static_assert(kLogBins <= kFiltTauMax + kSelBins, "filter histogram");
-  uint32_t* const s_union = s_pool;
-  uint32_t* const s_lists = s_pool + kFiltTauMax;
+  // the waves' top-t lists while tau is chosen, then the block's log-bin
+  // histogram of its survivors
+  __shared__ __align__(16) uint32_t s_pool[kLogBins];
+  static_assert(kFiltBS / kWave * kWaveTopMax <= kLogBins, "tau lists");
+  uint32_t* const s_lists = s_pool;
+  __shared__ uint32_t s_found[kFiltBS / kWave];
   __shared__ uint32_t s_cnt, s_tau, s_base;
   __shared__ uint32_t s_wmax[kFiltBS / kWave];
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), b = blockIdx.x;
   const uint32_t seg = b & (kSegs - 1);
   if (tid == 0) s_cnt = 0;
 
-  // The block's first step is loaded before the threshold is known, so the
-  // loads are in flight while tau is chosen.
+  // The sample union (when this block selects tau) is loaded first and the
+  // block's first step after it: a wave's loads return in order, so the
+  // union arrives at once and tau is chosen while the step is in flight.
   const u32x4* vec = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.values) +
                                                     static_cast<size_t>(a.head) * ES);
   const uint32_t vbeg = b * a.vpb;
   const uint32_t vend = min(vbeg + a.vpb, a.nvec);
+  constexpr int E = kFiltTauMax / kFiltBS;
+  const bool one_wave = a.union_n <= kWave * kFiltTauWave;
+  uint32_t uk[E];
+  uint32_t valid = 0;
+  if (a.union_n) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      // one wave: lane + 64 e for e < kFiltTauWave; four waves: tid + 256 e
+      const uint32_t i = one_wave ? lane + kWave * e : tid + kFiltBS * e;
+      const bool in = (one_wave ? (tid < kWave && e < static_cast<int>(kFiltTauWave)) : true) && i < a.union_n;
+      uk[e] = in ? a.union_keys[i] : 0u;
+      if (in) valid |= 1u << e;
+    }
+  }
   u32x4 v[kFiltU];
   auto load_step = [&](uint32_t vb, uint32_t fill) {
 #pragma unroll
@@ -278,42 +292,22 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   // passes, and the exact test skips slots past the end anyway.
   load_step(vbeg, 0xFFFFFFFFu);
 
-  // ---- threshold (stage 2) when the sample union is small
+  // ---- threshold (stage 2) when the sample union is small (t <= 32)
   uint32_t tau;
   if (a.union_n) {
-    if (a.t <= kWaveTopMax && a.union_n <= kWave * kFiltTauWave) {
+    uint32_t last = 0;
+    if (one_wave) {
       // one wave holds the whole union in registers
       if (tid < kWave) {
-        uint32_t uk[kFiltTauWave];
-        uint32_t valid = 0;
-#pragma unroll
-        for (int e = 0; e < static_cast<int>(kFiltTauWave); ++e) {
-          const uint32_t i = lane + kWave * e;
-          uk[e] = i < a.union_n ? a.union_keys[i] : 0u;
-          if (i < a.union_n) valid |= 1u << e;
-        }
-        uint32_t last = 0;
-        wave_top_t<kFiltTauWave>(uk, valid, a.t, nullptr, last);
+        wave_top_t<E>(uk, valid, a.t, nullptr, last);
         if (lane == 0) s_tau = last;
       }
-    } else if (a.t <= kWaveTopMax) {
-      for (uint32_t i = tid; i < a.union_n; i += kFiltBS) s_union[i] = a.union_keys[i];
-      __syncthreads();
+    } else {
       // every wave keeps the top t of its share, wave 0 merges the lists
       constexpr int NW = kFiltBS / kWave;
-      constexpr int E = kFiltTauMax / kFiltBS;
-      uint32_t uk[E];
-      uint32_t valid = 0;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint32_t i = tid + kFiltBS * e;
-        uk[e] = i < a.union_n ? s_union[i] : 0u;
-        if (i < a.union_n) valid |= 1u << e;
-      }
-      uint32_t last = 0;
       const uint32_t w = tid / kWave;
       const uint32_t got = wave_top_t<E>(uk, valid, a.t, s_lists + w * kWaveTopMax, last);
-      if (lane == 0) s_scr.found[w] = got;
+      if (lane == 0) s_found[w] = got;
       __syncthreads();
       if (w == 0) {
         constexpr int E2 = NW * kWaveTopMax / kWave;
@@ -325,21 +319,12 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
           v2[e] = 0;
 #pragma unroll
           for (int i = 0; i < NW; ++i)
-            if (li == static_cast<uint32_t>(i) && c >= s_scr.found[i]) { c -= s_scr.found[i]; li = i + 1; }
+            if (li == static_cast<uint32_t>(i) && c >= s_found[i]) { c -= s_found[i]; li = i + 1; }
           if (li < NW) { v2[e] = s_lists[li * kWaveTopMax + c]; valid2 |= 1u << e; }
         }
         wave_top_t<E2>(v2, valid2, a.t, nullptr, last);
         if (lane == 0) s_tau = last;
       }
-    } else {
-      for (uint32_t i = tid; i < a.union_n; i += kFiltBS) s_union[i] = a.union_keys[i];
-      __syncthreads();
-      const SelectResult r = block_select_kth<kFiltBS, kSelDigit>(
-          [&](auto f) {
-            for (uint32_t i = tid; i < a.union_n; i += kFiltBS) f(s_union[i]);
-          },
-          a.t, Elem<DT>::KEYBITS, 0u, s_lists, s_scr);
-      if (tid == 0) s_tau = r.kth;
     }
     __syncthreads();
     tau = s_tau;
@@ -394,11 +379,12 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   for (uint32_t vb = vbeg; vb < vend; vb += kFiltBS * kFiltU) {
     if (vb != vbeg) load_step(vb, th.neutral);
     if (__ballot(tile_any<DT, kFiltU>(v, th)) == 0) continue;
-    // Rare path: exact per-element test, one slot reservation per wave.
-    const TileExact<DT, kFiltU, kFiltBS, LEX> tx{v, th, vb, vend, tid, a.head};
+    // Rare path: per-vector survivor masks, one slot reservation per wave,
+    // then a short loop over each lane's set bits.
+    const TileSparse<DT, kFiltU, kFiltBS, LEX> ts(v, th, vb, vend, tid, a.head);
     uint32_t slot, first_over, gbase;
-    reserve(tx.count(), slot, first_over, gbase);
-    tx.emit([&](uint32_t key, uint32_t idx) { store(slot++, first_over, gbase, key, idx); });
+    reserve(ts.count(), slot, first_over, gbase);
+    ts.emit(v, [&](uint32_t key, uint32_t idx) { store(slot++, first_over, gbase, key, idx); });
   }
 
   // Elements before the first aligned vector and after the last one.
@@ -666,7 +652,9 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
     }
   } else {
     __syncthreads();
-    const uint32_t gmax = block_max<kFinBS>(tid < a.G_f ? a.blk_max[tid] : 0u, fs.wsum);
+    uint32_t bm = 0;
+    for (uint32_t i = tid; i < a.G_f; i += kFinBS) bm = max(bm, a.blk_max[i]);
+    const uint32_t gmax = block_max<kFinBS>(bm, fs.wsum);
     block_topk<kFinBS, kFinDigit>(src, total, kk, tau, max(gmax, tau), KB, sh.gen.topk());
     sort_write_any<DT, kFinBS>(sh.gen.sortbuf, kk, a.k, reinterpret_cast<uint64_t*>(sh.gen.cache),
                                a.out_vals, a.out_idx);
@@ -795,9 +783,10 @@ __global__ __launch_bounds__(1024) void k_gather_buffer(uint32_t cap, const uint
 static inline uint32_t cdiv(uint64_t a, uint64_t b) { return static_cast<uint32_t>((a + b - 1) / b); }
 static inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-// Filter workgroups one CU holds at once (the persistent grid is sized to
-// what is resident, so no workgroup starts after the others have finished).
-static int filter_blocks_per_cu(int dtype) {
+// Filter workgroups one CU holds at once, capped at `want` (the persistent
+// grid is sized to what is resident, so no workgroup starts after the
+// others have finished).
+static int filter_blocks_per_cu(int dtype, int want) {
   static int cached[2] = {0, 0};
   const int d = dtype == PROFK_F32 ? 0 : 1;
   if (cached[d] == 0) {
@@ -805,9 +794,9 @@ static int filter_blocks_per_cu(int dtype) {
     const hipError_t e = d == 0
         ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0, false>, kFiltBS, 0)
         : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1, false>, kFiltBS, 0);
-    cached[d] = (e == hipSuccess && n > 0) ? (n < 4 ? n : 4) : 4;
+    cached[d] = (e == hipSuccess && n > 0) ? n : kFiltPerCuDense;
   }
-  return cached[d];
+  return cached[d] < want ? cached[d] : want;
 }
 
 FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
@@ -820,7 +809,10 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   L.tcap = t < static_cast<uint32_t>(kSampPerBlock) ? t : kSampPerBlock;
   const uint32_t last_nb = S - (L.G_s - 1) * kSampPerBlock;
   L.union_n = (L.G_s - 1) * L.tcap + (t < last_nb ? t : last_nb);
-  const int per_cu = filter_blocks_per_cu(dtype);
+  // Expected survivors per element are about t / (S + 1).
+  const bool sparse = N * (dtype == PROFK_F32 ? 4u : 2u) >= kFiltSparseMinBytes &&
+                      static_cast<uint64_t>(t) * kFiltSparseInvDensity < static_cast<uint64_t>(S) + 1;
+  const int per_cu = filter_blocks_per_cu(dtype, sparse ? kFiltPerCuSparse : kFiltPerCuDense);
   const uint32_t maxg = static_cast<uint32_t>(num_cus * per_cu < kFiltMaxBlocks ? num_cus * per_cu : kFiltMaxBlocks);
   uint32_t g = cdiv(cdiv(N, epv), kFiltBS * kFiltU);
   L.G_f = g < 1 ? 1 : (g > maxg ? maxg : g);

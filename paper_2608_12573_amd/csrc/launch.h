@@ -30,9 +30,18 @@ constexpr int kTauBS = 1024;
 constexpr int kFiltBS = 256;                  // threads of a filter block
 constexpr int kFiltU = 8;                     // 16-byte loads in flight per lane
 constexpr int kFiltMaxBlocks = 1024;
+// Filter blocks per CU.  A large input whose survivors are rare streams
+// fastest with two (fewer concurrent streams: about 5 % on a GiB, and a
+// plain read kernel shows the same); where survivors are common, or the
+// input is smaller, four hide the survivor work better.
+constexpr int kFiltPerCuSparse = 2;
+constexpr int kFiltPerCuDense = 4;
+constexpr uint64_t kFiltSparseMinBytes = 512ull << 20;  // "large"
+constexpr uint64_t kFiltSparseInvDensity = 4096;        // "rare": t/(S+1) below 1/4096
 constexpr uint32_t kFiltTauMax = 2048;        // largest sample union a filter block selects from
 constexpr uint32_t kFiltTauWave = 4;          // union keys per lane when one wave selects tau
 constexpr uint32_t kFiltTauInMaxT = 32;       // largest t the filter blocks select tau for themselves
+static_assert(kFiltTauInMaxT <= kWaveTopMax, "the filter selects tau with the wave-level top-t");
 constexpr uint32_t kStage = 1024;             // survivors a filter block stages in LDS
 constexpr int kSegs = 8;                      // candidate segments (one counter each)
 constexpr int kSegStride = 64;                // words between segment counters
