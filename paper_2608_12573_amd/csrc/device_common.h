@@ -196,6 +196,113 @@ struct SelectResult {
   uint32_t equal;    // items equal to kth
 };
 
+// Hand-over of results between the workgroups of one kernel.  A device-wide
+// fence (__threadfence) writes back and invalidates the whole L2 of the
+// calling XCD, and when every producer pays for one they serialise.
+// Instead producers write the handed-over data with agent-scope stores
+// (coherent across the XCDs' L2 caches) or atomics and wait for them to
+// complete before taking a ticket; only the consumer that wins the ticket
+// invalidates its L2 (an agent-scope acquire) before it reads.
+__device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void wait_memory() { __builtin_amdgcn_s_waitcnt(0); }
+__device__ __forceinline__ void acquire_agent() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+
+// LDS histogram increment of `bin` for the calling lanes with `active`
+// set.  The lanes whose bin equals the first active lane's add with one
+// atomic; the others add their own.  A digit most keys share (a plateau of
+// equal values, candidates that all lie near the top) would otherwise
+// serialise every lane on one LDS address.  May be called from divergent
+// code: only the lanes that execute it take part.
+__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
+  const uint64_t act = __ballot(active);
+  if (act == 0) return;
+  const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
+  const uint32_t lb = __shfl(bin, leader, kWave);
+  const bool same = active && bin == lb;
+  const uint64_t sm = __ballot(same);
+  if (static_cast<int>(threadIdx.x & (kWave - 1)) == leader) atomicAdd(&hist[lb], static_cast<uint32_t>(__popcll(sm)));
+  if (active && !same) atomicAdd(&hist[bin], 1u);
+}
+
+// Slot in an LDS list for each calling lane with `take` set: one atomic on
+// the list's counter per wave, slots in lane order.  Returns the slot
+// (unspecified for lanes without `take`).  May be called from divergent
+// code: only the lanes that execute it take part.
+__device__ __forceinline__ uint32_t lds_append(uint32_t* counter, bool take) {
+  const uint64_t m = __ballot(take);
+  if (m == 0) return 0u;
+  const int leader = __ffsll(static_cast<unsigned long long>(m)) - 1;
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  uint32_t base = 0;
+  if (static_cast<int>(lane) == leader) base = atomicAdd(counter, static_cast<uint32_t>(__popcll(m)));
+  base = __shfl(base, leader, kWave);
+  const uint64_t below = lane == 0 ? 0ull : (m & (~0ull >> (kWave - lane)));
+  return base + static_cast<uint32_t>(__popcll(below));
+}
+
+// Wave 0 of a block (the caller makes only lanes of one wave call it)
+// finds the bin of `hist` (nb bins, a power of two, 16-byte aligned) that
+// holds rank krem (1-based) counted from the highest bin, and stores
+// sh.found = {bin, items in higher bins, items in the bin}.  Requires
+// 1 <= krem <= the histogram's total.
+__device__ __forceinline__ void rank_bin_search(const uint32_t* hist, uint32_t nb, uint32_t krem,
+                                                SelectScratch& sh) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (nb >= static_cast<uint32_t>(4 * kWave)) {
+    // lane L owns bins [nb - (L+1)*per, nb - L*per); lane 0 the highest
+    const uint32_t per = nb / kWave;  // a multiple of 4
+    const uint32_t base = nb - (lane + 1) * per;
+    uint32_t loc = 0;
+    for (uint32_t q = 0; q < per; q += 4) {
+      const uint4 v4 = *reinterpret_cast<const uint4*>(&hist[base + q]);
+      loc += v4.x + v4.y + v4.z + v4.w;
+    }
+    uint32_t run = wave_incl_sum(loc) - loc;
+    if (run < krem && krem <= run + loc) {
+      // the rank falls in this lane's bins: walk them from the top
+      for (int q = static_cast<int>(per) - 4; q >= 0; q -= 4) {
+        const uint4 v4 = *reinterpret_cast<const uint4*>(&hist[base + q]);
+        const uint32_t c4[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+        for (int j = 3; j >= 0; --j) {
+          if (run < krem && krem <= run + c4[j]) {
+            sh.found[0] = base + q + j;
+            sh.found[1] = run;
+            sh.found[2] = c4[j];
+          }
+          run += c4[j];
+        }
+      }
+    }
+  } else {
+    // at most 128 bins: lane L owns descending ranks [L*per, (L+1)*per)
+    const uint32_t per = (nb + kWave - 1) / kWave;  // 1 or 2
+    uint32_t hv[2];
+    uint32_t loc = 0;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const uint32_t r = lane * per + q;
+      hv[q] = (static_cast<uint32_t>(q) < per && r < nb) ? hist[nb - 1 - r] : 0u;
+      loc += hv[q];
+    }
+    uint32_t run = wave_incl_sum(loc) - loc;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const uint32_t r = lane * per + q;
+      if (static_cast<uint32_t>(q) < per && r < nb) {
+        if (run < krem && krem <= run + hv[q]) {
+          sh.found[0] = nb - 1 - r;
+          sh.found[1] = run;
+          sh.found[2] = hv[q];
+        }
+        run += hv[q];
+      }
+    }
+  }
+}
+
 // The kk-th largest (1-based, with multiplicity) of the selection keys
 // produced by `visit`.  visit(f) must call f(skey) once for every item of
 // the set, from any thread; every call site in the block calls it with the
@@ -211,7 +318,6 @@ __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t k
                                                          SelectScratch& sh) {
   static_assert(DIGIT >= 8 && DIGIT <= 13, "digit width");
   const uint32_t tid = threadIdx.x;
-  const int lane = tid & (kWave - 1);
   uint32_t krem = kk, above_total = 0, eq = 0;
   int hi = nbits;
   if (hi == 0) {
@@ -227,63 +333,9 @@ __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t k
     for (uint32_t b = tid; b < nb; b += BS) hist[b] = 0;
     __syncthreads();
     const uint32_t pre = prefix & hmask;
-    visit([&](uint32_t s) {
-      if ((s & hmask) == pre) atomicAdd(&hist[(s >> shift) & (nb - 1)], 1u);
-    });
+    visit([&](uint32_t s) { hist_add(hist, (s >> shift) & (nb - 1), (s & hmask) == pre); });
     __syncthreads();
-    if (tid < kWave) {
-      if (nb >= static_cast<uint32_t>(4 * kWave)) {
-        // lane L owns bins [nb - (L+1)*per, nb - L*per); lane 0 the highest
-        const uint32_t per = nb / kWave;  // a multiple of 4
-        const uint32_t base = nb - (lane + 1) * per;
-        uint32_t loc = 0;
-        for (uint32_t q = 0; q < per; q += 4) {
-          const uint4 v4 = *reinterpret_cast<const uint4*>(&hist[base + q]);
-          loc += v4.x + v4.y + v4.z + v4.w;
-        }
-        uint32_t run = wave_incl_sum(loc) - loc;
-        if (run < krem && krem <= run + loc) {
-          // the rank falls in this lane's bins: walk them from the top
-          for (int q = static_cast<int>(per) - 4; q >= 0; q -= 4) {
-            const uint4 v4 = *reinterpret_cast<const uint4*>(&hist[base + q]);
-            const uint32_t c4[4] = {v4.x, v4.y, v4.z, v4.w};
-#pragma unroll
-            for (int j = 3; j >= 0; --j) {
-              if (run < krem && krem <= run + c4[j]) {
-                sh.found[0] = base + q + j;
-                sh.found[1] = run;
-                sh.found[2] = c4[j];
-              }
-              run += c4[j];
-            }
-          }
-        }
-      } else {
-        // at most 128 bins: lane L owns descending ranks [L*per, (L+1)*per)
-        const uint32_t per = (nb + kWave - 1) / kWave;  // 1 or 2
-        uint32_t hv[2];
-        uint32_t loc = 0;
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const uint32_t r = lane * per + q;
-          hv[q] = (static_cast<uint32_t>(q) < per && r < nb) ? hist[nb - 1 - r] : 0u;
-          loc += hv[q];
-        }
-        uint32_t run = wave_incl_sum(loc) - loc;
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const uint32_t r = lane * per + q;
-          if (static_cast<uint32_t>(q) < per && r < nb) {
-            if (run < krem && krem <= run + hv[q]) {
-              sh.found[0] = nb - 1 - r;
-              sh.found[1] = run;
-              sh.found[2] = hv[q];
-            }
-            run += hv[q];
-          }
-        }
-      }
-    }
+    if (tid < kWave) rank_bin_search(hist, nb, krem, sh);
     __syncthreads();
     const uint32_t d = sh.found[0], ab = sh.found[1];
     eq = sh.found[2];

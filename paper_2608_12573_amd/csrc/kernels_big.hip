@@ -464,12 +464,12 @@ __global__ __launch_bounds__(kBigBS) void k_big_pass(BigArgs a) {
   __syncthreads();
   for (uint32_t b = tid; b < nb; b += kBigBS)
     if (hist[b]) atomicAdd(&a.ghist[b], hist[b]);
-  __threadfence();
+  wait_memory();  // the histogram is handed over through atomics
   __syncthreads();
   if (tid == 0) s_last = (atomicAdd(&s->ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
+  acquire_agent();
   // The last block finds the digit holding the remaining rank.
   const uint32_t krem = STAGE == 0 ? s->krem : s->ikrem;
   const uint32_t per = (nb + kBigBS - 1) / kBigBS;  // bins per thread, descending

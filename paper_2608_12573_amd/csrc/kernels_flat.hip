@@ -194,13 +194,13 @@ __global__ __launch_bounds__(kSampBS) void k_tau_index(TauIdxArgs a) {
     s_base = nb ? atomicAdd(&a.st->tie_n, nb) : 0u;
   }
   __syncthreads();
-  for (uint32_t i = tid; i < nb; i += kSampBS) a.list[s_base + i] = s_list[i];
-  __threadfence();
+  for (uint32_t i = tid; i < nb; i += kSampBS) store_agent(&a.list[s_base + i], s_list[i]);
+  wait_memory();
   __syncthreads();
   if (tid == 0) s_last = atomicAdd(&a.st->tie_ticket, 1u) == gridDim.x - 1 ? 1u : 0u;
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
+  acquire_agent();
   const uint32_t a_tot = a.st->tie_above, ne = a.st->tie_n;
   uint32_t i_tau = 0xFFFFFFFFu;
   if (ne > 0 && a_tot < a.t) {
@@ -444,7 +444,6 @@ constexpr int kFinDigit = 12;
 struct FinShared {
   uint32_t cache[kFinCache];       // candidate keys; later the sort's exchange buffers
   uint64_t sortbuf[kFinMaxK];      // radix histogram, then the collected top k
-  uint32_t pre[1024];
   SelectScratch sel;
   uint32_t misc[8];
   __device__ __forceinline__ TopkSmem topk() {
@@ -486,43 +485,149 @@ struct SegSrc {
   __device__ __forceinline__ uint32_t idx_at(uint32_t i) const { return idx[pos(i)]; }
 };
 
-// Per-chunk exact results of the fallback: G regions of capacity C, region
-// r holding pre[r+1] - pre[r] entries (pre an LDS exclusive prefix, R the
-// total); one wave per region.
-struct RegionSrc {
-  const uint32_t *key, *idx;
-  uint32_t C, G, R;
-  const uint32_t* pre;
-  template <int BS, class F>
-  __device__ __forceinline__ void visit(uint32_t, const uint32_t* cache, F f) const {
-    constexpr uint32_t groups = BS / kWave;
-    const uint32_t g = threadIdx.x / kWave, l = threadIdx.x % kWave;
-    for (uint32_t r = g; r < G; r += groups) {
-      const uint32_t bi = pre[r];
-      const uint32_t n = (r + 1 < G ? pre[r + 1] : R) - bi;
-      const size_t bg = static_cast<size_t>(r) * C;
-      for (uint32_t j0 = l; j0 < n; j0 += kWave * 8) {
-        uint32_t kv[8];
+// The part of the input one fallback block owns, in index order: chunk b
+// holds the aligned 16-byte vectors [v0, v1) (v0 = b*cv; the last chunk
+// runs to the last vector); chunk 0 also holds the `head` elements before
+// the first aligned vector and the last chunk the elements after the last
+// one (fewer than a vector each).
+template <int DT, int BS>
+struct ChunkSrc {
+  static constexpr int EPV = Elem<DT>::EPV, ES = Elem<DT>::ES;
+  const void* values;
+  uint32_t n, head, v0, v1;
+  bool first, last;
+  uint32_t* counter;  // one LDS word
+  uint32_t* wsum;     // LDS scratch of block_excl_sum
+  __device__ __forceinline__ const u32x4* vec() const {
+    return reinterpret_cast<const u32x4*>(static_cast<const char*>(values) + static_cast<size_t>(head) * ES);
+  }
+  static __device__ __forceinline__ uint32_t raw_of(const u32x4& x, int e) {
+    return DT == 0 ? x[e] : (x[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+  }
+  __device__ __forceinline__ uint32_t tail0() const { return head + v1 * EPV; }
+  template <class F>
+  __device__ __forceinline__ void keys(F f) const {
+    constexpr int U = 8;
+    const u32x4* vp = vec();
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t vb = v0; vb < v1; vb += BS * U) {
+      u32x4 x[U];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const uint32_t j = j0 + u * kWave;
-          kv[u] = j < n ? (cache ? cache[bi + j] : key[bg + j]) : 0u;
+      for (int u = 0; u < U; ++u) {
+        const uint32_t vi = vb + u * BS + tid;
+        x[u] = vi < v1 ? vp[vi] : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t vi = vb + u * BS + tid;
+        if (vi < v1) {
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) f(head + vi * EPV + e, key_of<DT>(raw_of(x[u], e)));
         }
+      }
+    }
+    if (first)
+      for (uint32_t i = tid; i < head; i += BS) f(i, key_of<DT>(load_raw<DT>(values, i)));
+    if (last)
+      for (uint32_t i = tail0() + tid; i < n; i += BS) f(i, key_of<DT>(load_raw<DT>(values, i)));
+  }
+  __device__ __forceinline__ uint32_t idx_of(uint32_t pos) const { return pos; }
+  // g(index, r) for the m elements equal to `key` of smallest index: one
+  // vector per thread per sweep, ranked by a block-wide exclusive scan
+  template <class G>
+  __device__ __forceinline__ void ties_in_order(uint32_t key, uint32_t m, G g) const {
+    const uint32_t tid = threadIdx.x;
+    uint32_t taken = 0;
+    auto scalar = [&](uint32_t s0, uint32_t s1) {  // fewer than EPV elements: one thread
+      if (tid == 0) {
+        uint32_t c = taken;
+        for (uint32_t i = s0; i < s1; ++i)
+          if (c < m && key_of<DT>(load_raw<DT>(values, i)) == key) g(i, c++);
+        *counter = c;
+      }
+      __syncthreads();
+      taken = *counter;
+      __syncthreads();
+    };
+    if (first) scalar(0u, head);
+    const u32x4* vp = vec();
+    for (uint32_t vb = v0; vb < v1 && taken < m; vb += BS) {
+      const uint32_t vi = vb + tid;
+      uint32_t mask = 0;
+      if (vi < v1) {
+        const u32x4 x = vp[vi];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const uint32_t j = j0 + u * kWave;
-          if (j < n) f(bi + j, kv[u], LoadIdx{idx + bg + j});
+        for (int e = 0; e < EPV; ++e) mask |= (key_of<DT>(raw_of(x, e)) == key ? 1u : 0u) << e;
+      }
+      uint32_t tot;
+      uint32_t r = taken + block_excl_sum<BS>(static_cast<uint32_t>(__popc(mask)), wsum, &tot);
+      while (mask) {
+        const uint32_t e = __builtin_ctz(mask);
+        mask &= mask - 1;
+        if (r < m) g(head + vi * EPV + e, r);
+        ++r;
+      }
+      taken += tot;
+    }
+    if (last && taken < m) scalar(tail0(), n);
+  }
+};
+
+// A run of R (key, index) pairs at positions [off, off + R) of two global
+// arrays: results of fallback chunks or chunk groups, k pairs each, in no
+// particular order.  Keys are read as aligned 16-byte vectors, which may
+// reach up to 3 words on either side of the run (the arrays have slack).
+template <int BS>
+struct CandSrc {
+  const uint32_t *key, *idx;
+  uint32_t off, R;
+  uint32_t* hist;       // LDS, 2^kSelDigit words, for ties_in_order
+  SelectScratch* scr;   // LDS scratch of the select
+  uint32_t* counter;    // one LDS word
+  template <class F>
+  __device__ __forceinline__ void keys(F f) const {
+    constexpr int U = 8;
+    const u32x4* kv = reinterpret_cast<const u32x4*>(key);
+    const uint32_t end = off + R, vb0 = off / 4, nv = (end + 3) / 4, tid = threadIdx.x;
+    for (uint32_t vb = vb0; vb < nv; vb += BS * U) {
+      u32x4 x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t vi = vb + u * BS + tid;
+        x[u] = vi < nv ? kv[vi] : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t vi = vb + u * BS + tid;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t p = vi * 4 + e;
+          if (vi < nv && p >= off && p < end) f(p, x[u][e]);
         }
       }
     }
   }
-  __device__ __forceinline__ uint32_t idx_at(uint32_t i) const {
-    uint32_t lo = 0, hi = G;  // last region r with pre[r] <= i
-    while (hi - lo > 1) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if (pre[mid] <= i) lo = mid; else hi = mid;
-    }
-    return idx[static_cast<size_t>(lo) * C + (i - pre[lo])];
+  __device__ __forceinline__ uint32_t idx_of(uint32_t pos) const { return idx[pos]; }
+  // the m smallest indices among the pairs with key kv: a radix select on
+  // ~index over those pairs, then one collect pass
+  template <class G>
+  __device__ __forceinline__ void ties_in_order(uint32_t kv, uint32_t m, G g) const {
+    const SelectResult r = block_select_kth<BS, kSelDigit>(
+        [&](auto f) {
+          keys([&](uint32_t pos, uint32_t k) {
+            if (k == kv) f(~idx[pos]);
+          });
+        },
+        m, 32, 0u, hist, *scr);
+    const uint32_t istar = ~r.kth;
+    if (threadIdx.x == 0) *counter = 0;
+    __syncthreads();
+    keys([&](uint32_t pos, uint32_t k) {
+      const bool take = k == kv && idx[pos] <= istar;
+      const uint32_t q = lds_append(counter, take);
+      if (take) g(pos, q);
+    });
+    __syncthreads();
   }
 };
 
@@ -533,8 +638,9 @@ struct FinishArgs {
   uint32_t G_f, seg_cap;
   const uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
   CallState* st;
-  uint32_t G_fb, chunk;
-  uint32_t *cand_key, *cand_idx, *cand_cnt;
+  uint32_t head, nvec, cv;          // fallback chunks: see ChunkSrc
+  uint32_t *cand_key, *cand_idx;    // each chunk's top k, chunk b at b*k
+  uint32_t *grp_key, *grp_idx;      // each chunk group's top k, group g at g*k
   const uint32_t* fhist;           // the filter's histogram of log_bin(key - tau)
   void* out_vals;
   int64_t* out_idx;
@@ -676,7 +782,6 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   __shared__ SelectScratch fs;
   __shared__ uint32_t seg_n[kSegs], seg_pre[kSegs + 1], flag;
   constexpr int KB = Elem<DT>::KEYBITS;
-  const uint32_t key_max = KB == 32 ? 0xFFFFFFFFu : 0xFFFFu;
   const uint32_t tid = threadIdx.x, b = blockIdx.x;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
   if (!a.direct) {
@@ -700,36 +805,69 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
     }
   }
   // Exact fallback: each block takes the exact top-k of its chunk ...
-  const uint32_t lo = static_cast<uint32_t>(min<uint64_t>(a.n, static_cast<uint64_t>(b) * a.chunk));
-  const uint32_t hi = static_cast<uint32_t>(min<uint64_t>(a.n, static_cast<uint64_t>(lo) + a.chunk));
-  const uint32_t nb = hi - lo;
-  const uint32_t kb = min(a.k, nb);
-  if (kb) {
-    InputSrc<DT> src{a.values, lo};
-    block_topk<kFinBS, kFinDigit>(src, nb, kb, 0u, key_max, KB, sh.gen.topk());
-    for (uint32_t i = tid; i < kb; i += kFinBS) {
-      const uint64_t c = sh.gen.sortbuf[i];
-      a.cand_key[static_cast<size_t>(b) * a.k + i] = comp_key(c);
-      a.cand_idx[static_cast<size_t>(b) * a.k + i] = comp_idx(c);
+  constexpr int EPV = Elem<DT>::EPV;
+  const uint32_t G = gridDim.x;
+  const uint32_t tail = a.n - (a.head + a.nvec * EPV);
+  // elements of chunk c (ChunkSrc's partition)
+  auto chunk_n = [&](uint32_t c) {
+    const uint32_t v0 = min(c * a.cv, a.nvec);
+    const uint32_t v1 = c == G - 1 ? a.nvec : min(v0 + a.cv, a.nvec);
+    return (v1 - v0) * EPV + (c == 0 ? a.head : 0u) + (c == G - 1 ? tail : 0u);
+  };
+  const TopkSmem sm = sh.gen.topk();
+  {
+    const uint32_t v0 = min(b * a.cv, a.nvec);
+    const uint32_t v1 = b == G - 1 ? a.nvec : min(v0 + a.cv, a.nvec);
+    const uint32_t kb = min(a.k, chunk_n(b));  // k for every chunk but possibly the last
+    if (kb) {
+      const ChunkSrc<DT, kFinBS> src{a.values, a.n, a.head, v0, v1, b == 0, b == G - 1, sm.counter, fs.wsum};
+      window_topk<kFinBS, kFinDigit>(src, kb, KB, sm);
+      for (uint32_t p = tid; p < kb; p += kFinBS) {
+        const uint64_t c = sh.gen.sortbuf[p];
+        store_agent(&a.cand_key[static_cast<size_t>(b) * a.k + p], comp_key(c));
+        store_agent(&a.cand_idx[static_cast<size_t>(b) * a.k + p], comp_idx(c));
+      }
     }
   }
-  if (tid == 0) a.cand_cnt[b] = kb;
-  // ... and the last block to finish merges the per-chunk results.
-  __threadfence();
+  // ... the last chunk of each group of kFbGroup to finish merges the
+  // group's results, and the last group to finish merges the groups'.
+  const uint32_t NG = (G + kFbGroup - 1) / kFbGroup, gi = b / kFbGroup;
+  const uint32_t g0 = gi * kFbGroup, gn = min(G - g0, static_cast<uint32_t>(kFbGroup));
+  wait_memory();
   __syncthreads();
-  if (tid == 0) flag = (atomicAdd(&a.st->ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
+  if (tid == 0) flag = (atomicAdd(&a.st->grp_ticket[gi], 1u) == gn - 1) ? 1u : 0u;
   __syncthreads();
   if (!flag) return;
-  __threadfence();
-  const uint32_t cc = tid < gridDim.x ? a.cand_cnt[tid] : 0u;
-  uint32_t R;
-  const uint32_t pre = block_excl_sum<kFinBS>(cc, fs.wsum, &R);
-  if (tid < gridDim.x) sh.gen.pre[tid] = pre;
-  __syncthreads();
-  RegionSrc src{a.cand_key, a.cand_idx, a.k, gridDim.x, R, sh.gen.pre};
-  block_topk<kFinBS, kFinDigit>(src, R, a.k, 0u, key_max, KB, sh.gen.topk());
-  sort_write_any<DT, kFinBS>(sh.gen.sortbuf, a.k, a.k, reinterpret_cast<uint64_t*>(sh.gen.cache), a.out_vals,
-                             a.out_idx);
+  acquire_agent();
+  // pairs of the group: k from each chunk but the last, which holds fewer
+  // only when it is the last chunk of the input
+  const uint32_t rg = (gn - 1) * a.k + min(a.k, chunk_n(g0 + gn - 1));
+  const CandSrc<kFinBS> group{a.cand_key, a.cand_idx, g0 * a.k, rg, sm.hist, sm.scratch, sm.counter};
+  uint64_t* const exch = reinterpret_cast<uint64_t*>(sh.gen.cache);
+  if (NG > 1) {
+    const uint32_t kg = min(a.k, rg);
+    window_topk<kFinBS, kFinDigit>(group, kg, KB, sm);
+    for (uint32_t p = tid; p < kg; p += kFinBS) {
+      const uint64_t c = sh.gen.sortbuf[p];
+      store_agent(&a.grp_key[static_cast<size_t>(gi) * a.k + p], comp_key(c));
+      store_agent(&a.grp_idx[static_cast<size_t>(gi) * a.k + p], comp_idx(c));
+    }
+    wait_memory();
+    __syncthreads();
+    if (tid == 0) flag = (atomicAdd(&a.st->ticket, 1u) == NG - 1) ? 1u : 0u;
+    __syncthreads();
+    if (!flag) return;
+    acquire_agent();
+    // every group but the last holds k; the last holds min(k, its pairs)
+    const uint32_t gl = (NG - 1) * kFbGroup;
+    const uint32_t rl = (G - gl - 1) * a.k + min(a.k, chunk_n(G - 1));
+    const CandSrc<kFinBS> groups{a.grp_key, a.grp_idx, 0u, (NG - 1) * a.k + min(a.k, rl), sm.hist, sm.scratch,
+                                 sm.counter};
+    window_topk<kFinBS, kFinDigit>(groups, a.k, KB, sm);
+  } else {
+    window_topk<kFinBS, kFinDigit>(group, a.k, KB, sm);
+  }
+  sort_write_any<DT, kFinBS>(sh.gen.sortbuf, a.k, a.k, exch, a.out_vals, a.out_idx);
   if (tid == 0) {
     a.st->status = status;
     if (a.info) {
@@ -820,7 +958,6 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   const uint32_t fbmax = static_cast<uint32_t>(num_cus < kFbMaxBlocks ? num_cus : kFbMaxBlocks);
   uint32_t gb = cdiv(N, kFbMinChunk);
   L.G_fb = gb < 1 ? 1 : (gb > fbmax ? fbmax : gb);
-  L.chunk = cdiv(N, L.G_fb);
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
   L.off_state = take(sizeof(CallState));
@@ -841,9 +978,12 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
     L.off_bcur = take(static_cast<size_t>(kLogBins) * kBktPad * 4);
     L.off_blist = take(static_cast<size_t>(kLogBins) * 4);
   } else {
-    L.off_cand_key = take(static_cast<size_t>(L.G_fb) * k * 4);
+    // the merges read keys as aligned 16-byte vectors: 4 words of slack
+    const size_t NG = (L.G_fb + kFbGroup - 1) / kFbGroup;
+    L.off_cand_key = take((static_cast<size_t>(L.G_fb) * k + 4) * 4);
     L.off_cand_idx = take(static_cast<size_t>(L.G_fb) * k * 4);
-    L.off_cand_cnt = take(static_cast<size_t>(L.G_fb) * 4);
+    L.off_grp_key = take((NG * k + 4) * 4);
+    L.off_grp_idx = take(NG * k * 4);
   }
   L.off_fhist = take(static_cast<size_t>(kLogBins) * 4);
   if (p.lexicographic) L.off_tie = take(static_cast<size_t>(S) * 4);
@@ -895,14 +1035,25 @@ static hipError_t launch_refine_t(const FlatCall& c, bool direct, uint32_t G_f) 
                L.G_big, c.out_vals, c.out_idx, c.info, c.stream};
     return launch_big(bc);
   }
+  // Fallback chunks (ChunkSrc): whole 16-byte vectors after the unaligned
+  // head, as the filter splits the input, and at least max(k, kFbMinChunk)
+  // elements each, so that every chunk but the last holds k of the top.
+  constexpr int ES = Elem<DT>::ES, EPV = Elem<DT>::EPV;
+  const uintptr_t addr = reinterpret_cast<uintptr_t>(c.values);
+  uint32_t head = static_cast<uint32_t>(((16 - (addr & 15)) & 15) / ES);
+  if (head > c.n) head = c.n;
+  const uint32_t nvec = (c.n - head) / EPV;
+  const uint64_t min_chunk = c.k > kFbMinChunk ? c.k : kFbMinChunk;
+  const uint64_t gmax = static_cast<uint64_t>(nvec) * EPV / min_chunk;
+  const uint32_t G_fb = gmax < 1 ? 1u : (gmax < L.G_fb ? static_cast<uint32_t>(gmax) : L.G_fb);
   FinishArgs fa{c.values, c.n, c.k, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M),
                 direct ? 1 : 0, G_f, L.seg_cap,
                 seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
                 at<uint32_t>(c.ws, L.off_blk_max), st,
-                L.G_fb, L.chunk, at<uint32_t>(c.ws, L.off_cand_key), at<uint32_t>(c.ws, L.off_cand_idx),
-                at<uint32_t>(c.ws, L.off_cand_cnt), fhist,
-                c.out_vals, c.out_idx, c.info};
-  hipLaunchKernelGGL(k_finish<DT>, dim3(L.G_fb), dim3(kFinBS), 0, c.stream, fa);
+                head, nvec, cdiv(nvec, G_fb), at<uint32_t>(c.ws, L.off_cand_key), at<uint32_t>(c.ws, L.off_cand_idx),
+                at<uint32_t>(c.ws, L.off_grp_key), at<uint32_t>(c.ws, L.off_grp_idx),
+                fhist, c.out_vals, c.out_idx, c.info};
+  hipLaunchKernelGGL(k_finish<DT>, dim3(G_fb), dim3(kFinBS), 0, c.stream, fa);
   return hipGetLastError();
 }
 

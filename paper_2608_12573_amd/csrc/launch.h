@@ -19,8 +19,10 @@ struct CallState {
   uint32_t tie_above;  // draws above tau (k_tau_index)
   uint32_t tie_n;      // draws equal to tau, listed in the workspace
   uint32_t tie_ticket; // last-block-done counter of k_tau_index
-  uint32_t pad[57];
+  uint32_t grp_ticket[16];  // last-block-done counters of the fallback's chunk groups
+  uint32_t pad[41];
 };
+static_assert(sizeof(CallState) == 256, "call state size");
 
 // Launch geometry.
 constexpr int kSampBS = 256;                  // threads of a sample block
@@ -48,6 +50,8 @@ constexpr int kSegStride = 64;                // words between segment counters
 constexpr int kFinBS = 1024;
 constexpr int kFinMaxK = 4096;                // largest k of the one-block refinement
 constexpr int kFbMaxBlocks = 256;
+constexpr int kFbGroup = 16;                  // fallback chunks merged together first
+static_assert(kFbMaxBlocks / kFbGroup <= 16, "group counters in CallState");
 constexpr uint32_t kFinSlice = 1024;          // candidates a block histograms, at least
 constexpr uint32_t kFastCap = 8192;           // candidates the bucket refinement holds in LDS
 constexpr uint32_t kFastBucket = 128;         // largest bucket it ranks by comparison
@@ -69,10 +73,10 @@ struct FlatLayout {
   uint32_t G_s = 0, tcap = 0, union_n = 0;    // sampling
   uint32_t G_f = 0;                           // filter blocks
   uint32_t seg_cap = 0;                       // entries per candidate segment (= M)
-  uint32_t G_fb = 0, chunk = 0;               // fallback blocks, elements each
+  uint32_t G_fb = 0;                          // fallback blocks (at most)
   size_t off_state = 0, off_segcnt = 0, off_union = 0, off_blk_max = 0;
   size_t off_seg_key = 0, off_seg_idx = 0;
-  size_t off_cand_key = 0, off_cand_idx = 0, off_cand_cnt = 0;
+  size_t off_cand_key = 0, off_cand_idx = 0, off_grp_key = 0, off_grp_idx = 0;
   size_t off_fhist = 0;                       // log-bin histogram of the candidates
   size_t off_tie = 0;                         // lexicographic plans: indices of the draws equal to tau
   bool big = false;                           // k > kFinMaxK: multi-block refinement

@@ -23,6 +23,7 @@ __device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt, ui
     st->tie_n = 0;
     st->tie_ticket = 0;
   }
+  if (threadIdx.x < 16) st->grp_ticket[threadIdx.x] = 0;
 }
 
 template <int BS>
