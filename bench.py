@@ -19,7 +19,9 @@ around the launch on its own stream; `cpu_baseline` times the CPU oracle
 """
 
 import argparse
+import csv
 import ctypes
+import glob
 import hashlib
 import json
 import os
@@ -34,7 +36,7 @@ COUNTERS = os.path.join(ROOT, "profiles", "filter_counters.json")
 CSRC = os.path.join(ROOT, "paper_2608_12573_amd", "csrc")
 # Every source the filter kernel is compiled from: the committed counters
 # stand for this exact code and are dropped once any of these changes.
-FILTER_SRCS = ("kernels_flat.hip", "filter_tile.h", "device_common.h", "launch.h", "topk_block.h")
+FILTER_SRCS = ("kernels_filter.hip", "filter_tile.h", "device_common.h", "launch.h")
 WORKLOADS = ("c2", "c1", "c3a", "c3b", "c3c", "c3d", "c3d2", "c4", "c5", "c5r", "c5p", "sae")
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 FLUSH_BYTES = 512 << 20
@@ -87,6 +89,82 @@ def counters_traffic(workload_key):
     if c.get("kernel_source_sha256") != sha or c.get("workload_key") != workload_key:
         return None
     return c.get("traffic_bytes_per_launch")
+
+
+def write_counters(fetch_dir, write_dir, bench_json):
+    """profiles/filter_counters.json from two rocprofv3 --pmc runs of the
+    default workload (FETCH_SIZE, then WRITE_SIZE) and the JSON line one of
+    them printed.  The counters' units are calibrated on the 1 GiB device
+    copy bench.py's copy probe makes in the same runs."""
+    def per_dispatch(d, counter):
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            sys.exit(f"no counter_collection.csv under {d}")
+        disp = {}
+        for f in files:
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    if r["Counter_Name"] != counter:
+                        continue
+                    key = (r["Kernel_Name"], int(r["Grid_Size"]), r["Dispatch_Id"])
+                    disp[key] = disp.get(key, 0.0) + float(r["Counter_Value"])
+        kern = {}
+        for (name, grid, _), v in disp.items():
+            kern.setdefault((name, grid), []).append(v)
+        return {key: (sum(v) / len(v), len(v)) for key, v in kern.items()}
+
+    fetch, write = per_dispatch(fetch_dir, "FETCH_SIZE"), per_dispatch(write_dir, "WRITE_SIZE")
+    with open(bench_json) as fh:
+        line = json.loads(fh.read().strip().splitlines()[-1])
+
+    def pick(table, pred, biggest=False):
+        keys = [key for key in table if pred(key[0])]
+        if not keys:
+            sys.exit("kernel not found in the counter files")
+        return max(keys, key=lambda key: table[key][0]) if biggest else keys[0]
+
+    is_filter = lambda n: "k_filter<0, false>" in n
+    is_copy = lambda n: "copyBuffer" in n
+    fk, ck = pick(fetch, is_filter), pick(fetch, is_copy, biggest=True)
+    wk, cwk = pick(write, is_filter), pick(write, is_copy, biggest=True)
+    gib = float(1 << 30)
+    fpu, wpu = gib / fetch[ck][0], gib / write[cwk][0]
+    fb, wb = fetch[fk][0] * fpu, write[wk][0] * wpu
+    algo = line["roofline"]["algorithmic_bytes_per_launch"]
+    out = {
+        "kernel": "profk::k_filter<0, false> (fp32 filter-and-compact)",
+        "workload_key": "c2-k1024",
+        "workload": line["config"]["workload"] + f"; {line['count']} survivors",
+        "commands": [
+            "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o fetch --output-format csv -- "
+            "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-torch-baseline",
+            "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o write --output-format csv -- "
+            "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-torch-baseline",
+            "python bench.py --write-counters gpurun_out/pmc_fetch gpurun_out/pmc_write "
+            "gpurun_out/pmc_fetch.json",
+        ],
+        "fetch_size_kib_per_dispatch": round(fetch[fk][0], 2),
+        "write_size_kib_per_dispatch": round(write[wk][0], 2),
+        "dispatches": [fetch[fk][1], write[wk][1]],
+        "calibration": {
+            "kernel": "__amd_rocclr_copyBuffer (the copy probe: torch copy_ of the same 1 GiB tensor, "
+                      "in the same runs)",
+            "bytes_read": 1 << 30, "bytes_written": 1 << 30,
+            "fetch_size_kib": round(fetch[ck][0], 2), "write_size_kib": round(write[cwk][0], 2),
+            "fetch_bytes_per_kib_unit": round(fpu, 3), "write_bytes_per_kib_unit": round(wpu, 3),
+        },
+        "fetch_bytes_per_launch": int(round(fb)),
+        "write_bytes_per_launch": int(round(wb)),
+        "traffic_bytes_per_launch": int(round(fb + wb)),
+        "algorithmic_bytes_per_launch": algo,
+        "traffic_over_algorithmic": round((fb + wb) / algo, 5),
+        "kernel_source_sha256": filter_source_sha256(),
+        "kernel_sources": list(FILTER_SRCS),
+    }
+    with open(COUNTERS, "w") as fh:
+        json.dump(out, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(out, indent=1))
 
 
 class Workload:
@@ -266,7 +344,12 @@ def main():
     ap.add_argument("--no-copy-probe", action="store_true")
     ap.add_argument("--lexicographic", action="store_true",
                     help="plan with the tie-exact filter rule on (key, -index) pairs")
+    ap.add_argument("--write-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
+                    help="write profiles/filter_counters.json from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
+    if args.write_counters:
+        write_counters(*args.write_counters)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)

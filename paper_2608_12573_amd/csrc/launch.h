@@ -108,6 +108,11 @@ struct FlatCall {
 };
 
 hipError_t launch_flat(const FlatCall& c);
+// The filter pass of c into the workspace's candidate segments; tau from
+// the sample union when union_keys is given, else from st.
+hipError_t launch_filter(const FlatCall& c, CallState* st, const uint32_t* union_keys, bool lex);
+// Filter workgroups one CU holds at once, at most `want`.
+int filter_blocks_per_cu(int dtype, int want);
 // Refinement of the candidates a filter left in c.ws by G_f workgroups
 // (the fallback reads c.values), and tau from a stage-1 union into st.
 hipError_t launch_refine(const FlatCall& c, uint32_t G_f);
