@@ -155,20 +155,24 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* wsum) {
 // Calls body(i, load(i)) for every i in [0, n), BS*UNR items per sweep with
 // all loads of a sweep issued before any body runs (memory-level
 // parallelism for global sources).
+// Offsets are compared with the remaining count, and the loop stops before
+// base + BS*UNR could pass n, so n may be as large as 2^32 - 1.
 template <int BS, int UNR, class Load, class Body>
 __device__ __forceinline__ void for_items(uint32_t n, Load load, Body body) {
   for (uint32_t base = 0; base < n; base += BS * UNR) {
+    const uint32_t rem = n - base;
     uint32_t v[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
-      const uint32_t i = base + u * BS + threadIdx.x;
-      v[u] = (i < n) ? load(i) : 0u;
+      const uint32_t o = u * BS + threadIdx.x;
+      v[u] = (o < rem) ? load(base + o) : 0u;
     }
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
-      const uint32_t i = base + u * BS + threadIdx.x;
-      if (i < n) body(i, v[u]);
+      const uint32_t o = u * BS + threadIdx.x;
+      if (o < rem) body(base + o, v[u]);
     }
+    if (rem <= static_cast<uint32_t>(BS * UNR)) break;
   }
 }
 

@@ -92,42 +92,48 @@ struct SegPos {
 };
 
 // Grid-stride visit of the call's source: f(key, index) for every item.
+// Offsets are compared with the remaining count and a block stops before
+// its next sweep could pass n, so n may be as large as 2^32 - 1.
 template <int DT, int BS, class F>
 __device__ __forceinline__ void big_visit(const BigArgs& a, const BigState& s, const uint32_t* segn, F f) {
   const uint32_t n = s.n_src;
   const uint32_t stride = gridDim.x * BS * 8;
   if (s.from_input) {
     for (uint32_t base = blockIdx.x * BS * 8; base < n; base += stride) {
+      const uint32_t rem = n - base;
       uint32_t kv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const uint32_t i = base + u * BS + threadIdx.x;
-        kv[u] = i < n ? key_of<DT>(load_raw<DT>(a.values, i)) : 0u;
+        const uint32_t o = u * BS + threadIdx.x;
+        kv[u] = o < rem ? key_of<DT>(load_raw<DT>(a.values, base + o)) : 0u;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const uint32_t i = base + u * BS + threadIdx.x;
-        if (i < n) f(kv[u], i);
+        const uint32_t o = u * BS + threadIdx.x;
+        if (o < rem) f(kv[u], base + o);
       }
+      if (rem <= stride) break;
     }
   } else {
     const SegPos pos{segn, a.seg_cap};
     for (uint32_t base = blockIdx.x * BS * 8; base < n; base += stride) {
+      const uint32_t rem = n - base;
       uint32_t kv[8], iv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const uint32_t i = base + u * BS + threadIdx.x;
-        if (i < n) {
-          const size_t p = pos(i);
+        const uint32_t o = u * BS + threadIdx.x;
+        if (o < rem) {
+          const size_t p = pos(base + o);
           kv[u] = a.seg_key[p];
           iv[u] = a.seg_idx[p];
         }
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const uint32_t i = base + u * BS + threadIdx.x;
-        if (i < n) f(kv[u], iv[u]);
+        const uint32_t o = u * BS + threadIdx.x;
+        if (o < rem) f(kv[u], iv[u]);
       }
+      if (rem <= stride) break;
     }
   }
 }

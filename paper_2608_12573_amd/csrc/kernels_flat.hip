@@ -315,8 +315,8 @@ struct ChunkSrc {
     }
     if (first)
       for (uint32_t i = tid; i < head; i += BS) f(i, key_of<DT>(load_raw<DT>(values, i)));
-    if (last)
-      for (uint32_t i = tail0() + tid; i < n; i += BS) f(i, key_of<DT>(load_raw<DT>(values, i)));
+    if (last)  // fewer than a vector's elements, so no offset passes 2^32
+      for (uint32_t o = tid; o < n - tail0(); o += BS) f(tail0() + o, key_of<DT>(load_raw<DT>(values, tail0() + o)));
   }
   __device__ __forceinline__ uint32_t idx_of(uint32_t pos) const { return pos; }
   // g(index, r) for the m elements equal to `key` of smallest index: one
