@@ -334,7 +334,10 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    # A GPU idle during input generation needs a few milliseconds of work to
+    # reach its steady clocks: after 5 steps the per-row workload still reads
+    # 7 % slower than after 50.
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="c2", choices=WORKLOADS)
     ap.add_argument("--k", type=int, default=1024, help="k of the default N=2^28 workload")
     ap.add_argument("--cold", action="store_true",
