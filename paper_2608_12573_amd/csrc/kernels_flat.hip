@@ -12,8 +12,9 @@
 //   k_filter      the filter-and-compact pass (kernels_filter.hip).
 //   k_finish      reads the segment counts; when k_req <= count <= M one
 //                 block refines the candidates exactly, otherwise every
-//                 block computes the exact top-k of its chunk of the input
-//                 and the last block to finish merges them.
+//                 block computes the exact top-k of its chunk of the input,
+//                 the last of each group of 16 chunks to finish merges the
+//                 group's, and the last group to finish merges the groups'.
 #include <climits>
 
 #include "device_common.h"

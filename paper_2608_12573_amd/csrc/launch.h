@@ -52,7 +52,6 @@ constexpr int kFinMaxK = 4096;                // largest k of the one-block refi
 constexpr int kFbMaxBlocks = 256;
 constexpr int kFbGroup = 16;                  // fallback chunks merged together first
 static_assert(kFbMaxBlocks / kFbGroup <= 16, "group counters in CallState");
-constexpr uint32_t kFinSlice = 1024;          // candidates a block histograms, at least
 constexpr uint32_t kFastCap = 8192;           // candidates the bucket refinement holds in LDS
 constexpr uint32_t kFastBucket = 128;         // largest bucket it ranks by comparison
 constexpr uint32_t kFbMinChunk = 8192;
