@@ -32,7 +32,8 @@ struct FilterArgs {
 };
 
 // The filter pass; the survival test is in filter_tile.h.
-template <int DT, bool LEX>
+// U: 16-byte loads in flight per lane and step.
+template <int DT, bool LEX, int U>
 __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   constexpr int EPV = Elem<DT>::EPV;
   constexpr int ES = Elem<DT>::ES;
@@ -70,10 +71,10 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
       if (in) valid |= 1u << e;
     }
   }
-  u32x4 v[kFiltU];
+  u32x4 v[U];
   auto load_step = [&](uint32_t vb, uint32_t fill) {
 #pragma unroll
-    for (int u = 0; u < kFiltU; ++u) {
+    for (int u = 0; u < U; ++u) {
       const uint32_t vi = vb + u * kFiltBS + tid;
       if (vi < vend) v[u] = __builtin_nontemporal_load(vec + vi);
       else v[u] = u32x4{fill, fill, fill, fill};
@@ -167,12 +168,12 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     }
   };
 
-  for (uint32_t vb = vbeg; vb < vend; vb += kFiltBS * kFiltU) {
+  for (uint32_t vb = vbeg; vb < vend; vb += kFiltBS * U) {
     if (vb != vbeg) load_step(vb, th.neutral);
-    if (__ballot(tile_any<DT, kFiltU>(v, th)) == 0) continue;
+    if (__ballot(tile_any<DT, U>(v, th)) == 0) continue;
     // Rare path: per-vector survivor masks, one slot reservation per wave,
     // then a short loop over each lane's set bits.
-    const TileSparse<DT, kFiltU, kFiltBS, LEX> ts(v, th, vb, vend, tid, a.head);
+    const TileSparse<DT, U, kFiltBS, LEX> ts(v, th, vb, vend, tid, a.head);
     uint32_t slot, first_over, gbase;
     reserve(ts.count(), slot, first_over, gbase);
     ts.emit(v, [&](uint32_t key, uint32_t idx) { store(slot++, first_over, gbase, key, idx); });
@@ -236,8 +237,8 @@ int filter_blocks_per_cu(int dtype, int want) {
   if (cached[d] == 0) {
     int n = 0;
     const hipError_t e = d == 0
-        ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0, false>, kFiltBS, 0)
-        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1, false>, kFiltBS, 0);
+        ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0, false, kFiltUSmall>, kFiltBS, 0)
+        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1, false, kFiltUSmall>, kFiltBS, 0);
     cached[d] = (e == hipSuccess && n > 0) ? n : kFiltPerCuDense;
   }
   return cached[d] < want ? cached[d] : want;
@@ -260,8 +261,11 @@ static hipError_t launch_filter_t(const FlatCall& c, CallState* st, const uint32
                 at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max),
                 at<uint32_t>(c.ws, L.off_fhist)};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
-  if (lex) hipLaunchKernelGGL((k_filter<DT, true>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
-  else hipLaunchKernelGGL((k_filter<DT, false>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  const bool large = L.filt_u == kFiltULarge;
+  if (lex && large) hipLaunchKernelGGL((k_filter<DT, true, kFiltULarge>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  else if (lex) hipLaunchKernelGGL((k_filter<DT, true, kFiltUSmall>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  else if (large) hipLaunchKernelGGL((k_filter<DT, false, kFiltULarge>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  else hipLaunchKernelGGL((k_filter<DT, false, kFiltUSmall>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
   return hipGetLastError();
 }

@@ -724,7 +724,8 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
                       static_cast<uint64_t>(t) * kFiltSparseInvDensity < static_cast<uint64_t>(S) + 1;
   const int per_cu = filter_blocks_per_cu(dtype, sparse ? kFiltPerCuSparse : kFiltPerCuDense);
   const uint32_t maxg = static_cast<uint32_t>(num_cus * per_cu < kFiltMaxBlocks ? num_cus * per_cu : kFiltMaxBlocks);
-  uint32_t g = cdiv(cdiv(N, epv), kFiltBS * kFiltU);
+  L.filt_u = N * (dtype == PROFK_F32 ? 4u : 2u) >= kFiltSparseMinBytes ? kFiltULarge : kFiltUSmall;
+  uint32_t g = cdiv(cdiv(N, epv), kFiltBS * static_cast<uint32_t>(L.filt_u));
   L.G_f = g < 1 ? 1 : (g > maxg ? maxg : g);
   L.seg_cap = M;
   const uint32_t fbmax = static_cast<uint32_t>(num_cus < kFbMaxBlocks ? num_cus : kFbMaxBlocks);

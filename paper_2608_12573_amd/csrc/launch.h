@@ -30,7 +30,13 @@ constexpr int kSampPerBlock = 4 * kSampBS;    // draws per sample block
 constexpr uint32_t kWaveTopMax = 32;          // largest t of the wave-level top-t
 constexpr int kTauBS = 1024;
 constexpr int kFiltBS = 256;                  // threads of a filter block
-constexpr int kFiltU = 8;                     // 16-byte loads in flight per lane
+// 16-byte loads in flight per lane of a filter step: 4 for inputs of at
+// least kFiltSparseMinBytes, 8 for smaller ones.  Measured on one MI355X:
+// 4 loads streamed the 1 GiB inputs 1-3 % faster than 8 (N = 2^28: 161.8
+// against 163.4 us; the BatchTopK shape: 170.6 against 175.2 us), and the
+// 256 MiB inputs about 4 % slower; 2, 12 and 16 were slower everywhere.
+constexpr int kFiltULarge = 4;
+constexpr int kFiltUSmall = 8;
 constexpr int kFiltMaxBlocks = 1024;
 // Filter blocks per CU.  A large input whose survivors are rare streams
 // fastest with two (fewer concurrent streams: about 5 % on a GiB, and a
@@ -71,6 +77,7 @@ constexpr int kBktSortBlocks = 512;           // bucket-sort grid (loops over th
 struct FlatLayout {
   uint32_t G_s = 0, tcap = 0, union_n = 0;    // sampling
   uint32_t G_f = 0;                           // filter blocks
+  int filt_u = 0;                             // 16-byte loads per lane and filter step
   uint32_t seg_cap = 0;                       // entries per candidate segment (= M)
   uint32_t G_fb = 0;                          // fallback blocks (at most)
   size_t off_state = 0, off_segcnt = 0, off_union = 0, off_blk_max = 0;
