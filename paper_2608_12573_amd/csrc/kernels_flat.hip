@@ -226,6 +226,12 @@ __global__ void k_init_state(InitArgs a) {
 
 // ------------------------------------------------------------ stage 4 -----
 constexpr uint32_t kFinCache = 28672;
+// The bucket refinement reads the candidates segment by segment: kPreThreads
+// threads per segment, kPreU keys each per sweep (kPreSeg per segment).
+constexpr uint32_t kPreThreads = kFinBS / kSegs;
+constexpr int kPreU = 8;
+constexpr uint32_t kPreSeg = kPreThreads * kPreU;
+static_assert(kPreThreads * kSegs == kFinBS, "threads per segment");
 constexpr int kFinDigit = 12;
 
 // LDS of the general refinement (radix select over the candidates).
@@ -445,9 +451,9 @@ struct FinishArgs {
 //   3. otherwise run the general radix refinement.
 template <int DT>
 __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh, const uint32_t* seg_pre,
-                                                uint32_t total, SelectScratch& fs) {
+                                                const uint32_t* seg_n, uint32_t total, SelectScratch& fs,
+                                                const uint32_t (&h)[4], const uint32_t (&pk)[kPreU]) {
   constexpr int KB = Elem<DT>::KEYBITS;
-  constexpr int UNR = 16;
   const uint32_t tid = threadIdx.x;
   const uint32_t tau = a.st->tau_key;
   const SegSrc src{a.seg_key, a.seg_idx, a.seg_cap, seg_pre};
@@ -457,12 +463,7 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
   //    [kLogBins - 4(t+1), kLogBins - 4t)
   constexpr uint32_t kOwners = kLogBins / 4;
   static_assert(kLogBins % 4 == 0 && kOwners <= kFinBS, "bucket ownership");
-  uint32_t h[4] = {0u, 0u, 0u, 0u};
-  const uint32_t bbase = kLogBins - 4 * (tid + 1);
-  if (tid < kOwners) {
-    const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
-    h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
-  }
+  const uint32_t bbase = kLogBins - 4 * (tid + 1);  // h: loaded by the caller
   const uint32_t above_me = block_excl_sum<kFinBS>(h[0] + h[1] + h[2] + h[3], fs.wsum, nullptr);
   if (tid < kOwners) {
     uint32_t run = above_me;
@@ -489,24 +490,34 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
   big = block_max<kFinBS>(big, fs.wsum);
 
   if (n_sel <= kFastCap && big <= kFastBucket) {
-    // place (key, candidate number) of buckets >= b* ...
-    for (uint32_t base = 0; base < total; base += kFinBS * UNR) {
-      uint32_t kv[UNR];
+    // place (key, candidate number) of buckets >= b* ...: thread t takes
+    // entries t % kPreThreads + kPreThreads * u of segment t / kPreThreads,
+    // the first kPreU of them already in registers
+    const uint32_t x = tid / kPreThreads, l = tid % kPreThreads;
+    const uint32_t nx = seg_n[x], px = seg_pre[x];
+    auto place = [&](uint32_t j, uint32_t key) {
+      const uint32_t bin = log_bin(key - tau);
+      if (bin >= bstar) {
+        const uint32_t slot = sh.bkt.off[bin] + atomicAdd(&sh.bkt.fill[bin], 1u);
+        sh.bkt.comp[slot] = (static_cast<uint64_t>(key) << 32) | (px + j);
+      }
+    };
 #pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        const uint32_t i = base + u * kFinBS + tid;
-        kv[u] = i < total ? a.seg_key[src.pos(i)] : 0u;
+    for (int u = 0; u < kPreU; ++u) {
+      const uint32_t j = l + kPreThreads * u;
+      if (j < nx) place(j, pk[u]);
+    }
+    for (uint32_t base = kPreSeg; base < nx; base += kPreSeg) {
+      uint32_t kv[kPreU];
+#pragma unroll
+      for (int u = 0; u < kPreU; ++u) {
+        const uint32_t j = base + l + kPreThreads * u;
+        kv[u] = j < nx ? a.seg_key[static_cast<size_t>(x) * a.seg_cap + j] : 0u;
       }
 #pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        const uint32_t i = base + u * kFinBS + tid;
-        if (i < total) {
-          const uint32_t bin = log_bin(kv[u] - tau);
-          if (bin >= bstar) {
-            const uint32_t slot = sh.bkt.off[bin] + atomicAdd(&sh.bkt.fill[bin], 1u);
-            sh.bkt.comp[slot] = (static_cast<uint64_t>(kv[u]) << 32) | i;
-          }
-        }
+      for (int u = 0; u < kPreU; ++u) {
+        const uint32_t j = base + l + kPreThreads * u;
+        if (j < nx) place(j, kv[u]);
       }
     }
     __syncthreads();
@@ -572,6 +583,24 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t tid = threadIdx.x, b = blockIdx.x;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
+  // Block 0 loads the bucket histogram and the first kPreSeg candidate keys
+  // of every segment together with the segment counts, before it knows
+  // them, so the three latencies overlap (reads past a segment's count stay
+  // within its capacity and are ignored).
+  uint32_t h[4] = {0u, 0u, 0u, 0u}, pk[kPreU];
+  if (!a.direct && b == 0) {
+    const uint32_t bbase = kLogBins - 4 * (tid + 1);
+    if (tid < kLogBins / 4) {
+      const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
+      h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
+    }
+    const uint32_t x = tid / kPreThreads, l = tid % kPreThreads;
+#pragma unroll
+    for (int u = 0; u < kPreU; ++u) {
+      const uint32_t j = l + kPreThreads * u;
+      pk[u] = j < a.seg_cap ? a.seg_key[static_cast<size_t>(x) * a.seg_cap + j] : 0u;
+    }
+  }
   if (!a.direct) {
     if (tid < kSegs) seg_n[tid] = a.seg_cnt[tid * kSegStride];
     __syncthreads();
@@ -588,7 +617,7 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
     status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
     if (status == PROFK_STATUS_FILTERED) {
-      if (b == 0) finish_filtered<DT>(a, sh, seg_pre, total, fs);
+      if (b == 0) finish_filtered<DT>(a, sh, seg_pre, seg_n, total, fs, h, pk);
       return;
     }
   }
