@@ -67,6 +67,7 @@ __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
 // tau = t-th largest key of the union.  Used when the union is too large
 // for the filter blocks to select from it themselves.
 constexpr uint32_t kTauCache = 32768;
+constexpr uint32_t kTauList = 2048;  // keys of the bin holding rank t
 
 struct TauArgs {
   const uint32_t* keys;
@@ -82,6 +83,7 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
   __shared__ SelectShared sel;
   __shared__ uint32_t lists[NW][kWaveTopMax];
   __shared__ uint32_t list_n[NW];
+  __shared__ uint32_t tlist[kTauList];
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   if (a.t <= kWaveTopMax && a.n <= static_cast<uint32_t>(kTauBS * E)) {
     // every wave keeps the top t of its share, wave 0 merges the lists
@@ -116,28 +118,59 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
     return;
   }
   auto gload = [&](uint32_t i) { return a.keys[i]; };
+  const bool cached = a.n <= kTauCache;
+  // every key of the union, from LDS when it fits (eight reads per thread
+  // issued before any visitor runs)
+  auto all = [&](auto f) {
+    if (cached) for_items<kTauBS, 8>(a.n, [&](uint32_t i) { return cache[i]; }, [&](uint32_t, uint32_t v) { f(v); });
+    else for_items<kTauBS, 8>(a.n, gload, [&](uint32_t, uint32_t v) { f(v); });
+  };
+  uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+  for_items<kTauBS, 8>(a.n, gload, [&](uint32_t i, uint32_t v) {
+    if (cached) cache[i] = v;
+    mn = min(mn, v);
+    mx = max(mx, v);
+  });
+  // The high bits all keys share need no digit pass, and the first pass
+  // then spreads the keys over its bins instead of piling them into a few.
+  mx = block_max<kTauBS>(mx, sel.wsum);
+  mn = ~block_max<kTauBS>(~mn, sel.wsum);
+  const int nbits = a.keybits - shared_prefix_bits(mn, mx, a.keybits);
   SelectResult r;
-  if (a.n <= kTauCache) {
-    uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-    for_items<kTauBS, 8>(a.n, gload, [&](uint32_t i, uint32_t v) {
-      cache[i] = v;
-      mn = min(mn, v);
-      mx = max(mx, v);
-    });
-    // The high bits all keys share need no digit pass, and the first pass
-    // then spreads the keys over its bins instead of piling them into a few.
-    mx = block_max<kTauBS>(mx, sel.wsum);
-    mn = ~block_max<kTauBS>(~mn, sel.wsum);
-    r = block_select_kth<kTauBS>(
-        [&](auto f) {
-          for (uint32_t i = tid; i < a.n; i += kTauBS) f(cache[i]);
-        },
-        a.t, a.keybits - shared_prefix_bits(mn, mx, a.keybits), mn, sel);
-  } else {
-    r = block_select_kth<kTauBS>(
-        [&](auto f) { for_items<kTauBS, 8>(a.n, gload, [&](uint32_t, uint32_t v) { f(v); }); },
-        a.t, a.keybits, 0u, sel);
+  bool done = false;
+  if (nbits > kSelDigit) {
+    // One digit pass over the whole union finds the bin that holds rank t;
+    // t is a small part of the union, so that bin holds few keys.  They are
+    // copied to a short list and the remaining digits are taken on the list
+    // alone.  A bin too full for the list falls through to the passes below.
+    const int shift = nbits - kSelDigit;
+    const uint32_t hmask = nbits >= 32 ? 0u : ~((1u << nbits) - 1u);
+    const uint32_t pre = mn & hmask;
+    for (uint32_t i = tid; i < static_cast<uint32_t>(kSelBins); i += kTauBS) sel.hist[i] = 0;
+    __syncthreads();
+    all([&](uint32_t v) { hist_add(sel.hist, (v >> shift) & (kSelBins - 1), true); });
+    __syncthreads();
+    if (tid < kWave) rank_bin_search(sel.hist, kSelBins, a.t, sel.scratch());
+    __syncthreads();
+    const uint32_t d = sel.found[0], above = sel.found[1], eq = sel.found[2];
+    if (eq <= kTauList) {
+      if (tid == 0) list_n[0] = 0;
+      __syncthreads();
+      all([&](uint32_t v) {
+        const bool take = ((v >> shift) & (kSelBins - 1)) == d;
+        const uint32_t p = lds_append(&list_n[0], take);
+        if (take) tlist[p] = v;
+      });
+      __syncthreads();
+      r = block_select_kth<kTauBS>(
+          [&](auto f) {
+            for (uint32_t i = tid; i < eq; i += kTauBS) f(tlist[i]);
+          },
+          a.t - above, shift, pre | (d << shift), sel);
+      done = true;
+    }
   }
+  if (!done) r = block_select_kth<kTauBS>(all, a.t, nbits, mn, sel);
   if (tid == 0) a.st->tau_key = r.kth;
 }
 
