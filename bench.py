@@ -123,7 +123,7 @@ def write_counters(fetch_dir, write_dir, bench_json):
             sys.exit("kernel not found in the counter files")
         return max(keys, key=lambda key: table[key][0]) if biggest else keys[0]
 
-    is_filter = lambda n: "k_filter<0, false>" in n
+    is_filter = lambda n: "k_filter<0, false," in n
     is_copy = lambda n: "copyBuffer" in n
     fk, ck = pick(fetch, is_filter), pick(fetch, is_copy, biggest=True)
     wk, cwk = pick(write, is_filter), pick(write, is_copy, biggest=True)
@@ -132,7 +132,7 @@ def write_counters(fetch_dir, write_dir, bench_json):
     fb, wb = fetch[fk][0] * fpu, write[wk][0] * wpu
     algo = line["roofline"]["algorithmic_bytes_per_launch"]
     out = {
-        "kernel": "profk::k_filter<0, false> (fp32 filter-and-compact)",
+        "kernel": "profk::k_filter<0, false, U> (fp32 filter-and-compact)",
         "workload_key": "c2-k1024",
         "workload": line["config"]["workload"] + f"; {line['count']} survivors",
         "commands": [
