@@ -2,8 +2,9 @@
 // compared with the threshold tau and the survivors are compacted into a
 // bounded candidate buffer, counting all of them.
 //
-// k_filter: a persistent grid, one contiguous chunk of the input per
-// workgroup, streamed with 16-byte nontemporal loads.  When the sample union
+// k_filter: a persistent grid streaming the input with 16-byte nontemporal
+// loads; tiles of the input are dealt to the workgroups in turn, so that the
+// survivors of a sorted or clustered input spread over every workgroup.  When the sample union
 // is small every workgroup first selects tau from it itself.  Survivors are
 // staged in LDS and appended to one of eight candidate segments with one
 // atomic per workgroup, because same-address global atomics serialise across
@@ -22,7 +23,7 @@ template <class T> static T* at(uint8_t* ws, size_t off) { return reinterpret_ca
 // ------------------------------------------------------------ stage 3 -----
 struct FilterArgs {
   const void* values;
-  uint32_t n, head, nvec, vpb;
+  uint32_t n, head, nvec;
   uint32_t seg_cap;
   CallState* st;
   const uint32_t* union_keys;  // sample union to select tau from, or null: tau in st
@@ -55,8 +56,12 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   // union arrives at once and tau is chosen while the step is in flight.
   const u32x4* vec = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.values) +
                                                     static_cast<size_t>(a.head) * ES);
-  const uint32_t vbeg = b * a.vpb;
-  const uint32_t vend = min(vbeg + a.vpb, a.nvec);
+  // step s of block b reads tile s * gridDim.x + b (kFiltBS * U vectors);
+  // nvec + the stride stays below 2^32 for every input the C ABI accepts
+  constexpr uint32_t kTile = kFiltBS * U;
+  const uint32_t vbeg = b * kTile;
+  const uint32_t vend = a.nvec;
+  const uint32_t vstride = gridDim.x * kTile;
   constexpr int E = kFiltTauMax / kFiltBS;
   const bool one_wave = a.union_n <= kWave * kFiltTauWave;
   uint32_t uk[E];
@@ -168,7 +173,7 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
     }
   };
 
-  for (uint32_t vb = vbeg; vb < vend; vb += kFiltBS * U) {
+  for (uint32_t vb = vbeg; vb < vend; vb += vstride) {
     if (vb != vbeg) load_step(vb, th.neutral);
     if (__ballot(tile_any<DT, U>(v, th)) == 0) continue;
     // Rare path: per-vector survivor masks, one slot reservation per wave,
@@ -253,9 +258,7 @@ static hipError_t launch_filter_t(const FlatCall& c, CallState* st, const uint32
   uint32_t head = static_cast<uint32_t>(((16 - (addr & 15)) & 15) / ES);
   if (head > c.n) head = c.n;
   const uint32_t nvec = (c.n - head) / EPV;
-  uint32_t vpb = cdiv(nvec, L.G_f);
-  vpb = cdiv(vpb, kFiltBS) * kFiltBS;
-  FilterArgs fa{c.values, c.n, head, nvec, vpb, L.seg_cap, st,
+  FilterArgs fa{c.values, c.n, head, nvec, L.seg_cap, st,
                 union_keys, union_keys ? L.union_n : 0u, static_cast<uint32_t>(c.plan->t),
                 at<uint32_t>(c.ws, L.off_segcnt), at<uint32_t>(c.ws, L.off_seg_key),
                 at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max),
