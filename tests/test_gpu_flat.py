@@ -230,3 +230,31 @@ def test_config3_adversarial_2p26(name):
     rec, ref = _f32_case(x, 512, 0)
     if name == "plateau_wide":
         assert ref.status == oprofk.STATUS_OVERFLOW
+
+
+# ------------------------------------------------------- sorted inputs ----
+# The filter deals tiles of the input to its workgroups in turn, so the
+# survivors of a sorted input sit in the first or last tiles: a few
+# workgroups hold them all, at either end of the grid, next to the ragged
+# head and tail outside the 16-byte vectors.
+@pytest.mark.parametrize("descending", [False, True])
+@pytest.mark.parametrize("k", [100, 4096])
+@pytest.mark.parametrize("offset", [0, 3])
+def test_sorted_f32_unaligned(descending, k, offset):
+    n = 3 * (1 << 20) + 7
+    x = workloads.ramp_f32(n)
+    if descending:
+        x = x[::-1].copy()
+    rec, ref = _f32_case(x, k, 5, offset=offset)
+    assert ref.status == oprofk.STATUS_FILTERED
+
+
+@pytest.mark.parametrize("descending", [False, True])
+def test_sorted_bf16_unaligned(descending):
+    # a ramp of fp32 in (0, 1] rounded to bf16: runs of equal values, the
+    # top one (1.0) about 4096 long, so the k-th key is cut in index order
+    n = (1 << 22) + 5
+    b = workloads.f32_to_bf16_bits(((np.arange(n, dtype=np.float64) + 1) / n).astype(np.float32))
+    if descending:
+        b = b[::-1].copy()
+    _bf16_case(b, 1000, 6, offset=1)
