@@ -144,6 +144,27 @@ int profk_topk(const profk_plan_t* plan, int32_t dtype, const void* values,
                int64_t* out_idx, void* ws, size_t ws_bytes, void* stream,
                profk_info_t* info_dev);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * profk_topk with the workspace taken from a fixed device array of
+ * PROFK_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on,
+ * until the process ends.  The call allocates nothing and frees nothing; the
+ * caller still provides values, out_vals, out_idx and (optionally) info_dev
+ * on the current device, and `stream` must belong to that device.
+ *   Limit: profk_workspace_size(plan, dtype, 1) <= PROFK_NOALLOC_SCRATCH_BYTES
+ *     (16 MiB: every k <= 4096 for N <= 2^28), else PROFK_EWORKSPACE and
+ *     nothing is enqueued.
+ *   Sharing: every call on one GPU uses that GPU's one array, and each call
+ *     initialises the parts it reads, so consecutive calls on one stream are
+ *     safe; calls that overlap on one GPU (other streams, other threads
+ *     without ordering) race on the array and give wrong results.
+ *   Other arguments, results and errors as profk_topk; a failed lookup of
+ *     the array's device address returns PROFK_EHIP. */
+#define PROFK_NOALLOC_SCRATCH_BYTES (16u << 20)
+int profk_topk_noalloc(const profk_plan_t* plan, int32_t dtype, const void* values,
+                       int64_t N, int64_t k, uint64_t seed, void* out_vals,
+                       int64_t* out_idx, void* stream, profk_info_t* info_dev);
+
 /* The short form: fp32, eps = 1e-6, recall 1, the null stream, a workspace
  * held by the library (released by profk_release), synchronous. */
 int profk_topk_simple(const float* values, int64_t N, int64_t k, uint64_t seed,

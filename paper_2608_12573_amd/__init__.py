@@ -26,6 +26,7 @@ MODE_FILTER, MODE_DIRECT = 0, 1
 FORCE_AUTO, FORCE_FILTER, FORCE_DIRECT = 0, 1, 2
 STATUS_FILTERED, STATUS_UNDERFLOW, STATUS_OVERFLOW, STATUS_DIRECT = 0, 1, 2, 3
 OK, EINVAL, EDTYPE, EWORKSPACE, ENULL, EHIP = 0, -1, -2, -3, -4, -5
+NOALLOC_SCRATCH_BYTES = 16 << 20   # PROFK_NOALLOC_SCRATCH_BYTES of include/profk.h
 
 
 class PlanOpts(ctypes.Structure):
@@ -87,6 +88,7 @@ def lib():
         L.profk_topk.argtypes = [P(Plan), i32, vp, i64, i64, u64, vp, vp, vp, ctypes.c_size_t, vp, vp]
         L.profk_topk_tau.argtypes = [P(Plan), i32, vp, i64, i64, u32, vp, vp, vp, ctypes.c_size_t, vp, vp]
         L.profk_topk_simple.argtypes = [vp, i64, i64, u64, vp, vp]
+        L.profk_topk_noalloc.argtypes = [P(Plan), i32, vp, i64, i64, u64, vp, vp, vp, vp]
         L.profk_topk_rows.argtypes = [P(Plan), i32, vp, i64, i64, i64, i64, u64, vp, vp, vp,
                                       ctypes.c_size_t, vp, vp]
         L.profk_batchtopk.argtypes = [P(Plan), i32, vp, i64, i64, i64, u64, vp, vp, vp,
@@ -215,6 +217,24 @@ def topk(x, k, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None, info=Non
     info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
     _check(lib().profk_topk(ctypes.byref(p), dt, _ptr(x), N, k, seed, _ptr(out[0]), _ptr(out[1]),
                             _ptr(ws), ws.numel(), _stream(), _ptr(info)))
+    return out[0], out[1], info
+
+
+def topk_noalloc(x, k, eps=1e-6, recall=1.0, seed=0, p=None, out=None, info=None):
+    """profk_topk_noalloc: topk with the library's fixed per-GPU scratch as
+    the workspace (no device allocation by the library)."""
+    torch = _torch()
+    if x.dim() != 1 or not x.is_cuda:
+        raise ProfkError("x must be a 1-D CUDA tensor")
+    dt = _dtype_code(x)
+    N = x.numel()
+    p = p if p is not None else plan(N, k, eps, recall)
+    if out is None:
+        out = (torch.empty(k, dtype=x.dtype, device=x.device),
+               torch.empty(k, dtype=torch.int64, device=x.device))
+    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    _check(lib().profk_topk_noalloc(ctypes.byref(p), dt, _ptr(x), N, k, seed, _ptr(out[0]), _ptr(out[1]),
+                                    _stream(), _ptr(info)))
     return out[0], out[1], info
 
 

@@ -278,6 +278,52 @@ int profk_debug_filter(const profk_plan_t* plan, int32_t dtype, const void* valu
   return e == hipSuccess ? PROFK_OK : hip_fail(e);
 }
 
+// ---- Entry point that allocates nothing ----
+//
+// profk_topk_noalloc runs profk_topk's kernels on a fixed device array
+// instead of a caller's workspace.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address is looked up once per
+// device with hipGetSymbolAddress and only that address is passed on.
+static __device__ __align__(256) uint8_t scratch[PROFK_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up on the first call on
+// that device (with it current); NULL with *err set when the lookup fails.
+void* device_scratch(hipError_t* err) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) { *err = e; return nullptr; }
+  if (dev < 0 || dev >= kMaxDevices) { *err = hipErrorInvalidDevice; return nullptr; }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) { *err = e != hipSuccess ? e : hipErrorInvalidSymbol; return nullptr; }
+    g_scratch_dev[dev] = ptr;
+  }
+  return g_scratch_dev[dev];
+}
+}  // namespace
+
+int profk_topk_noalloc(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t N, int64_t k,
+                       uint64_t seed, void* out_vals, int64_t* out_idx, void* stream, profk_info_t* info_dev) {
+  if (!plan || !values || !out_vals || !out_idx) return PROFK_ENULL;
+  if (!dtype_ok(dtype)) return PROFK_EDTYPE;
+  if (!plan_consistent(plan) || plan->N != N || plan->k != k) return PROFK_EINVAL;
+  const size_t need = profk_workspace_size(plan, dtype, 1);
+  if (need == 0) return PROFK_EINVAL;
+  if (need > static_cast<size_t>(PROFK_NOALLOC_SCRATCH_BYTES)) return PROFK_EWORKSPACE;
+  hipError_t e = hipSuccess;
+  void* ws = device_scratch(&e);
+  if (!ws) return hip_fail(e);
+  return run_flat(plan, dtype, values, N, k, seed, 0, out_vals, out_idx, ws, PROFK_NOALLOC_SCRATCH_BYTES,
+                  stream, info_dev, 0, 0);
+}
+
 namespace {
 std::mutex g_simple_mu;
 void* g_simple_ws = nullptr;
