@@ -202,37 +202,108 @@ def read_info(info_tensor):
     return np.frombuffer(raw, dtype=INFO_DTYPE)
 
 
+def _on_device(t, name, device):
+    """t must be a CUDA tensor on `device` (checked after its layout, so that
+    every layout rule is reported the same way with or without a GPU)."""
+    if not t.is_cuda:
+        raise ProfkError(f"{name} must be a CUDA tensor (got device {t.device})")
+    if device is not None and t.device != device:
+        raise ProfkError(f"{name} is on {t.device}, the input on {device}")
+
+
+def _input(x, name, dims, dtypes=(F32, BF16), layout="contiguous"):
+    """Checks an input tensor: rank, dtype, memory layout, then device.
+    layout: "contiguous", or "rows" (unit column stride, rows at any
+    stride at least D apart)."""
+    torch = _torch()
+    if not isinstance(x, torch.Tensor):
+        raise ProfkError(f"{name} must be a torch tensor")
+    if x.dim() != dims:
+        raise ProfkError(f"{name} must have {dims} dimension(s), got shape {tuple(x.shape)}")
+    dt = _dtype_code(x)
+    if dt not in dtypes:
+        raise ProfkError(f"{name} must be {' or '.join('float32' if d == F32 else 'bfloat16' for d in dtypes)}")
+    if layout == "contiguous" and not x.is_contiguous():
+        raise ProfkError(f"{name} must be contiguous (strides {tuple(x.stride())})")
+    if layout == "rows" and (x.stride(1) != 1 or (x.shape[0] > 1 and x.stride(0) < x.shape[1])):
+        raise ProfkError(f"{name} must be [B, D] with unit column stride and rows at least D apart "
+                         f"(strides {tuple(x.stride())})")
+    _on_device(x, name, None)
+    return dt
+
+
+def _buffer(t, name, dtype, numel, device):
+    """A caller-given output: the dtype, at least `numel` contiguous
+    elements, on the input's device."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise ProfkError(f"{name} must be a torch tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ProfkError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous() or t.numel() < numel:
+        raise ProfkError(f"{name} must be contiguous with at least {numel} elements")
+    _on_device(t, name, device)
+
+
+def _bytes_buffer(t, name, nbytes, device):
+    """A caller-given workspace or report buffer of at least nbytes bytes."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_contiguous():
+        raise ProfkError(f"{name} must be a contiguous torch tensor")
+    if t.numel() * t.element_size() < nbytes:
+        raise ProfkError(f"{name} holds {t.numel() * t.element_size()} bytes, {nbytes} needed")
+    _on_device(t, name, device)
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def _outputs(x, n, out, info, n_info):
+    """Preallocated or new (values, int64 indices) and info for n results."""
+    torch = _torch()
+    if out is None:
+        out = (torch.empty(n, dtype=x.dtype, device=x.device),
+               torch.empty(n, dtype=torch.int64, device=x.device))
+    else:
+        _buffer(out[0], "out[0]", x.dtype, n, x.device)
+        _buffer(out[1], "out[1]", torch.int64, n, x.device)
+    if info is None:
+        info = torch.empty(n_info * INFO_BYTES, dtype=torch.uint8, device=x.device)
+    else:
+        _bytes_buffer(info, "info", n_info * INFO_BYTES, x.device)
+    return out, info
+
+
+def _workspace_for(p, dt, batch, ws, device):
+    need = workspace_size(p, dt, batch)
+    if need == 0:
+        raise ProfkError("the plan does not fit this call (N, k or dtype)")
+    if ws is None:
+        return workspace(p, dt, batch, device)
+    _bytes_buffer(ws, "ws", need, device)
+    return ws
+
+
 def topk(x, k, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None, info=None):
     """Top-k of a 1-D fp32/bf16 CUDA tensor: (values, int64 indices, info)."""
-    torch = _torch()
-    if x.dim() != 1 or not x.is_cuda:
-        raise ProfkError("x must be a 1-D CUDA tensor")
-    dt = _dtype_code(x)
+    dt = _input(x, "x", 1)
     N = x.numel()
     p = p if p is not None else plan(N, k, eps, recall)
-    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
-    if out is None:
-        out = (torch.empty(k, dtype=x.dtype, device=x.device),
-               torch.empty(k, dtype=torch.int64, device=x.device))
-    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    ws = _workspace_for(p, dt, 1, ws, x.device)
+    out, info = _outputs(x, k, out, info, 1)
     _check(lib().profk_topk(ctypes.byref(p), dt, _ptr(x), N, k, seed, _ptr(out[0]), _ptr(out[1]),
-                            _ptr(ws), ws.numel(), _stream(), _ptr(info)))
+                            _ptr(ws), _nbytes(ws), _stream(), _ptr(info)))
     return out[0], out[1], info
 
 
 def topk_noalloc(x, k, eps=1e-6, recall=1.0, seed=0, p=None, out=None, info=None):
     """profk_topk_noalloc: topk with the library's fixed per-GPU scratch as
     the workspace (no device allocation by the library)."""
-    torch = _torch()
-    if x.dim() != 1 or not x.is_cuda:
-        raise ProfkError("x must be a 1-D CUDA tensor")
-    dt = _dtype_code(x)
+    dt = _input(x, "x", 1)
     N = x.numel()
     p = p if p is not None else plan(N, k, eps, recall)
-    if out is None:
-        out = (torch.empty(k, dtype=x.dtype, device=x.device),
-               torch.empty(k, dtype=torch.int64, device=x.device))
-    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    out, info = _outputs(x, k, out, info, 1)
     _check(lib().profk_topk_noalloc(ctypes.byref(p), dt, _ptr(x), N, k, seed, _ptr(out[0]), _ptr(out[1]),
                                     _stream(), _ptr(info)))
     return out[0], out[1], info
@@ -241,68 +312,54 @@ def topk_noalloc(x, k, eps=1e-6, recall=1.0, seed=0, p=None, out=None, info=None
 def topk_tau(x, k, tau_key, p, ws=None, eps=1e-6):
     """profk_topk_tau: the pipeline with the threshold given (forces the
     fallback paths on purpose)."""
-    torch = _torch()
-    dt = _dtype_code(x)
+    dt = _input(x, "x", 1)
     N = x.numel()
-    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
-    vals = torch.empty(k, dtype=x.dtype, device=x.device)
-    idx = torch.empty(k, dtype=torch.int64, device=x.device)
-    info = torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    ws = _workspace_for(p, dt, 1, ws, x.device)
+    (vals, idx), info = _outputs(x, k, None, None, 1)
     _check(lib().profk_topk_tau(ctypes.byref(p), dt, _ptr(x), N, k, tau_key, _ptr(vals), _ptr(idx),
-                                _ptr(ws), ws.numel(), _stream(), _ptr(info)))
+                                _ptr(ws), _nbytes(ws), _stream(), _ptr(info)))
     return vals, idx, info
 
 
 def topk_simple(x, k, seed=0):
-    torch = _torch()
-    vals = torch.empty(k, dtype=torch.float32, device=x.device)
-    idx = torch.empty(k, dtype=torch.int64, device=x.device)
+    """profk_topk_simple: fp32 only, synchronous, library-held workspace."""
+    _input(x, "x", 1, dtypes=(F32,))
+    (vals, idx), _ = _outputs(x, k, None, None, 1)
     _check(lib().profk_topk_simple(_ptr(x), x.numel(), k, seed, _ptr(vals), _ptr(idx)))
     return vals, idx
 
 
 def topk_rows(x, k, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None, info=None):
     """Per-row top-k of a [B, D] CUDA tensor (rows may be strided)."""
-    torch = _torch()
-    if x.dim() != 2 or x.stride(1) != 1:
-        raise ProfkError("x must be [B, D] with unit column stride")
-    dt = _dtype_code(x)
+    dt = _input(x, "x", 2, layout="rows")
     B, D = x.shape
     p = p if p is not None else plan_rows(D, k, eps, recall)
-    ws = ws if ws is not None else workspace(p, dt, B, x.device)
-    if out is None:
-        out = (torch.empty((B, k), dtype=x.dtype, device=x.device),
-               torch.empty((B, k), dtype=torch.int64, device=x.device))
-    info = info if info is not None else torch.empty(B * INFO_BYTES, dtype=torch.uint8, device=x.device)
+    ws = _workspace_for(p, dt, B, ws, x.device)
+    out, info = _outputs(x, B * k, out, info, B)
     _check(lib().profk_topk_rows(ctypes.byref(p), dt, _ptr(x), B, D, x.stride(0), k, seed,
-                                 _ptr(out[0]), _ptr(out[1]), _ptr(ws), ws.numel(), _stream(),
+                                 _ptr(out[0]), _ptr(out[1]), _ptr(ws), _nbytes(ws), _stream(),
                                  _ptr(info)))
-    return out[0], out[1], info
+    return out[0].view(B, k), out[1].view(B, k), info
 
 
 def batchtopk(x, k_row, eps=1e-6, recall=1.0, seed=0, p=None, ws=None, out=None, info=None):
     """BatchTopK: the B*k_row largest entries of a contiguous [B, D] tensor,
     with flat indices row*D + col."""
-    torch = _torch()
-    if x.dim() != 2 or not x.is_contiguous():
-        raise ProfkError("x must be a contiguous [B, D] tensor")
-    dt = _dtype_code(x)
+    dt = _input(x, "x", 2)
     B, D = x.shape
     K = B * k_row
     p = p if p is not None else plan(B * D, K, eps, recall)
-    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
-    if out is None:
-        out = (torch.empty(K, dtype=x.dtype, device=x.device),
-               torch.empty(K, dtype=torch.int64, device=x.device))
-    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    ws = _workspace_for(p, dt, 1, ws, x.device)
+    out, info = _outputs(x, K, out, info, 1)
     _check(lib().profk_batchtopk(ctypes.byref(p), dt, _ptr(x), B, D, k_row, seed, _ptr(out[0]),
-                                 _ptr(out[1]), _ptr(ws), ws.numel(), _stream(), _ptr(info)))
+                                 _ptr(out[1]), _ptr(ws), _nbytes(ws), _stream(), _ptr(info)))
     return out[0], out[1], info
 
 
 def debug_sample_indices(seed, row, S, N, device="cuda"):
     torch = _torch()
     out = torch.empty(S, dtype=torch.int64, device=device)
+    _on_device(out, "out", None)
     _check(lib().profk_debug_sample_indices(seed, row, S, N, _ptr(out), _stream()))
     return out
 
@@ -310,13 +367,13 @@ def debug_sample_indices(seed, row, S, N, device="cuda"):
 def debug_filter(x, tau_key, p, ws=None):
     """Stage 3 alone: (buffer keys, buffer indices, count) for a given tau."""
     torch = _torch()
-    dt = _dtype_code(x)
-    ws = ws if ws is not None else workspace(p, dt, 1, x.device)
+    dt = _input(x, "x", 1)
+    ws = _workspace_for(p, dt, 1, ws, x.device)
     bk = torch.empty(p.M, dtype=torch.int32, device=x.device)
     bi = torch.empty(p.M, dtype=torch.int32, device=x.device)
     cnt = torch.empty(1, dtype=torch.int32, device=x.device)
     _check(lib().profk_debug_filter(ctypes.byref(p), dt, _ptr(x), x.numel(), tau_key, _ptr(bk), _ptr(bi),
-                                    _ptr(cnt), _ptr(ws), ws.numel(), _stream()))
+                                    _ptr(cnt), _ptr(ws), _nbytes(ws), _stream()))
     return bk, bi, cnt
 
 
@@ -330,6 +387,9 @@ def _sae_shape(x, w_enc, b_enc):
         raise ProfkError("x and w_enc must be bfloat16, b_enc float32")
     if not (x.is_contiguous() and w_enc.is_contiguous() and b_enc.is_contiguous()):
         raise ProfkError("x, w_enc and b_enc must be contiguous")
+    _on_device(x, "x", None)
+    _on_device(w_enc, "w_enc", x.device)
+    _on_device(b_enc, "b_enc", x.device)
     return x.shape[0], x.shape[1], w_enc.shape[0]
 
 
@@ -349,13 +409,22 @@ def sae_encode_topk(x, w_enc, b_enc, k_row, eps=1e-6, recall=1.0, seed=0, p=None
     B, d_model, d_dict = _sae_shape(x, w_enc, b_enc)
     K = B * k_row
     p = p if p is not None else plan_sae(B, d_dict, k_row, eps, recall)
-    ws = ws if ws is not None else sae_workspace(p, B, d_dict, x.device)
+    if ws is None:
+        ws = sae_workspace(p, B, d_dict, x.device)
+    else:
+        _bytes_buffer(ws, "ws", int(lib().profk_sae_workspace_size(ctypes.byref(p), B, d_dict)), x.device)
     if out is None:
         out = (torch.empty(K, dtype=torch.float32, device=x.device),
                torch.empty(K, dtype=torch.int64, device=x.device))
-    info = info if info is not None else torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    else:
+        _buffer(out[0], "out[0]", torch.float32, K, x.device)
+        _buffer(out[1], "out[1]", torch.int64, K, x.device)
+    if info is None:
+        info = torch.empty(INFO_BYTES, dtype=torch.uint8, device=x.device)
+    else:
+        _bytes_buffer(info, "info", INFO_BYTES, x.device)
     _check(lib().profk_sae_encode_topk(ctypes.byref(p), _ptr(x), _ptr(w_enc), _ptr(b_enc), B, d_model, d_dict,
-                                       k_row, seed, _ptr(out[0]), _ptr(out[1]), _ptr(ws), ws.numel(),
+                                       k_row, seed, _ptr(out[0]), _ptr(out[1]), _ptr(ws), _nbytes(ws),
                                        _stream(), _ptr(info)))
     return out[0], out[1], info
 
@@ -364,7 +433,10 @@ def sae_encode_dense(x, w_enc, b_enc, out=None):
     """The latent matrix relu(x w_enc^T + b_enc), fp32 [B, d_dict]."""
     torch = _torch()
     B, d_model, d_dict = _sae_shape(x, w_enc, b_enc)
-    out = out if out is not None else torch.empty((B, d_dict), dtype=torch.float32, device=x.device)
+    if out is None:
+        out = torch.empty((B, d_dict), dtype=torch.float32, device=x.device)
+    else:
+        _buffer(out, "out", torch.float32, B * d_dict, x.device)
     _check(lib().profk_sae_encode_dense(_ptr(x), _ptr(w_enc), _ptr(b_enc), B, d_model, d_dict, _ptr(out),
                                         _stream()))
     return out
@@ -378,11 +450,23 @@ def sae_decode(vals, flat_idx, w_dec, b_dec, B, out=None, ws=None):
     if w_dec.dtype != torch.bfloat16 or b_dec.dtype != torch.float32 or vals.dtype != torch.float32 or \
             flat_idx.dtype != torch.int64 or flat_idx.numel() != K:
         raise ProfkError("vals fp32 [K], flat_idx int64 [K], w_dec bf16 [d_dict, d_model], b_dec fp32 [d_model]")
-    out = out if out is not None else torch.empty((B, d_model), dtype=torch.float32, device=vals.device)
+    if not (vals.is_contiguous() and flat_idx.is_contiguous() and w_dec.is_contiguous() and b_dec.is_contiguous()):
+        raise ProfkError("vals, flat_idx, w_dec and b_dec must be contiguous")
+    if b_dec.numel() != d_model:
+        raise ProfkError("b_dec must hold d_model values")
+    for t, name in ((vals, "vals"), (flat_idx, "flat_idx"), (w_dec, "w_dec"), (b_dec, "b_dec")):
+        _on_device(t, name, None if name == "vals" else vals.device)
+    if out is None:
+        out = torch.empty((B, d_model), dtype=torch.float32, device=vals.device)
+    else:
+        _buffer(out, "out", torch.float32, B * d_model, vals.device)
     n = int(lib().profk_sae_decode_workspace_size(B, K))
-    ws = ws if ws is not None else torch.empty(max(n, 1), dtype=torch.uint8, device=vals.device)
+    if ws is None:
+        ws = torch.empty(max(n, 1), dtype=torch.uint8, device=vals.device)
+    else:
+        _bytes_buffer(ws, "ws", n, vals.device)
     _check(lib().profk_sae_decode(_ptr(vals), _ptr(flat_idx), K, _ptr(w_dec), _ptr(b_dec), B, d_model, d_dict,
-                                  _ptr(out), _ptr(ws), ws.numel(), _stream()))
+                                  _ptr(out), _ptr(ws), _nbytes(ws), _stream()))
     return out
 
 
@@ -390,9 +474,12 @@ def debug_sae_sample(x, w_enc, b_enc, p, seed=0, ws=None):
     """The keys of the S latents the fused path samples (uint32 as int64)."""
     torch = _torch()
     B, d_model, d_dict = _sae_shape(x, w_enc, b_enc)
-    ws = ws if ws is not None else sae_workspace(p, B, d_dict, x.device)
+    if ws is None:
+        ws = sae_workspace(p, B, d_dict, x.device)
+    else:
+        _bytes_buffer(ws, "ws", int(lib().profk_sae_workspace_size(ctypes.byref(p), B, d_dict)), x.device)
     keys = torch.empty(p.S, dtype=torch.int32, device=x.device)
     _check(lib().profk_debug_sae_sample(ctypes.byref(p), _ptr(x), _ptr(w_enc), _ptr(b_enc), B, d_model, d_dict,
-                                        seed, _ptr(keys), _ptr(ws), ws.numel(), _stream()))
+                                        seed, _ptr(keys), _ptr(ws), _nbytes(ws), _stream()))
     return keys.to(torch.int64) & 0xFFFFFFFF
 
