@@ -19,7 +19,9 @@ Readings taken where the paper is silent or inconsistent
     that land among the m highest-ranked elements is exactly Bin(S, m/N), so
         Pr(R < k_req) = Pr(Bin(S, (k_req-1)/N) >= t)
         Pr(R > M)     = Pr(Bin(S, M/N) <= t-1)
-    hold exactly for distinct values (ties only raise R).
+    hold exactly for distinct values (ties only raise R).  Lemma 1's law of
+    R under sampling without replacement is kept below (rank_pmf_wo and the
+    *_wo tails) to check that these binomial tails bound it.
   * S comes from Algorithm 1.  t and M are the smallest integers that meet
     eps_A and eps_B under those exact tails, because the Gaussian forms of
     eq. t_choice and Corollary 1 under-provision M by orders of magnitude at
@@ -43,7 +45,8 @@ Readings taken where the paper is silent or inconsistent
 import math
 from dataclasses import dataclass
 
-from scipy.stats import binom, norm
+from scipy.special import gammaln
+from scipy.stats import binom, hypergeom, norm
 
 MODE_FILTER = 0
 MODE_DIRECT = 1
@@ -114,6 +117,46 @@ def p_underflow(S, t, N, k_req):
 def p_overflow(S, t, N, M):
     """Pr(R > M) = Pr(Bin(S, M/N) <= t-1)."""
     return float(binom.cdf(t - 1, S, M / N))
+
+
+# ---- Lemma 1: the threshold rank under sampling without replacement ----
+# The planner draws i.i.d. (with replacement); these are the paper's own
+# distribution, kept to compare the two sampling schemes.
+
+def _log_comb(n, r):
+    return gammaln(n + 1) - gammaln(r + 1) - gammaln(n - r + 1)
+
+
+def rank_pmf_wo(r, N, S, t):
+    """Lemma 1, eq. (nhg_pmf): Pr(R = r) for the t-th largest of S indices
+    drawn without replacement, rank 1 the largest, r in [t, N - S + t]:
+    C(r-1, t-1) C(N-r, S-t) / C(N, S)."""
+    if r < t or r > N - S + t:
+        return 0.0
+    return float(math.exp(_log_comb(r - 1, t - 1) + _log_comb(N - r, S - t) - _log_comb(N, S)))
+
+
+def rank_mean_wo(N, S, t):
+    """Lemma 1, eq. (nhg_mean_var): E[R] = (N + 1) t / (S + 1)."""
+    return (N + 1) * t / (S + 1)
+
+
+def rank_var_wo(N, S, t):
+    """Lemma 1, eq. (nhg_mean_var):
+    Var(R) = t (S - t + 1) (N + 1) (N - S) / ((S + 1)^2 (S + 2))."""
+    return t * (S - t + 1) * (N + 1) * (N - S) / ((S + 1) ** 2 * (S + 2))
+
+
+def p_underflow_wo(S, t, N, k_req):
+    """Pr(R < k_req) without replacement: at least t of the S draws land
+    among the k_req - 1 highest ranks (a hypergeometric tail)."""
+    return float(hypergeom.sf(t - 1, N, k_req - 1, S))
+
+
+def p_overflow_wo(S, t, N, M):
+    """Pr(R > M) without replacement: fewer than t draws among the M
+    highest ranks."""
+    return float(hypergeom.cdf(t - 1, N, M, S))
 
 
 def _min_int(lo, hi, ok):

@@ -101,3 +101,28 @@ def test_decode_is_linear_and_skips_padding():
     assert np.array_equal(b0, np.tile(m["b_dec"].astype(np.float64), (3, 1)))
     s = sae.decode_scale(np.r_[v1, v2], np.r_[i1, i2], m["w_dec"], m["b_dec"], 3)
     assert np.all(np.abs(both) <= s * (1 + 1e-12))
+
+
+def test_decode_scale_matches_loops_on_a_tiny_layer():
+    """decode_scale written out: for each row, sum over its selected
+    latents of |v| |W_dec[j, c]|, plus |b_dec[c]|.  Values and weights of
+    both signs, a padding entry, and a row with no latent."""
+    B, d_model, d_dict = 4, 6, 9
+    m = workloads.sae_model(B=B, d_model=d_model, d_dict=d_dict, seed=7)
+    g = np.random.default_rng(8)
+    idx = np.array([0 * 9 + 2, 0 * 9 + 7, 1 * 9 + 0, 2 * 9 + 5, 2 * 9 + 1, 2 * 9 + 8, -1], dtype=np.int64)
+    vals = g.standard_normal(idx.size) * 3.0
+    b_dec = g.standard_normal(d_model).astype(np.float32)
+    w = sae.bf16_to_f64(m["w_dec"])
+    assert (w < 0).any() and (vals < 0).any() and (b_dec < 0).any()
+    s = sae.decode_scale(vals, idx, m["w_dec"], b_dec, B)
+    for r in range(B):
+        for c in range(d_model):
+            mag = abs(float(b_dec[c]))
+            for v, f in zip(vals, idx):
+                if f < 0 or int(f) // d_dict != r:
+                    continue
+                mag += abs(v) * abs(w[int(f) % d_dict, c])
+            assert s[r, c] == pytest.approx(mag, rel=1e-15, abs=0.0), (r, c)
+    # row 3 holds no latent: only the bias magnitude
+    assert np.array_equal(s[3], np.abs(b_dec.astype(np.float64)))
