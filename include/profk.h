@@ -131,7 +131,9 @@ int profk_plan_rows(int64_t D, int64_t k, double eps, double recall,
 /* Device workspace in bytes for `batch` independent vectors under `plan`
  * (batch = 1 for profk_topk and profk_batchtopk, B for profk_topk_rows).
  * It holds the sample keys, the candidate buffer, counters and the scratch
- * of the exact fallback: O(S + M + k) bytes per vector, never O(N).
+ * of the exact fallback: O(S + M + k) bytes per vector, never O(N).  For
+ * profk_topk_rows it is a token 256 bytes when the row plan fits the
+ * one-workgroup row kernel, else one row's vector workspace.
  * Returns 0 when the plan or dtype is invalid. */
 size_t profk_workspace_size(const profk_plan_t* plan, int32_t dtype, int64_t batch);
 
@@ -175,10 +177,15 @@ int profk_topk_simple(const float* values, int64_t N, int64_t k, uint64_t seed,
  * draws its own sample (Philox counter word 1 = r) and falls back on its
  * own.  out_vals[B, k] and out_idx[B, k] (column indices) are contiguous.
  * `row_plan` comes from profk_plan_rows(D, k, ...).  info_dev is NULL or an
- * array of B reports.  One workgroup handles a row entirely in LDS, so `ws`
- * is not used (NULL, 0 are accepted).  Limits: k <= 1024 and a plan whose
- * sample and buffer fit the row block's LDS (4*max(S, M) + 4*M + 16*k
- * bytes plus about 14 KiB, within 144 KiB; PROFK_EINVAL otherwise). */
+ * array of B reports.
+ *   Plans with k <= 1024 whose sample and buffer fit one workgroup's LDS
+ *   (4*max(S, M) + 4*M + 16*k bytes plus about 14 KiB, within 144 KiB) run
+ *   one workgroup per row entirely in LDS; `ws` is then not used (NULL, 0
+ *   are accepted).  Any other plan (wider rows, larger k) runs the vector
+ *   path of profk_topk on each row in turn, on `stream`, with the same
+ *   per-row sample stream and result; `ws` must then hold
+ *   profk_workspace_size(row_plan, dtype, B) bytes (one row's workspace,
+ *   reused by every row), else PROFK_ENULL or PROFK_EWORKSPACE. */
 int profk_topk_rows(const profk_plan_t* row_plan, int32_t dtype,
                     const void* values, int64_t B, int64_t D,
                     int64_t row_stride, int64_t k, uint64_t seed,

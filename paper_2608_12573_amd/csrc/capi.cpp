@@ -59,6 +59,16 @@ int run_flat(const profk_plan_t* plan, int32_t dtype, const void* values, int64_
   return e == hipSuccess ? PROFK_OK : hip_fail(e);
 }
 
+// Row plans the one-workgroup row kernel takes: k within its collect limit
+// and the sample, buffer and refinement within its LDS budget.  The buffer
+// alone takes 4*M bytes (and a large sample 4*S), so larger plans are
+// refused before row_layout's 32-bit sums could wrap.
+bool rows_fit_block(const profk_plan_t* p, int32_t dtype) {
+  constexpr int64_t kMaxWords = profk::kRowMaxLds / 4;
+  return p->k <= profk::kRowMaxK && p->M <= kMaxWords && p->S <= kMaxWords &&
+         profk::row_layout(*p, dtype).bytes <= profk::kRowMaxLds;
+}
+
 int check_sae_shape(const void* x, const void* w_enc, const float* b_enc, int64_t B, int64_t d_model,
                     int64_t d_dict) {
   if (!x || !w_enc || !b_enc) return PROFK_ENULL;
@@ -120,7 +130,9 @@ int profk_plan_rows(int64_t D, int64_t k, double eps, double recall, const profk
 
 size_t profk_workspace_size(const profk_plan_t* plan, int32_t dtype, int64_t batch) {
   if (!plan || !dtype_ok(dtype) || !plan_consistent(plan) || batch < 1) return 0;
-  if (batch > 1) return 256;  // the per-row kernel keeps everything in LDS
+  // The one-workgroup row kernel keeps everything in LDS; rows outside its
+  // envelope run the vector kernels one row after another on one workspace.
+  if (batch > 1 && rows_fit_block(plan, dtype)) return 256;
   return profk::flat_layout(*plan, dtype, profk::device_cu_count()).bytes;
 }
 
@@ -235,16 +247,32 @@ int profk_sae_decode(const float* vals, const int64_t* flat_idx, int64_t K, cons
 int profk_topk_rows(const profk_plan_t* plan, int32_t dtype, const void* values, int64_t B, int64_t D,
                     int64_t row_stride, int64_t k, uint64_t seed, void* out_vals, int64_t* out_idx,
                     void* ws, size_t ws_bytes, void* stream, profk_info_t* info_dev) {
-  (void)ws;
-  (void)ws_bytes;
   if (!plan || !values || !out_vals || !out_idx) return PROFK_ENULL;
   if (!dtype_ok(dtype)) return PROFK_EDTYPE;
   if (!plan_consistent(plan) || plan->N != D || plan->k != k) return PROFK_EINVAL;
-  if (B < 1 || B > static_cast<int64_t>(INT32_MAX) || row_stride < D || k > profk::kRowMaxK)
-    return PROFK_EINVAL;
+  if (B < 1 || B > static_cast<int64_t>(INT32_MAX) || row_stride < D) return PROFK_EINVAL;
   if (reinterpret_cast<uintptr_t>(values) % elem_size(dtype) != 0) return PROFK_EINVAL;
+  if (!rows_fit_block(plan, dtype)) {
+    // Wide rows or large k: each row runs the vector path (sample, filter,
+    // refinement or fallback) with its own Philox stream, counter word 1 =
+    // row, in turn on `stream`, so the rows share one workspace.
+    if (!ws) return PROFK_ENULL;
+    const profk::FlatLayout FL = profk::flat_layout(*plan, dtype, profk::device_cu_count());
+    if (ws_bytes < FL.bytes) return PROFK_EWORKSPACE;
+    const uint64_t es = elem_size(dtype);
+    (void)hipGetLastError();
+    for (int64_t r = 0; r < B; ++r) {
+      profk::FlatCall fc{plan, dtype, static_cast<const uint8_t*>(values) + static_cast<uint64_t>(r) * row_stride * es,
+                         static_cast<uint32_t>(D), static_cast<uint32_t>(k), seed, static_cast<uint64_t>(r),
+                         static_cast<uint8_t*>(out_vals) + static_cast<uint64_t>(r) * k * es, out_idx + r * k,
+                         static_cast<uint8_t*>(ws), FL, static_cast<hipStream_t>(stream),
+                         info_dev ? info_dev + r : nullptr, 0, 0};
+      const hipError_t e = profk::launch_flat(fc);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    return PROFK_OK;
+  }
   const profk::RowLayout L = profk::row_layout(*plan, dtype);
-  if (L.bytes > profk::kRowMaxLds) return PROFK_EINVAL;
   profk::RowCall c{plan, dtype, values, static_cast<uint32_t>(B), static_cast<uint32_t>(D),
                    static_cast<uint32_t>(k), static_cast<uint64_t>(row_stride), seed, out_vals, out_idx,
                    info_dev, L, static_cast<hipStream_t>(stream)};

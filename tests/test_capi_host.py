@@ -153,3 +153,29 @@ def test_binding_shares_torchs_hip_runtime():
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
     assert out.returncode == 0, out.stderr
     assert out.stdout.splitlines()[0] == "1", out.stdout
+
+
+def test_rows_workspace_and_refusals_outside_the_row_kernel():
+    """Row plans the one-workgroup kernel takes need no workspace; larger
+    ones need one row's vector workspace, and the call refuses a missing
+    or short one before anything is enqueued (host-only checks)."""
+    import ctypes
+    fits = pk.plan_rows(131072, 32)
+    wide = pk.plan_rows(2**22, 32)
+    big_k = pk.plan_rows(65536, 2048)
+    assert pk.workspace_size(fits, pk.BF16, 4096) == 256
+    for p in (wide, big_k):
+        need = pk.workspace_size(p, pk.F32, 8)
+        assert need == pk.workspace_size(p, pk.F32, 1) > 256
+    L = pk.lib()
+    dummy = ctypes.c_void_p(256)   # never dereferenced: the calls fail their host checks
+    rc = L.profk_topk_rows(ctypes.byref(wide), pk.F32, dummy, 8, 2**22, 2**22, 32, 0, dummy, dummy,
+                           None, 0, None, None)
+    assert rc == pk.ENULL
+    rc = L.profk_topk_rows(ctypes.byref(wide), pk.F32, dummy, 8, 2**22, 2**22, 32, 0, dummy, dummy,
+                           dummy, pk.workspace_size(wide, pk.F32, 8) - 1, None, None)
+    assert rc == pk.EWORKSPACE
+    # a plan whose buffer words would wrap the row kernel's 32-bit LDS sums
+    huge = pk.plan_rows(2**32 - 1, 16, S_min=1, S_max=1, force_mode=pk.FORCE_FILTER)
+    assert huge.M > 2**30
+    assert pk.workspace_size(huge, pk.F32, 2) > 256

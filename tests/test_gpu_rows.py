@@ -7,39 +7,9 @@ import pytest
 import paper_2608_12573_amd as pk
 import workloads
 from oracle import keys as okeys, plan as oplan, profk as oprofk
-from gpu_util import gpu_bf16, gpu_f32, host_bits, note, oracle_plan_of, plan_from_lib, torch
+from gpu_util import check_rows as _check_rows, oracle_plan_of, plan_from_lib
 
 pytestmark = pytest.mark.gpu
-
-
-def _check_rows(bits2d, dtype, k, p, q, seed, offset=0, stride=None):
-    t = torch()
-    B, D = bits2d.shape
-    stride = D if stride is None else stride
-    padded = np.zeros((B, stride), dtype=bits2d.dtype)
-    padded[:, :D] = bits2d
-    flat = padded.reshape(-1)
-    g = gpu_f32(flat.view(np.float32), offset) if dtype == "f32" else gpu_bf16(flat, offset)
-    x = g.view(B, stride)[:, :D]
-    note(f"rows {dtype} B={B} D={D} stride={stride} off={offset} k={k} S={p.S} t={p.t} M={p.M}")
-    vals, idx, info = pk.topk_rows(x, k, seed=seed, p=p)
-    t.cuda.synchronize()
-    gv = host_bits(vals).reshape(B, k)
-    gi = idx.cpu().numpy().reshape(B, k)
-    recs = pk.read_info(info)
-    statuses = []
-    for r in range(B):
-        ref = oprofk.run(bits2d[r], dtype, k, q, seed, row=r)
-        statuses.append(ref.status)
-        rec = recs[r]
-        assert int(rec["status"]) == ref.status, (r, int(rec["status"]), ref.status)
-        if ref.status != oprofk.STATUS_DIRECT:
-            assert int(rec["tau_key"]) == ref.tau_key, r
-            assert int(rec["count"]) == ref.count, r
-        assert int(rec["n_valid"]) == ref.n_valid, r
-        assert np.array_equal(gi[r], ref.idx), (r, gi[r][:8], ref.idx[:8])
-        assert np.array_equal(gv[r], ref.vals), r
-    return statuses
 
 
 def _bits(dtype, B, D, seed):
