@@ -81,12 +81,13 @@ def survivors_lex(key, tau, tau_idx):
     return np.flatnonzero((key > tau) | ((key == tau) & (i <= tau_idx)))
 
 
-def run(bits, dtype, k, plan, seed, row=0, tau_override=None):
+def run(bits, dtype, k, plan, seed, row=0, tau_override=None, key=None):
     """Prof-K on one vector.  tau_override replaces stages 1-2 (used to force
     the failure paths); it is a key, or for a lexicographic plan a
-    (key, index) pair."""
+    (key, index) pair.  key: keys_of(bits, dtype) when the caller already
+    holds it (large inputs checked under several seeds)."""
     bits = np.asarray(bits)
-    key = keys_of(bits, dtype)
+    key = keys_of(bits, dtype) if key is None else key
     if plan.mode == MODE_DIRECT and tau_override is None:
         v, i = exact.topk(bits, dtype, k)
         return Result(v, i, STATUS_DIRECT, -1, -1, k)
@@ -126,9 +127,9 @@ def run_rows(bits2d, dtype, k, row_plan, seed, rows=None):
     return [run(bits2d[r], dtype, k, row_plan, seed, row=r) for r in rows]
 
 
-def run_batchtopk(bits2d, dtype, k_row, flat_plan, seed):
+def run_batchtopk(bits2d, dtype, k_row, flat_plan, seed, key=None):
     """BatchTopK (Sec. 5, BatchTopK SAEs): the [B, D] matrix is flattened to
     N = B*D and the K = B*k_row largest entries are selected globally.
-    Indices are flat (row*D + col)."""
+    Indices are flat (row*D + col).  key: as in run, for the flat view."""
     B = bits2d.shape[0]
-    return run(bits2d.reshape(-1), dtype, B * k_row, flat_plan, seed, row=0)
+    return run(bits2d.reshape(-1), dtype, B * k_row, flat_plan, seed, row=0, key=key)
