@@ -14,8 +14,10 @@ the flattened BatchTopK select); the printed line then describes that one.
 Prints one JSON line.  `value` is effective GB/s (input bytes / step time);
 `roofline` times the dominant kernel -- the filter, or for the per-row
 path its single fused kernel -- with HIP events recorded by the library
-around the launch on its own stream; `cpu_baseline` times the CPU oracle
-(exact stable-sort top-k) on a bounded prefix of the same input.
+around the launch on its own stream; `read_probe` times the library's
+read-only stream over the same bytes; `cpu_baseline` times the CPU oracle:
+its Prof-K stages on the whole input with the filter split over the host
+threads (O2), and the exact stable-sort top-k on a bounded prefix (O1).
 """
 
 import argparse
@@ -32,19 +34,36 @@ import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
-COUNTERS = os.path.join(ROOT, "profiles", "filter_counters.json")
+PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2608_12573_amd", "csrc")
-# Every source the filter kernel is compiled from: the committed counters
-# stand for this exact code and are dropped once any of these changes.
-FILTER_SRCS = ("kernels_filter.hip", "filter_tile.h", "device_common.h", "launch.h")
 WORKLOADS = ("c2", "c1", "c3a", "c3b", "c3c", "c3d", "c3d2", "c4", "c5", "c5r", "c5p", "sae")
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 FLUSH_BYTES = 512 << 20
 
+# The dominant kernel of each workload family: the name it has in rocprofv3
+# output, and every source it is compiled from (committed counters stand
+# for this exact code and are dropped once any of these changes).
+KERNELS = {
+    "filter": {"match": "k_filter<0, false,", "what": "profk::k_filter<0, false, U> (fp32 filter-and-compact)",
+               "sources": ("kernels_filter.hip", "filter_tile.h", "device_common.h", "launch.h")},
+    "rows": {"match": "k_rows<1, false>", "what": "profk::k_rows<1, false> (bf16 per-row Prof-K, one workgroup per row)",
+             "sources": ("kernels_rows.hip", "filter_tile.h", "topk_block.h", "device_common.h", "launch.h")},
+    "sae": {"match": "k_sae_filter", "what": "profk::k_sae_filter (bf16 MFMA encoder GEMM + filter epilogue)",
+            "sources": ("kernels_sae.hip", "sample_union.h", "device_common.h", "launch.h")},
+}
 
-def filter_source_sha256():
+
+def kernel_family(workload):
+    return "rows" if workload == "c4" else "sae" if workload == "sae" else "filter"
+
+
+def counters_path(workload_key):
+    return os.path.join(PROFILES, f"counters_{workload_key}.json")
+
+
+def source_sha256(family):
     h = hashlib.sha256()
-    for name in FILTER_SRCS:
+    for name in KERNELS[family]["sources"]:
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
@@ -76,26 +95,27 @@ class HipEvents:
         self.hip.hipEventDestroy(ev)
 
 
-def counters_traffic(workload_key):
-    """HBM bytes per filter launch from the committed rocprofv3 counter
-    summary, or None when it covers another workload or the kernel source
-    changed since it was taken."""
+def counters_traffic(workload_key, family):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 counter summary of this workload, or None when there is none
+    or the kernel's sources changed since it was taken."""
     try:
-        with open(COUNTERS) as f:
+        with open(counters_path(workload_key)) as f:
             c = json.load(f)
-        sha = filter_source_sha256()
+        sha = source_sha256(family)
     except OSError:
         return None
-    if c.get("kernel_source_sha256") != sha or c.get("workload_key") != workload_key:
+    if c.get("kernel_source_sha256") != sha:
         return None
     return c.get("traffic_bytes_per_launch")
 
 
 def write_counters(fetch_dir, write_dir, bench_json):
-    """profiles/filter_counters.json from two rocprofv3 --pmc runs of the
-    default workload (FETCH_SIZE, then WRITE_SIZE) and the JSON line one of
-    them printed.  The counters' units are calibrated on the 1 GiB device
-    copy bench.py's copy probe makes in the same runs."""
+    """profiles/counters_<workload>.json from two rocprofv3 --pmc runs of one
+    bench.py workload (FETCH_SIZE with TA_FLAT_ATOMIC_WAVEFRONTS_sum, then
+    WRITE_SIZE with TCC_ATOMIC_sum) and the JSON line one of them printed.
+    The byte counters' units are calibrated on the device copy bench.py's
+    copy probe makes in the same runs."""
     def per_dispatch(d, counter):
         files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
         if not files:
@@ -113,9 +133,14 @@ def write_counters(fetch_dir, write_dir, bench_json):
             kern.setdefault((name, grid), []).append(v)
         return {key: (sum(v) / len(v), len(v)) for key, v in kern.items()}
 
-    fetch, write = per_dispatch(fetch_dir, "FETCH_SIZE"), per_dispatch(write_dir, "WRITE_SIZE")
     with open(bench_json) as fh:
         line = json.loads(fh.read().strip().splitlines()[-1])
+    wl = line["config"]["workload_key"]
+    family = kernel_family(wl.split("-")[0])
+    spec = KERNELS[family]
+    fetch, write = per_dispatch(fetch_dir, "FETCH_SIZE"), per_dispatch(write_dir, "WRITE_SIZE")
+    atom_w = per_dispatch(fetch_dir, "TA_FLAT_ATOMIC_WAVEFRONTS_sum")
+    atom_l2 = per_dispatch(write_dir, "TCC_ATOMIC_sum")
 
     def pick(table, pred, biggest=False):
         keys = [key for key in table if pred(key[0])]
@@ -123,45 +148,47 @@ def write_counters(fetch_dir, write_dir, bench_json):
             sys.exit("kernel not found in the counter files")
         return max(keys, key=lambda key: table[key][0]) if biggest else keys[0]
 
-    is_filter = lambda n: "k_filter<0, false," in n
+    is_kernel = lambda n: spec["match"] in n
     is_copy = lambda n: "copyBuffer" in n
-    fk, ck = pick(fetch, is_filter), pick(fetch, is_copy, biggest=True)
-    wk, cwk = pick(write, is_filter), pick(write, is_copy, biggest=True)
-    gib = float(1 << 30)
-    fpu, wpu = gib / fetch[ck][0], gib / write[cwk][0]
+    fk, ck = pick(fetch, is_kernel), pick(fetch, is_copy, biggest=True)
+    wk, cwk = pick(write, is_kernel), pick(write, is_copy, biggest=True)
+    copy_bytes = line["copy_probe"]["bytes_read"]
+    fpu, wpu = copy_bytes / fetch[ck][0], copy_bytes / write[cwk][0]
     fb, wb = fetch[fk][0] * fpu, write[wk][0] * wpu
-    algo = line["roofline"]["algorithmic_bytes_per_launch"]
+    algo = line["roofline"].get("algorithmic_bytes_per_launch")
+    base = "python bench.py --workload {} --steps 3 --warmup 1 --no-cpu-baseline --no-torch-baseline --no-read-probe"
+    wl_args = base.format(wl.split("-")[0]) + (f" --k {line['config']['k']}" if wl.startswith("c2") else "")
     out = {
-        "kernel": "profk::k_filter<0, false, U> (fp32 filter-and-compact)",
-        "workload_key": "c2-k1024",
+        "kernel": spec["what"],
+        "workload_key": wl,
         "workload": line["config"]["workload"] + f"; {line['count']} survivors",
         "commands": [
-            "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o fetch --output-format csv -- "
-            "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-torch-baseline",
-            "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o write --output-format csv -- "
-            "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-torch-baseline",
-            "python bench.py --write-counters gpurun_out/pmc_fetch gpurun_out/pmc_write "
-            "gpurun_out/pmc_fetch.json",
+            f"rocprofv3 --pmc FETCH_SIZE TA_FLAT_ATOMIC_WAVEFRONTS_sum -d {fetch_dir} -o fetch --output-format csv -- "
+            + wl_args,
+            f"rocprofv3 --pmc WRITE_SIZE TCC_ATOMIC_sum -d {write_dir} -o write --output-format csv -- " + wl_args,
+            f"python bench.py --write-counters {fetch_dir} {write_dir} <the JSON line the first run printed>",
         ],
         "fetch_size_kib_per_dispatch": round(fetch[fk][0], 2),
         "write_size_kib_per_dispatch": round(write[wk][0], 2),
         "dispatches": [fetch[fk][1], write[wk][1]],
         "calibration": {
-            "kernel": "__amd_rocclr_copyBuffer (the copy probe: torch copy_ of the same 1 GiB tensor, "
-                      "in the same runs)",
-            "bytes_read": 1 << 30, "bytes_written": 1 << 30,
+            "kernel": "__amd_rocclr_copyBuffer (the copy probe: torch copy_ of a device buffer, in the same runs)",
+            "bytes_read": copy_bytes, "bytes_written": copy_bytes,
             "fetch_size_kib": round(fetch[ck][0], 2), "write_size_kib": round(write[cwk][0], 2),
             "fetch_bytes_per_kib_unit": round(fpu, 3), "write_bytes_per_kib_unit": round(wpu, 3),
         },
         "fetch_bytes_per_launch": int(round(fb)),
         "write_bytes_per_launch": int(round(wb)),
         "traffic_bytes_per_launch": int(round(fb + wb)),
-        "algorithmic_bytes_per_launch": algo,
-        "traffic_over_algorithmic": round((fb + wb) / algo, 5),
-        "kernel_source_sha256": filter_source_sha256(),
-        "kernel_sources": list(FILTER_SRCS),
+        "atomic_wave_instructions_per_launch": round(atom_w[pick(atom_w, is_kernel)][0], 1),
+        "l2_atomic_requests_per_launch": round(atom_l2[pick(atom_l2, is_kernel)][0], 1),
+        "kernel_source_sha256": source_sha256(family),
+        "kernel_sources": list(spec["sources"]),
     }
-    with open(COUNTERS, "w") as fh:
+    if algo:
+        out["algorithmic_bytes_per_launch"] = algo
+        out["traffic_over_algorithmic"] = round((fb + wb) / algo, 5)
+    with open(counters_path(wl), "w") as fh:
         json.dump(out, fh, indent=1)
         fh.write("\n")
     print(json.dumps(out, indent=1))
@@ -300,22 +327,92 @@ class Workload:
         return f"{self.name}-k{self.k}" + ("-lex" if self.lex else "")
 
 
-def cpu_baseline(w, budget_s=10.0):
-    """The oracle's exact top-k (full stable sort, oracle.exact) on a bounded
-    prefix of the workload -- 2^24 values, or 128 rows of the per-row batch --
-    repeated for about budget_s seconds."""
+def _o2_flat(bits, dtype, k, plan, seed, workers):
+    """The oracle's Prof-K stages on one vector, with stage 3 (the filter)
+    split into `workers` contiguous chunks run on a thread pool: sample
+    (oracle.philox), threshold (oracle.profk.threshold), survivors per chunk
+    (oracle.keys.keys_of, key >= tau), then the status and the sorted top-k
+    of the survivors (or O1 on a failure), as oracle.profk.run composes them.
+    Returns (indices, count, tau)."""
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import exact, keys, philox, profk
+    n = bits.size
+    sidx = philox.sample_indices(seed, 0, plan.S, n)
+    tau = profk.threshold(keys.keys_of(bits[sidx], dtype), plan.t)
+    bounds = np.linspace(0, n, workers + 1).astype(np.int64)
+
+    def part(c):
+        lo, hi = int(bounds[c]), int(bounds[c + 1])
+        return np.flatnonzero(keys.keys_of(bits[lo:hi], dtype) >= tau) + lo
+
+    with ThreadPoolExecutor(workers) as ex:
+        surv = np.concatenate(list(ex.map(part, range(workers))))
+    count = int(surv.size)
+    if count < plan.k_req or count > plan.M:
+        return exact.topk(bits, dtype, k)[1], count, tau
+    order = surv[np.argsort(-keys.keys_of(bits[surv], dtype), kind="stable")]
+    return order[:k].astype(np.int64), count, tau
+
+
+def cpu_baseline(w, gpu_idx, budget_s=10.0):
+    """The oracle timed on the host.
+
+    O2 (the reported value): the CPU Prof-K of oracle.profk on the whole
+    workload, with its filter stage split over the host threads (for the
+    per-row batch: 256 rows, one oracle.profk.run per row on the same pool),
+    the sample seed of the GPU steps; its indices are compared with the GPU
+    result.  O1: the exact top-k by a full stable sort (oracle.exact) on one
+    thread, on a bounded prefix (2^24 values or 128 rows)."""
     sys.path.insert(0, ROOT)
-    from oracle import exact, keys
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import exact, keys, plan as oplan, profk
+    host_cpus = os.cpu_count() or 1
+    workers = max(1, min(host_cpus, int(os.environ.get("OMP_NUM_THREADS") or host_cpus)))
+    dt = "bf16" if w.es == 2 else "f32"
+    out = {"kind": "oracle", "unit": "GB/s", "cores": workers, "host_cpu_count": host_cpus}
+    if w.lex:
+        out.update(value=None, sample="O2 not timed for the lexicographic rule")
+    elif w.rows:
+        R = 256
+        bits = w.host[:R]
+        q = oplan.plan_rows(w.D, w.k)
+        t0 = time.perf_counter()
+        with ThreadPoolExecutor(workers) as ex:
+            res = list(ex.map(lambda r: profk.run(bits[r], dt, w.k, q, 0, row=r), range(R)))
+        el = time.perf_counter() - t0
+        same = all(np.array_equal(res[r].idx, gpu_idx[r]) for r in range(R))
+        out.update(value=round(R * w.D * w.es / el / 1e9, 4),
+                   sample=(f"O2: oracle.profk.run on the first {R} of the {w.B} rows, one row per task on "
+                           f"{workers} threads, {el:.2f} s"),
+                   elements_per_s=round(R * w.D / el, 1), matches_gpu=bool(same))
+    else:
+        bits = keys.f32_bits(w.host) if dt == "f32" else w.host
+        q = oplan.plan(w.N, w.k, 1e-6, w.recall)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            idx, count, tau = _o2_flat(bits, dt, w.k, q, 0, workers)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or reps >= 3:
+                break
+        per = el / reps
+        n_valid = min(w.k, count) if count >= q.k_req else w.k
+        same = bool(np.array_equal(idx[:n_valid], gpu_idx[:n_valid]))
+        out.update(value=round(w.N * w.es / per / 1e9, 4),
+                   sample=(f"O2: oracle Prof-K stages on all {w.N} values, filter split over {workers} threads, "
+                           f"{reps} runs, {per:.2f} s each ({count} survivors)"),
+                   elements_per_s=round(w.N / per, 1), matches_gpu=same)
+    # O1 on one thread, bounded
     if w.rows:
         R = 128
-        bits = w.host[:R]
-        run = lambda: exact.topk_rows(bits, "bf16", w.k)
+        b1 = w.host[:R]
+        run = lambda: exact.topk_rows(b1, dt, w.k)
         n_s, what = R * w.D, f"oracle.exact.topk_rows on the first {R} of the {w.B} rows"
     else:
         n_s = min(w.N, 2**24)
-        bits = keys.f32_bits(w.host[:n_s])
+        b1 = keys.f32_bits(w.host[:n_s]) if dt == "f32" else w.host[:n_s]
         kk = min(w.k, n_s)
-        run = lambda: exact.topk(bits, "f32", kk)
+        run = lambda: exact.topk(b1, dt, kk)
         what = f"oracle.exact.topk on the first 2^{n_s.bit_length() - 1} of the {w.N} values, k={kk}"
     reps, t0 = 0, time.perf_counter()
     while True:
@@ -325,9 +422,26 @@ def cpu_baseline(w, budget_s=10.0):
         if el >= budget_s:
             break
     per = el / reps
-    return {"value": round(n_s * w.es / per / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{what} (numpy stable argsort, one thread), {reps} runs, {per * 1e3:.0f} ms each",
-            "elements_per_s": round(n_s / per, 1)}
+    out["o1"] = {"value": round(n_s * w.es / per / 1e9, 4), "unit": "GB/s", "cores": 1,
+                 "sample": f"{what} (numpy stable argsort, one thread), {reps} runs, {per * 1e3:.0f} ms each",
+                 "elements_per_s": round(n_s / per, 1)}
+    return out
+
+
+def read_probe(pk, torch, x, per_cu, loads, reps=10):
+    """The library's read-only stream probe over x's bytes: (ms, GB/s)."""
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = torch.empty(1024, dtype=torch.int32, device=x.device)
+    for _ in range(2):
+        pk.debug_read_probe(x, per_cu, loads, out=out)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(reps):
+        pk.debug_read_probe(x, per_cu, loads, out=out)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / reps
+    return ms, x.numel() * x.element_size() / (ms * 1e-3) / 1e9
 
 
 def main():
@@ -345,10 +459,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-torch-baseline", action="store_true")
     ap.add_argument("--no-copy-probe", action="store_true")
+    ap.add_argument("--no-read-probe", action="store_true")
     ap.add_argument("--lexicographic", action="store_true",
                     help="plan with the tie-exact filter rule on (key, -index) pairs")
     ap.add_argument("--write-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
-                    help="write profiles/filter_counters.json from two rocprofv3 --pmc runs and exit")
+                    help="write profiles/counters_<workload>.json from two rocprofv3 --pmc runs of one workload and exit")
     args = ap.parse_args()
     if args.write_counters:
         write_counters(*args.write_counters)
@@ -417,7 +532,7 @@ def main():
     else:
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                    "traffic": counters_traffic(w.key()), "kernel": w.kernel,
+                    "traffic": counters_traffic(w.key(), kernel_family(w.name)), "kernel": w.kernel,
                     "algorithmic_bytes_per_launch": kern_bytes}
 
     line = {
@@ -433,7 +548,7 @@ def main():
         "vs_baseline": None,
         "dtype": "u16" if w.es == 2 else "u32",
         "data": "synthetic",
-        "config": {"workload": w.desc, "N": w.N, "k": w.k, "eps": 1e-6, "recall": w.recall,
+        "config": {"workload": w.desc, "workload_key": w.key(), "N": w.N, "k": w.k, "eps": 1e-6, "recall": w.recall,
                    "plan": {"S": w.p.S, "t": w.p.t, "M": w.p.M, "mode": w.p.mode,
                             "lexicographic": int(w.p.lexicographic)}},
         "elements_per_s": round(w.N / (ms_per_step * 1e-3), 1),
@@ -497,27 +612,43 @@ def main():
                                           "are rounded to bf16, so values differ")
         del tv, ti
 
-    if not args.no_copy_probe and not w.flops:
-        # A plain device-to-device copy of the same input: the practical
-        # streaming ceiling on this GPU, and the reference kernel that scales
-        # the FETCH_SIZE / WRITE_SIZE counters into bytes.
-        dst = torch.empty_like(w.x)
+    if not args.no_copy_probe:
+        # A plain device-to-device copy of the input (of the latent buffer
+        # for the SAE layer, whose input is small): the reference kernel that
+        # scales the FETCH_SIZE / WRITE_SIZE counters into bytes.
+        src = w.dense if w.flops else w.x
+        src_bytes = src.numel() * src.element_size()
+        dst = torch.empty_like(src)
         for _ in range(2):
-            dst.copy_(w.x)
+            dst.copy_(src)
         torch.cuda.synchronize()
         reps = 5
         start.record()
         for _ in range(reps):
-            dst.copy_(w.x)
+            dst.copy_(src)
         stop.record()
         torch.cuda.synchronize()
         c_ms = start.elapsed_time(stop) / reps
-        line["copy_probe"] = {"bytes_read": w.in_bytes, "bytes_written": w.in_bytes, "ms": round(c_ms, 4),
-                              "GB/s": round(2 * w.in_bytes / (c_ms * 1e-3) / 1e9, 1)}
+        line["copy_probe"] = {"bytes_read": src_bytes, "bytes_written": src_bytes, "ms": round(c_ms, 4),
+                              "GB/s": round(2 * src_bytes / (c_ms * 1e-3) / 1e9, 1)}
         del dst
 
+    if not args.no_read_probe and not w.flops and (w.in_bytes % 16 == 0):
+        # The library's read-only stream with the filter's access pattern:
+        # the practical ceiling of a single read of the input.  First the
+        # launch shape the filter uses for this size, then the best of a
+        # small sweep.
+        big = w.in_bytes >= (512 << 20)
+        shape = (2, 4) if big else (4, 8)
+        ms, gbps = read_probe(pk, torch, w.x, *shape)
+        sweep = {f"{pc}x{u}": round(read_probe(pk, torch, w.x, pc, u)[1], 1)
+                 for pc in (1, 2, 4) for u in (4, 8)}
+        line["read_probe"] = {"bytes_read": w.in_bytes, "workgroups_per_cu": shape[0], "loads_per_lane": shape[1],
+                              "ms": round(ms, 4), "GB/s": round(gbps, 1),
+                              "sweep_GB/s (workgroups per CU x loads per lane)": sweep}
+
     if not args.no_cpu_baseline and not w.flops:
-        line["cpu_baseline"] = cpu_baseline(w)
+        line["cpu_baseline"] = cpu_baseline(w, w.out[1].cpu().numpy())
 
     print(json.dumps(line), flush=True)
 

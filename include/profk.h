@@ -224,6 +224,21 @@ int profk_debug_filter(const profk_plan_t* plan, int32_t dtype,
                        uint32_t* count_dev, void* ws, size_t ws_bytes,
                        void* stream);
 
+/* A read-only stream over `bytes` bytes of device memory (a multiple of 16,
+ * 16-byte aligned), with the filter pass's access pattern: a persistent grid
+ * of blocks_per_cu (1..8) workgroups per compute unit, at most 1024, taking
+ * tiles of 16-byte vectors in turn, each lane with loads_per_lane (4 or 8)
+ * nontemporal loads in flight.  Nothing is compared or written but one word
+ * per workgroup: out_dev[w] = the XOR of every 32-bit word workgroup w read
+ * (so the XOR over out_dev[0 .. *grid) is the XOR of the whole buffer).
+ * out_dev: 1024 uint32 on the device; *grid (host) receives the number of
+ * workgroups launched.  bytes / 16 <= 2^32 - 2^22 - 1, else PROFK_EINVAL.  Measurement tools time it as the practical read
+ * ceiling of the filter pass (Sec. 3, stage "Filtering", a single streaming
+ * pass over the input). */
+int profk_debug_read_probe(const void* values, uint64_t bytes, int32_t blocks_per_cu,
+                           int32_t loads_per_lane, uint32_t* out_dev, uint32_t* grid,
+                           void* stream);
+
 /* ---- BatchTopK SAE layer (Sec. 5, "Application: BatchTopK Sparse
  * Autoencoders"; the encoder and decoder are those of the BatchTopK SAE the
  * paper builds on) ----

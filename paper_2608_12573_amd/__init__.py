@@ -95,6 +95,7 @@ def lib():
                                       ctypes.c_size_t, vp, vp]
         L.profk_debug_sample_indices.argtypes = [u64, i64, i64, i64, vp, vp]
         L.profk_debug_filter.argtypes = [P(Plan), i32, vp, i64, u32, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.profk_debug_read_probe.argtypes = [vp, u64, i32, i32, vp, P(u32), vp]
         L.profk_status_string.argtypes = [ctypes.c_int]
         L.profk_status_string.restype = ctypes.c_char_p
         L.profk_last_hip_error.restype = ctypes.c_int
@@ -375,6 +376,23 @@ def debug_filter(x, tau_key, p, ws=None):
     _check(lib().profk_debug_filter(ctypes.byref(p), dt, _ptr(x), x.numel(), tau_key, _ptr(bk), _ptr(bi),
                                     _ptr(cnt), _ptr(ws), _nbytes(ws), _stream()))
     return bk, bi, cnt
+
+
+def debug_read_probe(x, blocks_per_cu=2, loads_per_lane=4, out=None):
+    """profk_debug_read_probe over the bytes of a contiguous CUDA tensor whose
+    size is a multiple of 16 bytes: (per-workgroup XOR words, workgroups)."""
+    torch = _torch()
+    if not isinstance(x, torch.Tensor) or not x.is_contiguous():
+        raise ProfkError("x must be a contiguous tensor")
+    _on_device(x, "x", None)
+    if out is None:
+        out = torch.empty(1024, dtype=torch.int32, device=x.device)
+    else:
+        _buffer(out, "out", torch.int32, 1024, x.device)
+    grid = ctypes.c_uint32(0)
+    _check(lib().profk_debug_read_probe(_ptr(x), _nbytes(x), blocks_per_cu, loads_per_lane, _ptr(out),
+                                        ctypes.byref(grid), _stream()))
+    return out, int(grid.value)
 
 
 # ------------------------------------------------------ BatchTopK SAE layer ---

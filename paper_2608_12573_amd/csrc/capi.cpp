@@ -352,6 +352,20 @@ int profk_topk_noalloc(const profk_plan_t* plan, int32_t dtype, const void* valu
                   stream, info_dev, 0, 0);
 }
 
+int profk_debug_read_probe(const void* values, uint64_t bytes, int32_t blocks_per_cu, int32_t loads_per_lane,
+                           uint32_t* out_dev, uint32_t* grid, void* stream) {
+  if (!values || !out_dev || !grid) return PROFK_ENULL;
+  // the probe's vector indices and its grid stride (at most 2^21 vectors)
+  // stay below 2^32
+  if (bytes < 16 || bytes % 16 != 0 || bytes / 16 > static_cast<uint64_t>(UINT32_MAX) - (1u << 22))
+    return PROFK_EINVAL;
+  if (reinterpret_cast<uintptr_t>(values) % 16 != 0) return PROFK_EINVAL;
+  if (blocks_per_cu < 1 || blocks_per_cu > 8 || (loads_per_lane != 4 && loads_per_lane != 8)) return PROFK_EINVAL;
+  const hipError_t e = profk::launch_read_probe(values, bytes / 16, blocks_per_cu, loads_per_lane, out_dev, grid,
+                                                static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PROFK_OK : hip_fail(e);
+}
+
 namespace {
 std::mutex g_simple_mu;
 void* g_simple_ws = nullptr;

@@ -233,6 +233,11 @@ hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64
 hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* buf_idx,
                                uint32_t* count_dev);
 
+// Read-only stream probe: XOR fold of nvec 16-byte vectors, one word per
+// workgroup into out (kFiltMaxBlocks words at most); *grid_out = workgroups.
+hipError_t launch_read_probe(const void* values, uint64_t nvec, int blocks_per_cu, int loads_per_lane,
+                             uint32_t* out, uint32_t* grid_out, hipStream_t s);
+
 int device_cu_count();
 
 }  // namespace profk

@@ -179,3 +179,18 @@ def test_rows_workspace_and_refusals_outside_the_row_kernel():
     huge = pk.plan_rows(2**32 - 1, 16, S_min=1, S_max=1, force_mode=pk.FORCE_FILTER)
     assert huge.M > 2**30
     assert pk.workspace_size(huge, pk.F32, 2) > 256
+
+
+def test_read_probe_refuses_bad_arguments():
+    """Host-side checks of profk_debug_read_probe; the dummy pointers are
+    never dereferenced because every call fails before a launch."""
+    import ctypes
+    L = pk.lib()
+    ptr, out = ctypes.c_void_p(4096), ctypes.c_void_p(8192)
+    grid = ctypes.c_uint32(0)
+    assert L.profk_debug_read_probe(ptr, 100, 2, 4, out, ctypes.byref(grid), None) == pk.EINVAL      # not 16-byte multiple
+    assert L.profk_debug_read_probe(ctypes.c_void_p(4100), 4096, 2, 4, out, ctypes.byref(grid), None) == pk.EINVAL
+    assert L.profk_debug_read_probe(ptr, 4096, 0, 4, out, ctypes.byref(grid), None) == pk.EINVAL
+    assert L.profk_debug_read_probe(ptr, 4096, 2, 5, out, ctypes.byref(grid), None) == pk.EINVAL
+    assert L.profk_debug_read_probe(ptr, 16 * (2**32 - 2**22), 2, 4, out, ctypes.byref(grid), None) == pk.EINVAL
+    assert L.profk_debug_read_probe(None, 4096, 2, 4, out, ctypes.byref(grid), None) == pk.ENULL
