@@ -17,16 +17,10 @@
 #include "device_common.h"
 #include "filter_tile.h"
 #include "launch.h"
+#include "row_common.h"
 #include "topk_block.h"
 
 namespace profk {
-
-// Radix digit of the refinement and fallback: 16-bit keys take two 8-bit
-// passes (a 256-word histogram), 32-bit keys three 11-bit ones.
-template <int DT> constexpr int row_digit() { return Elem<DT>::KEYBITS == 16 ? 8 : 11; }
-
-// Buffer keys are stored at their own width (bf16 keys in 16 bits).
-template <int DT> using RowKey = typename std::conditional<Elem<DT>::KEYBITS == 16, uint16_t, uint32_t>::type;
 
 // tau from the sample held in registers (at most 8 keys per thread): each
 // wave's top-t, then the top-t of their union.
@@ -45,10 +39,6 @@ struct RowArgs {
   profk_info_t* info;
   RowLayout L;
 };
-
-// Log-scale buckets a row key distance can fall in: 16-bit keys keep every
-// distance below 2^16, so bf16 rows need only the first 1280.
-template <int DT> constexpr uint32_t row_log_bins() { return Elem<DT>::KEYBITS == 16 ? 1280u : kLogBins; }
 
 template <int DT, bool LEX>
 __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
