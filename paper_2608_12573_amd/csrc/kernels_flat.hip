@@ -3,9 +3,10 @@
 // Sec. 3 "The Prof-K Algorithm".
 //
 // Kernel sequence of one call, all on the caller's stream:
-//   k_sample      ceil(S/1024) blocks: Philox draws, gathers, and each block's
-//                 local top-t sample keys (the t-th largest of the whole
-//                 sample is among the union of the blocks' top-t).
+//   k_sample      ceil(S/1024) blocks (ceil(S/4096) of 1024 threads when
+//                 t > 32): Philox draws, gathers, and each block's local
+//                 top-t sample keys (the t-th largest of the whole sample is
+//                 among the union of the blocks' top-t).
 //   k_select_tau  only when that union is large: one block picks tau.
 //   k_tau_index   lexicographic plans only: the sample blocks list the draws
 //                 that carry tau, and the last one picks the threshold pair.
@@ -36,14 +37,14 @@ struct SampleArgs {
   uint32_t* fhist;
 };
 
-template <int DT>
-__global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
-  static_assert(kSampPerBlock == 4 * kSampBS, "four draws per thread");
-  __shared__ SampleUnionShared<kSampBS> sh;
+template <int DT, int BS>
+__global__ __launch_bounds__(BS) void k_sample(SampleArgs a) {
+  constexpr uint32_t kPer = 4 * BS;  // four draws per thread
+  __shared__ SampleUnionShared<BS> sh;
   const uint32_t b = blockIdx.x, tid = threadIdx.x;
   if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist);
-  const uint32_t j0 = b * kSampPerBlock;
-  const uint32_t nb = min(static_cast<uint32_t>(kSampPerBlock), a.S - j0);
+  const uint32_t j0 = b * kPer;
+  const uint32_t nb = min(kPer, a.S - j0);
   uint32_t kv[4];
   uint32_t valid = 0;
   {
@@ -59,8 +60,7 @@ __global__ __launch_bounds__(kSampBS) void k_sample(SampleArgs a) {
       }
     }
   }
-  sample_block_top<kSampBS, Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap,
-                                                sh);
+  sample_block_top<BS, Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
 }
 
 // ------------------------------------------------------------ stage 2 -----
@@ -777,9 +777,11 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   const uint32_t epv = dtype == PROFK_F32 ? 4 : 8;
   const uint32_t S = static_cast<uint32_t>(p.S), t = static_cast<uint32_t>(p.t);
   const uint32_t M = static_cast<uint32_t>(p.M), k = static_cast<uint32_t>(p.k);
-  L.G_s = cdiv(S, kSampPerBlock);
-  L.tcap = t < static_cast<uint32_t>(kSampPerBlock) ? t : kSampPerBlock;
-  const uint32_t last_nb = S - (L.G_s - 1) * kSampPerBlock;
+  L.samp_bs = (!p.lexicographic && t > kWaveTopMax) ? kSampWideBS : kSampBS;
+  const uint32_t spb = 4u * L.samp_bs;
+  L.G_s = cdiv(S, spb);
+  L.tcap = t < spb ? t : spb;
+  const uint32_t last_nb = S - (L.G_s - 1) * spb;
   L.union_n = (L.G_s - 1) * L.tcap + (t < last_nb ? t : last_nb);
   // Expected survivors per element are about t / (S + 1).
   const bool sparse = N * (dtype == PROFK_F32 ? 4u : 2u) >= kFiltSparseMinBytes &&
@@ -887,7 +889,8 @@ static hipError_t launch_flat_t(const FlatCall& c) {
     uint32_t* uk = at<uint32_t>(c.ws, L.off_union);
     SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
                   L.tcap, uk, st, seg_cnt, fhist};
-    hipLaunchKernelGGL(k_sample<DT>, dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
+    if (L.samp_bs == kSampWideBS) hipLaunchKernelGGL((k_sample<DT, kSampWideBS>), dim3(L.G_s), dim3(kSampWideBS), 0, c.stream, sa);
+    else hipLaunchKernelGGL((k_sample<DT, kSampBS>), dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
     if (!lex && L.union_n <= kFiltTauMax && static_cast<uint32_t>(p.t) <= kFiltTauInMaxT) {
       union_for_filter = uk;
     } else {

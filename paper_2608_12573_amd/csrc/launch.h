@@ -27,6 +27,10 @@ static_assert(sizeof(CallState) == 256, "call state size");
 // Launch geometry.
 constexpr int kSampBS = 256;                  // threads of a sample block
 constexpr int kSampPerBlock = 4 * kSampBS;    // draws per sample block
+// Sample blocks of plans with t > kWaveTopMax (key rule): 1024 threads and
+// 4096 draws, so that the union of the blocks' top-t lists, which one
+// workgroup selects tau from, is four times smaller.
+constexpr int kSampWideBS = 1024;
 constexpr uint32_t kWaveTopMax = 32;          // largest t of the wave-level top-t
 constexpr int kTauBS = 1024;
 constexpr int kFiltBS = 256;                  // threads of a filter block
@@ -76,6 +80,7 @@ constexpr int kBktSortBlocks = 512;           // bucket-sort grid (loops over th
 // Workspace layout of one flat (vector) call.
 struct FlatLayout {
   uint32_t G_s = 0, tcap = 0, union_n = 0;    // sampling
+  uint32_t samp_bs = 0;                       // threads of a sample block (four draws each)
   uint32_t G_f = 0;                           // filter blocks
   int filt_u = 0;                             // 16-byte loads per lane and filter step
   uint32_t seg_cap = 0;                       // entries per candidate segment (= M)
