@@ -207,6 +207,19 @@ struct SelectResult {
 // (coherent across the XCDs' L2 caches) or atomics and wait for them to
 // complete before taking a ticket; only the consumer that wins the ticket
 // invalidates its L2 (an agent-scope acquire) before it reads.
+// Why this orders the data before the ticket without a release fence: an
+// agent-scope store is issued with the sc1 bit, so it is written through to
+// the memory side shared by every XCD rather than kept in the producer's
+// L2; vmcnt counts it until that write has been acknowledged, so after
+// s_waitcnt vmcnt(0) (wait_memory) every such store of the wave is visible
+// device-wide.  A workgroup barrier then covers the other waves' stores, and
+// only after it does one lane take the ticket with an atomic, which is
+// performed at the device-coherent level.  A consumer that sees the final
+// ticket value therefore follows every producer's completed stores, and its
+// acquire drops any stale lines its own L2 held.  The argument rests on the
+// hardware's write-through and counter semantics rather than on a fence the
+// language memory model names; the GPU tests of every hand-over (fallback
+// merges, large-k radix passes, the lexicographic tie list) check it.
 __device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
