@@ -23,6 +23,8 @@
 //
 // One 32x32x16 MFMA step rounds once: the accumulator and its 16 products
 // are summed together before rounding to fp32.
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 #include "sample_union.h"
@@ -321,21 +323,35 @@ __device__ __forceinline__ bool sae_passes(uint32_t akey, float b, float tf) {
   return __uint_as_float(bits_from_key_f32(akey)) + b >= tf;
 }
 
-__global__ void k_sae_thresholds(const CallState* st, const float* bias, uint32_t d_dict, float* thr) {
+// col[j] = {thr[j], b_enc[j]} for j < d_dict, and {NaN, 0} up to the
+// padded length (a multiple of kSaeFBN), so that the filter copies a tile's
+// columns whole.  When tau is at most key(+0) every latent survives (relu
+// maps each to +0 or above) and thr[j] is -inf.
+__global__ void k_sae_thresholds(const CallState* st, const float* bias, uint32_t d_dict, uint32_t d_pad,
+                                 float2* col) {
   const uint32_t j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= d_dict) return;
-  const float tf = __uint_as_float(bits_from_key_f32(st->tau_key));
+  if (j >= d_pad) return;
+  if (j >= d_dict) {
+    col[j] = float2{__uint_as_float(0x7FC00000u), 0.0f};
+    return;
+  }
+  const uint32_t tau = st->tau_key;
+  const float tf = __uint_as_float(bits_from_key_f32(tau));
   const float b = bias[j];
+  if (tau <= 0x80000000u) {
+    col[j] = float2{-__builtin_inff(), b};
+    return;
+  }
   uint32_t lo = key_f32(0xFF800000u), hi = key_f32(0x7F800000u);  // -inf, +inf
   if (!sae_passes(hi, b, tf)) {
-    thr[j] = __uint_as_float(0x7FC00000u);
+    col[j] = float2{__uint_as_float(0x7FC00000u), b};
     return;
   }
   while (lo < hi) {  // the smallest passing key in [lo, hi]
     const uint32_t mid = lo + (hi - lo) / 2;
     if (sae_passes(mid, b, tf)) hi = mid; else lo = mid + 1;
   }
-  thr[j] = __uint_as_float(bits_from_key_f32(lo));
+  col[j] = float2{__uint_as_float(bits_from_key_f32(lo)), b};
 }
 
 // ------------------------------------------------------------ stage 3 -----
@@ -346,43 +362,170 @@ struct SaeFilterArgs {
   uint32_t seg_cap;
   uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
   uint32_t* fhist;   // refinement histogram, zero on entry
-  const float* thr;  // [d_dict] from k_sae_thresholds
+  const float2* col;  // {threshold, bias} per column, padded to whole tiles (k_sae_thresholds)
 };
 
 constexpr uint32_t kSaeSlice = kStage / (kSaeBS / kWave);  // survivors a wave stages in LDS
 
+// The filter's GEMM: 256 x 256 tiles (waves in a 4 x 2 grid, 64 x 128 each
+// as 2 x 4 32x32 accumulators), twice the arithmetic per loaded byte and per
+// LDS fragment read of the 256 x 128 tiles above.  d_model is consumed in
+// chunks of kSaeFK, in two LDS stages that direct-to-LDS loads fill
+// (global_load_lds, 16 bytes per lane: lane L of a wave's instruction fills
+// the granule at the instruction's base + L), so no registers stage them.
+// Fragments are double-buffered in registers: the reads of a k-step are in
+// flight during the previous k-step's MFMAs, and a chunk's last MFMAs are in
+// flight during the wait and barrier for the next chunk.  The k-steps are the
+// same 32x32x16 MFMAs in the same ascending order as sae_tile_mma, so every
+// latent is bit-identical to the sample's and the dense kernel's.
+constexpr uint32_t kSaeFBM = 256, kSaeFBN = 256, kSaeFK = 64;
+constexpr uint32_t kSaeFSeg = kSaeFK / 8;              // 16-byte granules of a row in a chunk
+constexpr uint32_t kSaeFGran = kSaeFBM * kSaeFSeg;     // granules of one operand stage
+constexpr int kSaeFQ = kSaeFGran / kSaeBS;             // loads per lane, operand and chunk
+constexpr int kSaeFKS = kSaeFK / 16;                   // k-steps per chunk
+static_assert(kSaeFBN == kSaeFBM && kSaeFGran % kSaeBS == 0 && kSaeFKS % 2 == 0, "filter tile shape");
+static_assert(kSaeBS / kWave == 8, "waves of the filter tile");
 
+// s_waitcnt vmcnt(0) lgkmcnt(0), leaving expcnt alone (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt in 6:4, lgkmcnt in 11:8).
+__device__ __forceinline__ void wait_loads_lds() { __builtin_amdgcn_s_waitcnt(0x7 << 4); }
+// vmcnt(N) lgkmcnt(0)
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+}
 
-// Persistent: workgroup b takes its XCD group's tiles (XcdTiles).  Each
-// wave stages survivors (key, index) in its own slice of the workgroup stage
-// with a wave-uniform fill count, so the common path takes no atomics; a
-// slice is appended to the workgroup's candidate segment (one atomic) when it
-// is half full at a tile's start, and at the end.  The log-bin counts and the
-// maximum key are taken from the slice as it is appended.
+// Granule of row `row`, 16-byte k segment `seg` in a stage: the XOR puts the
+// eight rows that eight neighbouring lanes read together into eight
+// different 16-byte bank groups.  Its inverse is itself.
+__device__ __forceinline__ uint32_t sae_swz(uint32_t row, uint32_t seg) { return row * kSaeFSeg + (seg ^ (row & 7)); }
+
+// Tile-local row and column of element v of accumulator (i, j) in the filter
+// tile.
+__device__ __forceinline__ uint32_t sae_frow(uint32_t lane, uint32_t w, int i, int v) {
+  return (w >> 1) * 64 + i * 32 + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
+}
+__device__ __forceinline__ uint32_t sae_fcol(uint32_t lane, uint32_t w, int j) {
+  return (w & 1) * 128 + j * 32 + (lane & 31);
+}
+
+// Persistent: workgroup b takes its XCD group's tiles (XcdTiles).  A wave
+// writes a tile's survivors to its own slice of LDS at their ranks (a
+// wave-uniform fill count, no atomics); during the next tile's MFMAs they are
+// converted to (key, flat index) and appended to the workgroup's candidate
+// segment with one atomic, and their log-bin counts and maximum key taken.
 //
-// Per latent of a full tile, the fast epilogue costs one compare against the
-// column threshold and a wave-uniform branch; the body runs only for
-// accumulator elements with a survivor in the wave.  A tile whose survivors
-// do not fit the slice, a tile cut by the last row, and every tile when tau
-// is at most key(+0) (all latents survive) go through the general epilogue: the accumulators pass through LDS and each
-// element's survivors are appended to the segment directly.
+// Epilogue: per accumulator element one compare against the column's
+// threshold, ballots taken eight at a time, and a wave-uniform branch to the
+// out-of-line body, taken only for elements with a survivor in the wave.
+// Columns past d_dict have a NaN threshold, rows past B NaN accumulators (see
+// issue), so neither passes; when tau is at most key(+0) every latent
+// survives and in-range columns have the threshold -inf.
+//
+// CROSS (the chunks of a tile are even in number, so chunk c of every tile
+// is in stage c % 2): the next tile's first chunk is awaited, and its second
+// issued, before this tile's epilogue, so that they load meanwhile.
+// Otherwise each tile starts its own loads behind a barrier.
+//
+// Waits: with two stages the chunk awaited is the newest one issued, so each
+// wait is vmcnt(0) (with lgkmcnt(0), which also completes this wave's
+// fragment reads of the stage refilled after the barrier); the barrier then
+// covers the other waves' loads and reads.
+template <bool CROSS>
 __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
-  __shared__ SaeTileLds tl;
-  __shared__ uint32_t s_skey[kStage], s_sidx[kStage];
+  // distinct arrays per stage, so that the compiler can tell the stage being
+  // read from the one being filled
+  __shared__ __align__(16) uint4 sA0[kSaeFGran], sA1[kSaeFGran], sB0[kSaeFGran], sB1[kSaeFGran];
+  __shared__ uint2 s_slice[kStage];  // per wave kSaeSlice (accumulator bits, element id) pairs
   __shared__ uint32_t s_hist[kLogBins];
   __shared__ uint32_t s_wmax[kSaeBS / kWave];
-  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  __shared__ __align__(16) float2 s_col[2][kSaeFBN];  // a tile's {threshold, bias}, by tile parity
+  // the wave index is wave-uniform: read from lane 0 it is a scalar, and so
+  // are the LDS bases derived from it
+  const uint32_t b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1);
+  const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const uint32_t wm = w >> 1, wn = w & 1;
   const uint32_t seg = b & (kSegs - 1);
   const uint32_t tau = a.st->tau_key;
-  const bool all = tau <= 0x80000000u;  // tau <= key(+0): every latent survives
-  for (uint32_t i = tid; i < kLogBins; i += kSaeBS) s_hist[i] = 0;  // visible after the first tile's barrier
+  for (uint32_t i = tid; i < kLogBins; i += kSaeBS) s_hist[i] = 0;  // complete before the first barrier
   uint32_t* const seg_counter = a.seg_cnt + seg * kSegStride;
   uint32_t* const seg_key = a.seg_key + static_cast<size_t>(seg) * a.seg_cap;
   uint32_t* const seg_idx = a.seg_idx + static_cast<size_t>(seg) * a.seg_cap;
-  uint32_t* const wkey = s_skey + w * kSaeSlice;
-  uint32_t* const widx = s_sidx + w * kSaeSlice;
-  uint32_t wcnt = 0;  // wave-uniform fill of the wave's slice
+  // the wave's slice: a tile's survivors as (accumulator bits, element id);
+  // its last entry is a spare that takes every rank past the others
+  uint2* const wslice = s_slice + w * kSaeSlice;
+  constexpr uint32_t kHot = kSaeSlice - 1;
   uint32_t my_max = 0;
+  const uint32_t nchunk = a.g.d_model / kSaeFK;
+  const uint32_t B = a.g.B, dd = a.g.d_dict, dm = a.g.d_model;
+
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  // Load q (of kSaeFQ) of an operand fills granules (kSaeFQ w + q) 64 + lane
+  // of a stage; granule P holds row P / 8, segment (P % 8) ^ (row % 8), so
+  // lane L loads row 32 w + 8 q + L / 8 of the tile, segment
+  // (L % 8) ^ (L / 8 % 8): a wave-uniform row base plus a lane offset that is
+  // the same for every load (the loads take a scalar base and a 32-bit
+  // offset).
+  const uint32_t loff = ((lane / 8) * dm + (((lane & 7) ^ ((lane >> 3) & 7)) * 8)) * 2;  // bytes
+  // chunk kc of tile (m0, n0) into stage S.  In a tile that passes B or
+  // d_dict, lanes of rows out of range write their granule instead: NaN for x
+  // (such rows' accumulators are NaN and pass no compare), zero for W_enc
+  // (such columns have a NaN threshold).
+  auto issue = [&](auto S, uint32_t m0, uint32_t n0, uint32_t kc) {
+    uint4* const A = decltype(S)::value == 0 ? sA0 : sA1;
+    uint4* const W = decltype(S)::value == 0 ? sB0 : sB1;
+    // a wave-uniform base (row, chunk) and the lane's byte offset
+    const char* const xc = reinterpret_cast<const char*>(a.g.x) + static_cast<size_t>(kc) * kSaeFK * 2 + loff;
+    const char* const wc = reinterpret_cast<const char*>(a.g.w) + static_cast<size_t>(kc) * kSaeFK * 2 + loff;
+    const size_t rb = static_cast<size_t>(dm) * 2;  // bytes per row
+#define SAE_SRC(base, row) reinterpret_cast<const uint16_t*>((base) + static_cast<size_t>(row) * rb)
+    if (m0 + kSaeFBM <= B && n0 + kSaeFBN <= dd) {
+#pragma unroll
+      for (int q = 0; q < kSaeFQ; ++q)
+        __builtin_amdgcn_global_load_lds(SAE_SRC(xc, m0 + 32 * w + 8 * q), A + (kSaeFQ * w + q) * kWave, 16, 0, 0);
+#pragma unroll
+      for (int q = 0; q < kSaeFQ; ++q)
+        __builtin_amdgcn_global_load_lds(SAE_SRC(wc, n0 + 32 * w + 8 * q), W + (kSaeFQ * w + q) * kWave, 16, 0, 0);
+    } else {
+#pragma unroll
+      for (int q = 0; q < kSaeFQ; ++q) {
+        const uint32_t r = m0 + 32 * w + 8 * q;
+        uint4* const slot = A + (kSaeFQ * w + q) * kWave;
+        if (r + lane / 8 < B) __builtin_amdgcn_global_load_lds(SAE_SRC(xc, r), slot, 16, 0, 0);
+        else slot[lane] = uint4{0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
+      }
+#pragma unroll
+      for (int q = 0; q < kSaeFQ; ++q) {
+        const uint32_t r = n0 + 32 * w + 8 * q;
+        uint4* const slot = W + (kSaeFQ * w + q) * kWave;
+        if (r + lane / 8 < dd) __builtin_amdgcn_global_load_lds(SAE_SRC(wc, r), slot, 16, 0, 0);
+        else slot[lane] = uint4{0u, 0u, 0u, 0u};
+      }
+    }
+#undef SAE_SRC
+  };
+  struct Frag {
+    bf16x8 a[2], b[4];
+  };
+  auto rd = [&](auto S, uint32_t ks, Frag& f) {
+    const uint4* const A = decltype(S)::value == 0 ? sA0 : sA1;
+    const uint4* const W = decltype(S)::value == 0 ? sB0 : sB1;
+    const uint32_t sg = 2 * ks + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) f.a[i] = __builtin_bit_cast(bf16x8, A[sae_swz(wm * 64 + i * 32 + (lane & 31), sg)]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) f.b[j] = __builtin_bit_cast(bf16x8, W[sae_swz(wn * 128 + j * 32 + (lane & 31), sg)]);
+  };
+  f32x16 acc[2][4];
+  auto mma = [&](const Frag& f) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+  };
+
   // one survivor's log-bin count and maximum
   auto note = [&](uint32_t key) {
     atomicAdd(&s_hist[log_bin(key - tau)], 1u);
@@ -390,106 +533,211 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
   };
   // the wave's n staged survivors to the segment (a wave's LDS operations
   // execute in program order, so the slice reads see its writes)
-  auto flush = [&](uint32_t n) {
+  // one survivor to the segment (lanes of `ok`; the whole wave calls it)
+  auto append_direct = [&](bool ok, uint32_t key, uint32_t idx) {
+    const uint64_t s = __ballot(ok);
+    if (s == 0) return;
     uint32_t base = 0;
-    if (lane == 0) base = atomicAdd(seg_counter, n);
-    base = __shfl(base, 0, kWave);
-    for (uint32_t q = lane; q < n; q += kWave) {
-      const uint32_t key = wkey[q], gp = base + q;
+    if (lane == 0) base = atomicAdd(seg_counter, static_cast<uint32_t>(__popcll(s)));
+    base = __builtin_amdgcn_readfirstlane(base);  // the whole wave is active here: lane 0's
+    if (ok) {
+      const uint32_t gp = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(s >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(s), base));
       note(key);
       if (gp < a.seg_cap) {
         seg_key[gp] = key;
-        seg_idx[gp] = widx[q];
+        seg_idx[gp] = idx;
       }
     }
   };
-  float* const stage = reinterpret_cast<float*>(&tl) + w * (32 * kWave);
-  static_assert(kSaeBS / kWave * 32 * kWave * 4 <= sizeof(SaeTileLds), "epilogue stage");
-  const XcdTiles xt(a.tiles_m, a.tiles_n);
-  for (uint32_t tl_i = xt.first; tl_i < xt.count; tl_i += xt.stride) {
-    uint32_t m0, n0;
-    xt.tile(tl_i, m0, n0);
-    // the lane's two columns: threshold, bias (loaded ahead of the MFMAs)
-    float thr[2], bias[2];
-    bool pass_all[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t c = n0 + sae_col(lane, w, j), cc = min(c, a.g.d_dict - 1);
-      const bool colok = c < a.g.d_dict;
-      const float th = a.thr[cc], bi = a.g.bias[cc];  // unconditional loads, then the column check
-      thr[j] = colok ? th : __uint_as_float(0x7FC00000u);
-      bias[j] = colok ? bi : 0.0f;
-      pass_all[j] = all && colok;
-    }
-    if (wcnt > kSaeSlice / 2) {
-      flush(wcnt);
-      wcnt = 0;
-    }
-    f32x16 acc[2][2];
-    sae_tile_mma(a.g, m0, n0, tl, acc);
-    const uint32_t wcnt0 = wcnt;
-    if (!all && m0 + kSaeBM <= a.g.B) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float av = acc[i][j][v];
-            const bool ok = av >= thr[j];
-            const uint64_t s = __ballot(ok);
-            if (s == 0) continue;
-            if (ok) {
-              const uint32_t pos =
-                  wcnt + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(s >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(s), 0u));
-              if (pos < kSaeSlice) {
-                wkey[pos] = key_f32(__float_as_uint(sae_relu(av + bias[j])));
-                widx[pos] = (m0 + sae_row(lane, w, i, v)) * a.g.d_dict + n0 + sae_col(lane, w, j);
-              }
-            }
-            wcnt += static_cast<uint32_t>(__popcll(s));
-          }
-      if (wcnt <= kSaeSlice) continue;
-      wcnt = wcnt0;  // the slice overflowed: drop this tile's entries, redo it below
-    }
-    // General epilogue, per half i: the lane's 32 accumulators through the
-    // wave's 8 KB of the (idle) tile buffers; element e = 16 j + v.
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const f32x16& src = acc[i][q >> 2];
-        const int v0 = 4 * (q & 3);
-        *reinterpret_cast<float4*>(&stage[lane * 32 + 4 * q]) =
-            make_float4(src[v0], src[v0 + 1], src[v0 + 2], src[v0 + 3]);
+  // key and flat index of element e = 32 (2 j + i) + ... (see epilogue) of a
+  // lane, from its accumulator value and the tile's column table
+  auto survivor = [&](float av, uint32_t e, uint32_t l, const float2* cols, uint32_t m0, uint32_t n0, uint32_t& key,
+                      uint32_t& idx) {
+    const uint32_t j = e >> 5, i = (e >> 4) & 1, v = e & 15;
+    const uint32_t row = m0 + wm * 64 + i * 32 + 8 * (v / 4) + 4 * (l >> 5) + (v % 4);
+    const uint32_t cl = wn * 128 + j * 32 + (l & 31);
+    key = key_f32(__float_as_uint(sae_relu(av + cols[cl].y)));
+    idx = row * dd + n0 + cl;
+  };
+  // A tile's slice is appended to the segment while the next tile's MFMAs
+  // run: the position (one atomic per wave) is requested at that tile's
+  // start and used after its first chunk, whose wait covers it.
+  uint32_t pend = 0, pm0 = 0, pn0 = 0, ppar = 0;  // the slice's survivors and their tile
+  uint32_t pbase = 0;                             // lane 0: the segment position for them
+  auto request_pending = [&]() {
+    if (pend && lane == 0) pbase = atomicAdd(seg_counter, pend);
+  };
+  auto flush_pending = [&]() {
+    if (pend == 0) return;
+    const uint32_t base = __builtin_amdgcn_readfirstlane(pbase);  // the whole wave is active here
+    for (uint32_t q = lane; q < pend; q += kWave) {
+      const uint2 en = wslice[q];
+      const uint32_t gp = base + q;
+      uint32_t key, idx;
+      survivor(__uint_as_float(en.x), en.y >> 6, en.y & 63, s_col[ppar], pm0, pn0, key, idx);
+      note(key);
+      if (gp < a.seg_cap) {
+        seg_key[gp] = key;
+        seg_idx[gp] = idx;
       }
-      for (uint32_t e = 0; e < 32; ++e) {
-        const uint32_t j = e >> 4, v = e & 15;
-        const float av = stage[lane * 32 + e];
-        const uint32_t r = m0 + (w >> 1) * 64 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        const bool ok = (j ? pass_all[1] || av >= thr[1] : pass_all[0] || av >= thr[0]) && r < a.g.B;
-        const uint64_t s = __ballot(ok);
-        if (s == 0) continue;
-        uint32_t base = 0;
-        if (lane == 0) base = atomicAdd(seg_counter, static_cast<uint32_t>(__popcll(s)));
-        base = __shfl(base, 0, kWave);
-        if (ok) {
-          const uint32_t gp = base + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(s >> 32),
-                                                               __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(s), 0u));
-          const uint32_t key = key_f32(__float_as_uint(sae_relu(av + (j ? bias[1] : bias[0]))));
-          note(key);
-          if (gp < a.seg_cap) {
-            seg_key[gp] = key;
-            seg_idx[gp] = r * a.g.d_dict + n0 + (w & 1) * 64 + j * 32 + (lane & 31);
+    }
+    pend = 0;
+  };
+  // Epilogue of one tile.  Hot pass, straight-line: per element a compare,
+  // a ballot, and the survivors' (accumulator bits, element id) written to
+  // the wave's slice at their ranks (lanes without a survivor are masked
+  // off).  The slice is converted and appended later (flush_pending).  A
+  // tile whose survivors do not fit the slice is done again by the cold
+  // pass, which appends each element's survivors to the segment directly.
+  auto epilogue = [&](const float2* cols, uint32_t m0, uint32_t n0) {
+    uint32_t fill = 0;  // survivors of the tile so far (may pass kHot)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float thr = cols[sae_fcol(lane, w, j)].x;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        // the ballots of 8 elements first, so that each branch finds its
+        // mask computed
+        uint64_t sm[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sm[u] = __ballot(acc[g >> 1][j][(g & 1) * 8 + u] >= thr);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = g >> 1, v = (g & 1) * 8 + u;
+          const uint32_t e = (2 * j + i) * 16 + v;
+          const uint64_t s = sm[u];
+          // most elements have no survivor: that case falls through
+          if (__builtin_expect(s == 0, 1)) continue;
+          const float av = acc[i][j][v];
+          if (av >= thr) {
+            // the empty asm keeps the id inside the branch: it does not
+            // depend on the tile, and hoisted out of the tile loop for
+            // every element it would hold 128 registers
+            uint32_t ln = lane;
+            asm volatile("" : "+v"(ln));
+            const uint32_t pos = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(s >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(s), fill));
+            wslice[min(pos, kHot)] = uint2{__float_as_uint(av), (e << 6) | ln};
           }
+          fill += static_cast<uint32_t>(__popcll(s));
         }
       }
     }
+    if (fill <= kHot) {
+      pend = fill;  // appended during the next tile's first chunks (flush_pending)
+      return;
+    }
+    // cold pass: every element again, straight to the segment
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float thr = cols[sae_fcol(lane, w, j)].x;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const uint32_t e = (2 * j + i) * 16 + v;
+          const float av = acc[i][j][v];
+          const bool ok = av >= thr;
+          uint32_t key = 0, idx = 0;
+          if (ok) survivor(av, e, lane, cols, m0, n0, key, idx);
+          append_direct(ok, key, idx);
+        }
+    }
+  };
+
+  const XcdTiles xt(a.tiles_m, a.tiles_n);
+  auto tile_of = [&](uint32_t t, uint32_t& m0, uint32_t& n0) {
+    m0 = (t / xt.nx) * kSaeFBM;
+    n0 = (xt.nlo + t % xt.nx) * kSaeFBN;
+  };
+  Frag F0, F1;
+  bool primed = false;  // the tile's chunk 0 is in stage 0, awaited behind a barrier
+  uint32_t par = 0;     // parity of the tile in this workgroup's sequence
+  for (uint32_t t = xt.first; t < xt.count; t += xt.stride, par ^= 1) {
+    uint32_t m0, n0, nm0 = 0, nn0 = 0;
+    tile_of(t, m0, n0);
+    const bool has_next = t + xt.stride < xt.count;
+    if (has_next) tile_of(t + xt.stride, nm0, nn0);
+    // the tile's {threshold, bias} into s_col[par] (2 KB, wave 0).  A wait
+    // and barrier of this tile before its epilogue cover it; its last
+    // readers, two tiles back (the epilogue, and the slice's append in the
+    // next tile) are behind a barrier: the one that ends chunk 1 of the tile
+    // before this one when the tile is primed, else the prologue's first.
+    auto load_cols = [&]() {
+      if (w == 0) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4*>(a.col + n0) + q * kWave + lane,
+                                           reinterpret_cast<uint4*>(s_col[par]) + q * kWave, 16, 0, 0);
+      }
+    };
+    request_pending();
+    if (!primed) {
+      // this tile's first two chunks; a barrier first, after which no wave
+      // still reads the stages (the previous tile's fragment reads)
+      wait_loads_lds();
+      __builtin_amdgcn_s_barrier();
+      load_cols();
+      issue(I0{}, m0, n0, 0);
+      if (nchunk > 1) issue(I1{}, m0, n0, 1);
+      // all loads (a masked-off load instruction is not counted)
+      wait_loads_lds();
+      __builtin_amdgcn_s_barrier();
+    } else {
+      load_cols();
+    }
+    rd(I0{}, 0, F0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    const bool cross = CROSS && has_next;
+    // chunk c in stage S, its first fragments in F0
+    auto chunk = [&](auto S, uint32_t c) {
+      constexpr int st = decltype(S)::value;
+#pragma unroll
+      for (int ks = 0; ks + 1 < kSaeFKS; ++ks) {
+        if (ks % 2 == 0) rd(S, ks + 1, F1);
+        else rd(S, ks + 1, F0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (ks % 2 == 0) mma(F0);
+        else mma(F1);
+        __builtin_amdgcn_sched_barrier(0);
+        // the previous tile's slice, while these MFMAs run: in chunk 1,
+        // after the wait that ends chunk 0 (chunk 0 when there is no other)
+        if (ks == 0 && c == (nchunk > 1 ? 1u : 0u)) flush_pending();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      mma(F1);  // the last k-step (kSaeFKS is even)
+      __builtin_amdgcn_sched_barrier(0);
+      // the next chunk: c + 1 here, or chunk 0 of the next tile (CROSS)
+      const bool here = c + 1 < nchunk;
+      if (here || cross) {
+        wait_loads_lds();
+        __builtin_amdgcn_s_barrier();
+        // stage st is free: the chunk after the next one
+        if (c + 2 < nchunk) issue(S, m0, n0, c + 2);
+        else if (cross && c + 2 - nchunk < nchunk) issue(S, nm0, nn0, c + 2 - nchunk);
+        // the next tile's first fragments are read after the epilogue, so
+        // that they do not hold registers through it
+        if (here) rd(std::integral_constant<int, 1 - st>{}, 0, F0);
+      }
+    };
+    for (uint32_t c = 0; c < nchunk; c += 2) {
+      chunk(I0{}, c);
+      if (c + 1 < nchunk) chunk(I1{}, c + 1);
+    }
+    primed = cross;
+    epilogue(s_col[par], m0, n0);
+    pm0 = m0;
+    pn0 = n0;
+    ppar = par;
   }
-  if (wcnt) flush(wcnt);
-  const uint32_t wm = wave_max_u32(my_max);
-  if (lane == 0) s_wmax[w] = wm;
+  request_pending();
+  flush_pending();
+  const uint32_t wmx = wave_max_u32(my_max);
+  if (lane == 0) s_wmax[w] = wmx;
   __syncthreads();
   uint32_t m = 0;
 #pragma unroll
@@ -667,7 +915,7 @@ static uint32_t sae_grid(uint32_t tiles) {
 SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int num_cus) {
   SaeLayout S;
   S.flat = flat_layout(plan, PROFK_F32, num_cus);
-  S.G = sae_grid(cdiv_s(B, kSaeBM) * cdiv_s(d_dict, kSaeBN));
+  S.G = sae_grid(cdiv_s(B, kSaeFBM) * cdiv_s(d_dict, kSaeFBN));
   if (S.G > S.flat.G_f) S.G = S.flat.G_f >= kXcds ? S.flat.G_f / kXcds * kXcds : S.flat.G_f;  // blk_max: G_f entries
   const uint32_t Sn = static_cast<uint32_t>(plan.S), t = static_cast<uint32_t>(plan.t);
   S.G_u = cdiv_s(Sn, kSaeUnionPer);
@@ -676,7 +924,7 @@ SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int 
   S.union_n_u = (S.G_u - 1) * S.tcap_u + (t < last_nb ? t : last_nb);  // fits the vector path's union area
   S.off_skeys = (S.flat.bytes + 255) & ~static_cast<size_t>(255);
   S.off_thr = (S.off_skeys + static_cast<size_t>(Sn) * 4 + 255) & ~static_cast<size_t>(255);
-  S.off_dense = (S.off_thr + static_cast<size_t>(d_dict) * 4 + 255) & ~static_cast<size_t>(255);
+  S.off_dense = (S.off_thr + static_cast<size_t>(cdiv_s(d_dict, kSaeFBN)) * kSaeFBN * 8 + 255) & ~static_cast<size_t>(255);
   S.bytes = S.off_dense + static_cast<size_t>(B) * d_dict * 4;
   return S;
 }
@@ -734,15 +982,19 @@ hipError_t launch_sae_topk(const SaeCall& c) {
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_select_tau(uk, c.L.union_n_u, static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess)
     return e;
-  float* thr = reinterpret_cast<float*>(ws + c.L.off_thr);
-  hipLaunchKernelGGL(k_sae_thresholds, dim3(cdiv_s(c.d_dict, 256)), dim3(256), 0, c.stream, st, c.bias, c.d_dict,
-                     thr);
+  float2* col = reinterpret_cast<float2*>(ws + c.L.off_thr);
+  const uint32_t d_pad = cdiv_s(c.d_dict, kSaeFBN) * kSaeFBN;
+  hipLaunchKernelGGL(k_sae_thresholds, dim3(d_pad / 256), dim3(256), 0, c.stream, st, c.bias, c.d_dict, d_pad, col);
   const uint32_t tm = cdiv_s(c.B, kSaeBM), tn = cdiv_s(c.d_dict, kSaeBN);
-  SaeFilterArgs fa{g, tm, tn, st, L.seg_cap, seg_cnt,
+  const uint32_t ftm = cdiv_s(c.B, kSaeFBM), ftn = cdiv_s(c.d_dict, kSaeFBN);
+  SaeFilterArgs fa{g, ftm, ftn, st, L.seg_cap, seg_cnt,
                    reinterpret_cast<uint32_t*>(ws + L.off_seg_key), reinterpret_cast<uint32_t*>(ws + L.off_seg_idx),
-                   reinterpret_cast<uint32_t*>(ws + L.off_blk_max), fhist, thr};
+                   reinterpret_cast<uint32_t*>(ws + L.off_blk_max), fhist, col};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
-  hipLaunchKernelGGL(k_sae_filter, dim3(c.L.G), dim3(kSaeBS), 0, c.stream, fa);
+  // the next tile's loads overlap the epilogue when the chunks of a tile
+  // are even in number (chunk c is then in stage c % 2 in every tile)
+  if ((c.d_model / kSaeFK) % 2 == 0) hipLaunchKernelGGL(k_sae_filter<true>, dim3(c.L.G), dim3(kSaeBS), 0, c.stream, fa);
+  else hipLaunchKernelGGL(k_sae_filter<false>, dim3(c.L.G), dim3(kSaeBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
   // the dense latents only when the candidates do not suffice (exact fallback)
   SaeDenseArgs da{g, tm, tn, dense, seg_cnt, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M)};
