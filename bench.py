@@ -444,6 +444,38 @@ def read_probe(pk, torch, x, per_cu, loads, reps=10):
     return ms, x.numel() * x.element_size() / (ms * 1e-3) / 1e9
 
 
+def graph_leg(w, torch, steps, warmup):
+    """The same step captured once in a HIP graph and replayed: per-step time
+    without the host's launch overhead between the kernels, and whether every
+    replay left the eager step's outputs (values, indices, reports)."""
+    outs = [w.out[0], w.out[1], w.info]
+    ref = [o.clone() for o in outs]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        w.step()  # the capture stream's first use, outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        w.step()
+    for o in outs:  # eager work between the capture and the replays
+        o.fill_(-7 if o.dtype == torch.int64 else 0)
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    equal = all(bool(torch.equal(a, b)) for a, b in zip(outs, ref))
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        g.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    equal = equal and all(bool(torch.equal(a, b)) for a, b in zip(outs, ref))
+    del g
+    return start.elapsed_time(stop) / steps, equal
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -460,6 +492,8 @@ def main():
     ap.add_argument("--no-torch-baseline", action="store_true")
     ap.add_argument("--no-copy-probe", action="store_true")
     ap.add_argument("--no-read-probe", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the graph-replay leg (the step captured once in a HIP graph)")
     ap.add_argument("--lexicographic", action="store_true",
                     help="plan with the tie-exact filter rule on (key, -index) pairs")
     ap.add_argument("--write-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
@@ -579,6 +613,12 @@ def main():
                            "ms": round(u_ms, 4), "values_equal": bool(torch.equal(w.out_flat[0], w.out[0])),
                            "indices_equal": bool(torch.equal(w.out_flat[1], w.out[1])),
                            "speedup_of_fused": round(u_ms / ms_per_step, 3)}
+
+    if not args.no_graph:
+        g_ms, g_equal = graph_leg(w, torch, args.steps, max(5, args.warmup))
+        line["graph"] = {"what": "the same step captured once in a HIP graph and replayed",
+                         "ms_per_step": round(g_ms, 5), "value": round(w.in_bytes / (g_ms * 1e-3) / 1e9, 2),
+                         "outputs_equal_eager": g_equal}
 
     if args.cold:
         flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")

@@ -8,15 +8,17 @@
 // The latent matrix is never written to HBM:
 //   k_sae_sample   stage 1: the S sampled latents, each computed with the same
 //                  MFMA sequence as the GEMM (so its value is the GEMM's, bit
-//                  for bit), and each sample workgroup's top-t of them;
-//   k_select_tau   stage 2 (shared with the vector path);
-//   k_sae_thresholds  each column's accumulator threshold for tau;
+//                  for bit);
+//   k_select_tau   stage 2 (shared with the vector path), over the S keys;
+//   k_sae_thresholds  each column's accumulator threshold for tau, with its
+//                  bias;
 //   k_sae_filter   the GEMM with stage 3 in its epilogue: survivors are
-//                  compacted exactly as the vector filter does it, so the
-//                  vector path's refinement (stage 4) runs unchanged;
-//   k_sae_dense    the GEMM with a dense epilogue: for the exact fallback only
-//                  (it returns at once when the filter's count is in range),
-//                  and as an inspection entry point.
+//                  compacted as the vector filter does it, so the vector
+//                  path's refinement (stage 4) runs unchanged;
+//   k_sae_dense    the same GEMM with a dense epilogue: for the exact
+//                  fallback (it returns at once when the filter's count is in
+//                  range), for plans without sampling, and as an inspection
+//                  entry point.
 // Sparse decode (k_dec_*): x_hat[b, :] = sum over b's selected latents of
 // z W_dec[j, :] + b_dec, grouped by row and summed in ascending j, so the
 // result does not depend on the order the selection lists them in.
@@ -35,18 +37,10 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 
-// GEMM tiling: a workgroup of 8 waves computes a 256 x 128 tile of z (waves
-// in a 4 x 2 grid, 64 x 64 each as 2 x 2 32x32 MFMA accumulators); d_model
-// is consumed in chunks of 64, double-buffered in LDS (rows padded to 144 B)
-// with one barrier per chunk: the next chunk's global loads are in flight,
-// and then written to the other buffer, while this chunk's MFMAs run.
-constexpr int kSaeBS = 512;
-constexpr uint32_t kSaeBM = 256, kSaeBN = 128, kSaeBK = 64;
-constexpr uint32_t kSaeLd = kSaeBK + 8;  // LDS row stride in bf16 elements
+constexpr int kSaeBS = 512;              // threads of a GEMM workgroup (8 waves)
+constexpr uint32_t kSaeBK = 64;           // d_model chunk of the sample kernel
+constexpr uint32_t kSaeLd = kSaeBK + 8;   // its LDS row stride in bf16 elements
 constexpr uint32_t kSaeMaxBlocks = 1024;
-constexpr int kSaeApieces = kSaeBM * kSaeBK / 8 / kSaeBS;  // 16-byte pieces per thread and chunk
-constexpr int kSaeBpieces = kSaeBN * kSaeBK / 8 / kSaeBS;
-static_assert(kSaeBS / kWave == (kSaeBM / 64) * (kSaeBN / 64), "one wave per 64 x 64 block");
 
 struct SaeGemm {
   const uint16_t* x;  // [B, d_model] bf16 bits, 16-byte aligned rows
@@ -55,117 +49,8 @@ struct SaeGemm {
   uint32_t B, d_model, d_dict;
 };
 
-struct alignas(16) SaeTileLds {
-  uint16_t a[2][kSaeBM * kSaeLd];
-  uint16_t b[2][kSaeBN * kSaeLd];
-};
-
 __device__ __forceinline__ float sae_relu(float pre) { return pre > 0.0f ? pre : 0.0f; }
 
-// acc[i][j] = this wave's 64x64 part of the product for the tile at (m0, n0).
-// Ends with a barrier, after which the tile buffers are free.
-__device__ __forceinline__ void sae_tile_mma(const SaeGemm& g, uint32_t m0, uint32_t n0, SaeTileLds& sh,
-                                             f32x16 (&acc)[2][2]) {
-  const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-  const uint32_t wm = w >> 1, wn = w & 1;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  const uint32_t nchunk = g.d_model / kSaeBK;
-  // piece id = q * kSaeBS + tid is row id / 8, 16-byte segment id % 8 of the
-  // chunk.  Two register sets hold the chunks in flight: chunk c + 2 is
-  // loaded while chunk c is computed and stored to LDS after chunk c + 1 is.
-  // Rows past B and columns past d_dict load the last row or column instead
-  // (no branch around a load, so the loads' waits stay exact): they only
-  // feed accumulators of rows and columns the epilogues skip.
-  u32x4v ra[2][kSaeApieces], rb[2][kSaeBpieces];
-  auto gload = [&](uint32_t kc, u32x4v (&xa)[kSaeApieces], u32x4v (&xb)[kSaeBpieces]) {
-    const size_t col = static_cast<size_t>(kc) * kSaeBK;
-#pragma unroll
-    for (int q = 0; q < kSaeApieces; ++q) {
-      const uint32_t id = q * kSaeBS + tid, gm = min(m0 + (id >> 3), g.B - 1);
-      xa[q] = *reinterpret_cast<const u32x4v*>(g.x + static_cast<size_t>(gm) * g.d_model + col + (id & 7) * 8);
-    }
-#pragma unroll
-    for (int q = 0; q < kSaeBpieces; ++q) {
-      const uint32_t id = q * kSaeBS + tid, gn = min(n0 + (id >> 3), g.d_dict - 1);
-      xb[q] = *reinterpret_cast<const u32x4v*>(g.w + static_cast<size_t>(gn) * g.d_model + col + (id & 7) * 8);
-    }
-  };
-  auto lstore = [&](uint32_t buf, const u32x4v (&xa)[kSaeApieces], const u32x4v (&xb)[kSaeBpieces]) {
-#pragma unroll
-    for (int q = 0; q < kSaeApieces; ++q) {
-      const uint32_t id = q * kSaeBS + tid;
-      *reinterpret_cast<u32x4v*>(&sh.a[buf][(id >> 3) * kSaeLd + (id & 7) * 8]) = xa[q];
-    }
-#pragma unroll
-    for (int q = 0; q < kSaeBpieces; ++q) {
-      const uint32_t id = q * kSaeBS + tid;
-      *reinterpret_cast<u32x4v*>(&sh.b[buf][(id >> 3) * kSaeLd + (id & 7) * 8]) = xb[q];
-    }
-  };
-  auto compute = [&](uint32_t buf) {
-#pragma unroll
-    for (uint32_t ks = 0; ks < kSaeBK / 16; ++ks) {
-      const uint32_t kofs = ks * 16 + 8 * (lane >> 5);
-      bf16x8 fa[2], fb[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        fa[i] = *reinterpret_cast<const bf16x8*>(&sh.a[buf][(wm * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
-        fb[i] = *reinterpret_cast<const bf16x8*>(&sh.b[buf][(wn * 64 + i * 32 + (lane & 31)) * kSaeLd + kofs]);
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
-  };
-  __syncthreads();  // the previous tile's epilogue is done with the buffers
-  gload(0, ra[0], rb[0]);
-  lstore(0, ra[0], rb[0]);
-  if (nchunk > 1) gload(1, ra[1], rb[1]);
-  __syncthreads();
-  // Chunk c is in LDS buffer c % 2 and register set c % 2.  The steady loop
-  // has no branch around its loads, so the compiler's waits before each LDS
-  // store cover that set's loads only and chunk c + 2 stays in flight; the
-  // last one to three chunks are peeled off.
-  // (sched_barrier keeps the compiler from sinking the loads below the
-  // MFMAs, which would shorten their lead to under one chunk.)
-  uint32_t kc = 0;
-  for (; kc + 3 < nchunk; kc += 2) {
-    gload(kc + 2, ra[0], rb[0]);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(0);
-    lstore(1, ra[1], rb[1]);  // buffer 1 was last read before the previous barrier
-    __syncthreads();
-    gload(kc + 3, ra[1], rb[1]);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(1);
-    lstore(0, ra[0], rb[0]);  // buffer 0 was read before the barrier above
-    __syncthreads();
-  }
-  if (kc + 2 < nchunk) {  // chunks kc, kc + 1, kc + 2
-    gload(kc + 2, ra[0], rb[0]);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(0);
-    lstore(1, ra[1], rb[1]);
-    __syncthreads();
-    compute(1);
-    lstore(0, ra[0], rb[0]);
-    __syncthreads();
-    compute(0);
-  } else if (kc + 1 < nchunk) {  // chunks kc, kc + 1
-    compute(0);
-    lstore(1, ra[1], rb[1]);
-    __syncthreads();
-    compute(1);
-  } else {  // chunk kc
-    compute(0);
-  }
-  __syncthreads();
-}
 
 // XCD-aware tile order.  Workgroups are dispatched to the 8 XCDs round-robin
 // (workgroup b runs on XCD b % 8), each XCD with its own L2.  The grid is a
@@ -188,27 +73,12 @@ struct XcdTiles {
     first = blockIdx.x / V;
     stride = gridDim.x / V;
   }
-  __device__ __forceinline__ void tile(uint32_t t, uint32_t& m0, uint32_t& n0) const {
-    m0 = (t / nx) * kSaeBM;
-    n0 = (nlo + t % nx) * kSaeBN;
-  }
 };
 
-// Tile-local row and column of accumulator element v of block (i, j).
-__device__ __forceinline__ uint32_t sae_row(uint32_t lane, uint32_t w, int i, int v) {
-  return (w >> 1) * 64 + i * 32 + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
-}
-__device__ __forceinline__ uint32_t sae_col(uint32_t lane, uint32_t w, int j) {
-  return (w & 1) * 64 + j * 32 + (lane & 31);
-}
 
 // ------------------------------------------------------------ stage 1 -----
-// k_sae_sample: every draw's latent key, into skeys[S].  k_sae_union: each
-// workgroup of 1024 threads takes 4096 of them and keeps its top-t (the
-// union stays small enough for one workgroup to select tau from in LDS even
-// when t is in the hundreds).
-constexpr int kSaeUnionBS = 1024;
-constexpr uint32_t kSaeUnionPer = 4 * kSaeUnionBS;
+// k_sae_sample: every draw's latent key, into skeys[S]; k_select_tau then
+// takes the t-th largest of them.
 
 struct SaeSampleArgs {
   SaeGemm g;
@@ -289,27 +159,6 @@ __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
   if (in && (lane >> 5) == ((i >> 2) & 1)) a.skeys[j] = key_f32(__float_as_uint(sae_relu(d + a.g.bias[c])));
 }
 
-struct SaeUnionArgs {
-  const uint32_t* skeys;
-  uint32_t S, t, tcap;
-  uint32_t* union_keys;
-};
-
-__global__ __launch_bounds__(kSaeUnionBS) void k_sae_union(SaeUnionArgs a) {
-  __shared__ SampleUnionShared<kSaeUnionBS> sh;
-  const uint32_t b = blockIdx.x, tid = threadIdx.x;
-  const uint32_t j0 = b * kSaeUnionPer;
-  const uint32_t nb = min(kSaeUnionPer, a.S - j0);
-  uint32_t kv[4];
-  uint32_t valid = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const uint32_t j = 4 * tid + q;
-    kv[q] = j < nb ? a.skeys[j0 + j] : 0u;
-    if (j < nb) valid |= 1u << q;
-  }
-  sample_block_top<kSaeUnionBS, 32>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
-}
 
 // ------------------------------------------------------- thresholds ------
 // A latent relu(acc + b_enc[j]) survives iff its key is >= tau.  With tau
@@ -432,8 +281,24 @@ __device__ __forceinline__ uint32_t sae_fcol(uint32_t lane, uint32_t w, int j) {
 // wait is vmcnt(0) (with lgkmcnt(0), which also completes this wave's
 // fragment reads of the stage refilled after the barrier); the barrier then
 // covers the other waves' loads and reads.
-template <bool CROSS>
-__global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
+// The dense variant (DENSE) runs the same GEMM and writes every latent
+// relu(acc + b_enc[j]) to d.out instead of filtering; given d.chk it first
+// returns when the candidate count there is within [k_req, M] (the exact
+// fallback's case only).
+struct SaeDenseOut {
+  float* out;               // [B, d_dict]
+  const uint32_t* chk;      // null: always write; else the filter's segment counters
+  uint32_t k_req, M;
+};
+
+template <bool CROSS, bool DENSE>
+__device__ __forceinline__ void sae_gemm_body(const SaeFilterArgs& a, const SaeDenseOut& d) {
+  if (DENSE && d.chk) {
+    uint32_t total = 0;
+#pragma unroll
+    for (int x = 0; x < kSegs; ++x) total += d.chk[x * kSegStride];
+    if (total >= d.k_req && total <= d.M) return;  // filtered: the candidates suffice
+  }
   // distinct arrays per stage, so that the compiler can tell the stage being
   // read from the one being filled
   __shared__ __align__(16) uint4 sA0[kSaeFGran], sA1[kSaeFGran], sB0[kSaeFGran], sB1[kSaeFGran];
@@ -447,8 +312,9 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
   const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const uint32_t wm = w >> 1, wn = w & 1;
   const uint32_t seg = b & (kSegs - 1);
-  const uint32_t tau = a.st->tau_key;
-  for (uint32_t i = tid; i < kLogBins; i += kSaeBS) s_hist[i] = 0;  // complete before the first barrier
+  const uint32_t tau = DENSE ? 0u : a.st->tau_key;
+  if (!DENSE)
+    for (uint32_t i = tid; i < kLogBins; i += kSaeBS) s_hist[i] = 0;  // complete before the first barrier
   uint32_t* const seg_counter = a.seg_cnt + seg * kSegStride;
   uint32_t* const seg_key = a.seg_key + static_cast<size_t>(seg) * a.seg_cap;
   uint32_t* const seg_idx = a.seg_idx + static_cast<size_t>(seg) * a.seg_cap;
@@ -566,10 +432,10 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
   uint32_t pend = 0, pm0 = 0, pn0 = 0, ppar = 0;  // the slice's survivors and their tile
   uint32_t pbase = 0;                             // lane 0: the segment position for them
   auto request_pending = [&]() {
-    if (pend && lane == 0) pbase = atomicAdd(seg_counter, pend);
+    if (!DENSE && pend && lane == 0) pbase = atomicAdd(seg_counter, pend);
   };
   auto flush_pending = [&]() {
-    if (pend == 0) return;
+    if (DENSE || pend == 0) return;
     const uint32_t base = __builtin_amdgcn_readfirstlane(pbase);  // the whole wave is active here
     for (uint32_t q = lane; q < pend; q += kWave) {
       const uint2 en = wslice[q];
@@ -583,6 +449,25 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
       }
     }
     pend = 0;
+  };
+  // the dense variant's epilogue: every latent of the tile that is in range
+  auto write_dense = [&](uint32_t m0, uint32_t n0) {
+    const uint32_t r0 = m0 + wm * 64 + 4 * (lane >> 5);
+    const bool full = m0 + kSaeFBM <= B;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t c = n0 + sae_fcol(lane, w, j);
+      if (c >= dd) continue;
+      const float bias = a.g.bias[c];
+      float* const o = d.out + static_cast<size_t>(r0) * dd + c;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const uint32_t ro = i * 32 + 8 * (v / 4) + (v % 4);
+          if (full || r0 + ro < B) o[static_cast<size_t>(ro) * dd] = sae_relu(acc[i][j][v] + bias);
+        }
+    }
   };
   // Epilogue of one tile.  Hot pass, straight-line: per element a compare,
   // a ballot, and the survivors' (accumulator bits, element id) written to
@@ -665,7 +550,7 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
     // next tile) are behind a barrier: the one that ends chunk 1 of the tile
     // before this one when the tile is primed, else the prologue's first.
     auto load_cols = [&]() {
-      if (w == 0) {
+      if (!DENSE && w == 0) {
 #pragma unroll
         for (int q = 0; q < 2; ++q)
           __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4*>(a.col + n0) + q * kWave + lane,
@@ -729,11 +614,13 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
       if (c + 1 < nchunk) chunk(I1{}, c + 1);
     }
     primed = cross;
-    epilogue(s_col[par], m0, n0);
+    if constexpr (DENSE) write_dense(m0, n0);
+    else epilogue(s_col[par], m0, n0);
     pm0 = m0;
     pn0 = n0;
     ppar = par;
   }
+  if constexpr (DENSE) return;
   request_pending();
   flush_pending();
   const uint32_t wmx = wave_max_u32(my_max);
@@ -751,47 +638,17 @@ __global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
   }
 }
 
-// ------------------------------------------------------------- dense ------
-struct SaeDenseArgs {
-  SaeGemm g;
-  uint32_t tiles_m, tiles_n;
-  float* out;               // [B, d_dict]
-  const uint32_t* seg_cnt;  // null: always write; else only when the count is outside [k_req, M]
-  uint32_t k_req, M;
-};
-
-__global__ __launch_bounds__(kSaeBS) void k_sae_dense(SaeDenseArgs a) {
-  __shared__ SaeTileLds tl;
-  if (a.seg_cnt) {
-    uint32_t total = 0;
-#pragma unroll
-    for (int x = 0; x < kSegs; ++x) total += a.seg_cnt[x * kSegStride];
-    if (total >= a.k_req && total <= a.M) return;  // filtered: the candidates suffice
-  }
-  const uint32_t lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
-  const XcdTiles xt(a.tiles_m, a.tiles_n);
-  for (uint32_t tl_i = xt.first; tl_i < xt.count; tl_i += xt.stride) {
-    uint32_t m0, n0;
-    xt.tile(tl_i, m0, n0);
-    float bias[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) bias[j] = a.g.bias[min(n0 + sae_col(lane, w, j), a.g.d_dict - 1)];
-    f32x16 acc[2][2];
-    sae_tile_mma(a.g, m0, n0, tl, acc);
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t c = n0 + sae_col(lane, w, j);
-      if (c >= a.g.d_dict) continue;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const uint32_t r = m0 + sae_row(lane, w, i, v);
-          if (r < a.g.B) a.out[static_cast<size_t>(r) * a.g.d_dict + c] = sae_relu(acc[i][j][v] + bias[j]);
-        }
-    }
-  }
+template <bool CROSS>
+__global__ __launch_bounds__(kSaeBS) void k_sae_filter(SaeFilterArgs a) {
+  sae_gemm_body<CROSS, false>(a, SaeDenseOut{});
 }
+
+template <bool CROSS>
+__global__ __launch_bounds__(kSaeBS) void k_sae_dense(SaeFilterArgs a, SaeDenseOut d) {
+  sae_gemm_body<CROSS, true>(a, d);
+}
+
+// ------------------------------------------------------------- dense ------
 
 // ------------------------------------------------------------ decode ------
 // Selected latents grouped by row: counts, offsets, a scatter, then one
@@ -917,11 +774,7 @@ SaeLayout sae_layout(const profk_plan_t& plan, uint32_t B, uint32_t d_dict, int 
   S.flat = flat_layout(plan, PROFK_F32, num_cus);
   S.G = sae_grid(cdiv_s(B, kSaeFBM) * cdiv_s(d_dict, kSaeFBN));
   if (S.G > S.flat.G_f) S.G = S.flat.G_f >= kXcds ? S.flat.G_f / kXcds * kXcds : S.flat.G_f;  // blk_max: G_f entries
-  const uint32_t Sn = static_cast<uint32_t>(plan.S), t = static_cast<uint32_t>(plan.t);
-  S.G_u = cdiv_s(Sn, kSaeUnionPer);
-  S.tcap_u = t < kSaeUnionPer ? t : kSaeUnionPer;
-  const uint32_t last_nb = Sn - (S.G_u - 1) * kSaeUnionPer;
-  S.union_n_u = (S.G_u - 1) * S.tcap_u + (t < last_nb ? t : last_nb);  // fits the vector path's union area
+  const uint32_t Sn = static_cast<uint32_t>(plan.S);
   S.off_skeys = (S.flat.bytes + 255) & ~static_cast<size_t>(255);
   S.off_thr = (S.off_skeys + static_cast<size_t>(Sn) * 4 + 255) & ~static_cast<size_t>(255);
   S.off_dense = (S.off_thr + static_cast<size_t>(cdiv_s(d_dict, kSaeFBN)) * kSaeFBN * 8 + 255) & ~static_cast<size_t>(255);
@@ -934,11 +787,27 @@ static SaeGemm gemm_of(const SaeCall& c) {
                  c.d_dict};
 }
 
+// Filter-tile arguments for the dense variant: only the GEMM and the tiles.
+static SaeFilterArgs dense_args(const SaeCall& c) {
+  SaeFilterArgs fa{};
+  fa.g = gemm_of(c);
+  fa.tiles_m = cdiv_s(c.B, kSaeFBM);
+  fa.tiles_n = cdiv_s(c.d_dict, kSaeFBN);
+  return fa;
+}
+
+// The dense variant on the filter's tiles; chk as in SaeDenseOut.
+static void launch_dense_tiles(const SaeCall& c, float* out, const uint32_t* chk, uint32_t k_req, uint32_t M) {
+  const SaeFilterArgs fa = dense_args(c);
+  const SaeDenseOut d{out, chk, k_req, M};
+  const dim3 grid(sae_grid(fa.tiles_m * fa.tiles_n));
+  if ((c.d_model / kSaeFK) % 2 == 0) hipLaunchKernelGGL(k_sae_dense<true>, grid, dim3(kSaeBS), 0, c.stream, fa, d);
+  else hipLaunchKernelGGL(k_sae_dense<false>, grid, dim3(kSaeBS), 0, c.stream, fa, d);
+}
+
 hipError_t launch_sae_dense(const SaeCall& c, float* out) {
   (void)hipGetLastError();
-  const uint32_t tm = cdiv_s(c.B, kSaeBM), tn = cdiv_s(c.d_dict, kSaeBN);
-  SaeDenseArgs da{gemm_of(c), tm, tn, out, nullptr, 0, 0};
-  hipLaunchKernelGGL(k_sae_dense, dim3(sae_grid(tm * tn)), dim3(kSaeBS), 0, c.stream, da);
+  launch_dense_tiles(c, out, nullptr, 0, 0);
   return hipGetLastError();
 }
 
@@ -972,20 +841,16 @@ hipError_t launch_sae_topk(const SaeCall& c) {
   CallState* st = reinterpret_cast<CallState*>(ws + L.off_state);
   uint32_t* seg_cnt = reinterpret_cast<uint32_t*>(ws + L.off_segcnt);
   uint32_t* fhist = reinterpret_cast<uint32_t*>(ws + L.off_fhist);
-  uint32_t* uk = reinterpret_cast<uint32_t*>(ws + L.off_union);
   const SaeGemm g = gemm_of(c);
   hipError_t e = launch_sae_sample(c);
   if (e != hipSuccess) return e;
-  SaeUnionArgs ua{reinterpret_cast<const uint32_t*>(ws + c.L.off_skeys), static_cast<uint32_t>(p.S),
-                  static_cast<uint32_t>(p.t), c.L.tcap_u, uk};
-  hipLaunchKernelGGL(k_sae_union, dim3(c.L.G_u), dim3(kSaeUnionBS), 0, c.stream, ua);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = launch_select_tau(uk, c.L.union_n_u, static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess)
+  // tau: the t-th largest of the S sampled keys, selected by one block
+  if ((e = launch_select_tau(reinterpret_cast<const uint32_t*>(ws + c.L.off_skeys), static_cast<uint32_t>(p.S),
+                             static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess)
     return e;
   float2* col = reinterpret_cast<float2*>(ws + c.L.off_thr);
   const uint32_t d_pad = cdiv_s(c.d_dict, kSaeFBN) * kSaeFBN;
   hipLaunchKernelGGL(k_sae_thresholds, dim3(d_pad / 256), dim3(256), 0, c.stream, st, c.bias, c.d_dict, d_pad, col);
-  const uint32_t tm = cdiv_s(c.B, kSaeBM), tn = cdiv_s(c.d_dict, kSaeBN);
   const uint32_t ftm = cdiv_s(c.B, kSaeFBM), ftn = cdiv_s(c.d_dict, kSaeFBN);
   SaeFilterArgs fa{g, ftm, ftn, st, L.seg_cap, seg_cnt,
                    reinterpret_cast<uint32_t*>(ws + L.off_seg_key), reinterpret_cast<uint32_t*>(ws + L.off_seg_idx),
@@ -997,8 +862,7 @@ hipError_t launch_sae_topk(const SaeCall& c) {
   else hipLaunchKernelGGL(k_sae_filter<false>, dim3(c.L.G), dim3(kSaeBS), 0, c.stream, fa);
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
   // the dense latents only when the candidates do not suffice (exact fallback)
-  SaeDenseArgs da{g, tm, tn, dense, seg_cnt, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M)};
-  hipLaunchKernelGGL(k_sae_dense, dim3(sae_grid(tm * tn)), dim3(kSaeBS), 0, c.stream, da);
+  launch_dense_tiles(c, dense, seg_cnt, static_cast<uint32_t>(p.k_req), static_cast<uint32_t>(p.M));
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_refine(fc, c.L.G);
 }

@@ -188,7 +188,6 @@ hipError_t launch_rows(const RowCall& c);
 struct SaeLayout {
   FlatLayout flat;
   uint32_t G = 0;                                 // filter workgroups (persistent)
-  uint32_t G_u = 0, tcap_u = 0, union_n_u = 0;    // stage-1 union: 4096-draw workgroups
   size_t off_skeys = 0;                           // every draw's latent key (S words)
   size_t off_thr = 0;                             // per-column {threshold, bias}, padded to whole filter tiles
   size_t off_dense = 0, bytes = 0;

@@ -82,3 +82,23 @@ def test_graph_rows_bf16():
     call = lambda: pk.topk_rows(g, k, seed=2, p=p, ws=ws, out=out, info=info)
     call()
     _replays_equal_eager(call, [out[0].view(t.int16), out[1], info])
+
+
+def test_graph_sae_encode_topk():
+    # the fused SAE layer: sample, tau, thresholds, the GEMM with the filter
+    # in its epilogue, the fallback check and the refinement, all captured
+    t = torch()
+    B, d_model, d_dict, k_row = 512, 128, 2048, 16
+    m = workloads.sae_model(B=B, d_model=d_model, d_dict=d_dict, seed=29)
+    bf = lambda a: t.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(t.bfloat16)
+    x, w, b = bf(m["x"]), bf(m["w_enc"]), t.from_numpy(m["b_enc"]).cuda()
+    p = pk.plan_sae(B, d_dict, k_row)
+    note(f"graph sae B={B} d_model={d_model} d_dict={d_dict} K={B * k_row} S={p.S} t={p.t} M={p.M}")
+    ws = pk.sae_workspace(p, B, d_dict)
+    out = (t.empty(B * k_row, dtype=t.float32, device="cuda"),
+           t.empty(B * k_row, dtype=t.int64, device="cuda"))
+    info = t.empty(pk.INFO_BYTES, dtype=t.uint8, device="cuda")
+    call = lambda: pk.sae_encode_topk(x, w, b, k_row, seed=0, p=p, ws=ws, out=out, info=info)
+    call()
+    assert int(pk.read_info(info)[0]["status"]) == 0
+    _replays_equal_eager(call, [out[0], out[1], info])

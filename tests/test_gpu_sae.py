@@ -55,7 +55,7 @@ def _check_selection(vals, idx, z, tol, K):
     return gpu_only.size
 
 
-@pytest.mark.parametrize("B,d_model,d_dict", [(200, 128, 300), (256, 512, 1024), (1, 64, 129)])
+@pytest.mark.parametrize("B,d_model,d_dict", [(200, 128, 300), (256, 512, 1024), (1, 64, 129), (300, 192, 700)])
 def test_sae_dense_latents(B, d_model, d_dict):
     m = workloads.sae_model(B=B, d_model=d_model, d_dict=d_dict, seed=B + d_dict)
     note(f"sae dense B={B} d_model={d_model} d_dict={d_dict}")
@@ -82,7 +82,8 @@ def test_sae_sampled_latents_are_the_gemm_values():
     assert np.array_equal(keys, bits[idx] ^ 0x80000000)     # latents are >= +0: key = bits with the sign set
 
 
-@pytest.mark.parametrize("B,d_model,d_dict,k_row", [(256, 512, 2048, 32), (300, 128, 1000, 8), (128, 256, 4096, 4)])
+@pytest.mark.parametrize("B,d_model,d_dict,k_row", [(256, 512, 2048, 32), (300, 128, 1000, 8), (128, 256, 4096, 4),
+                                                   (200, 192, 700, 8), (64, 64, 513, 4)])
 def test_sae_encode_topk(B, d_model, d_dict, k_row):
     m = workloads.sae_model(B=B, d_model=d_model, d_dict=d_dict, seed=11)
     g = _dev(m)
@@ -100,6 +101,36 @@ def test_sae_encode_topk(B, d_model, d_dict, k_row):
     order = np.lexsort((np.arange(dense.size), -dense.astype(np.float64)))[:K]
     assert np.array_equal(idx.cpu().numpy(), order)
     assert np.array_equal(vals.cpu().numpy().view(np.uint32), dense[order].view(np.uint32))
+
+
+def _exact_topk_of(dense, K):
+    """Indices of the K largest of a flat fp32 array under the total order
+    (value descending, then index ascending), and their values."""
+    d64 = dense.astype(np.float64)
+    kth = np.partition(-d64, K - 1)[K - 1]            # minus the K-th largest value
+    cand = np.nonzero(-d64 <= kth)[0]                  # every index with a value >= it
+    order = cand[np.lexsort((cand, -d64[cand]))][:K]
+    return order, dense[order]
+
+
+@pytest.mark.parametrize("B,d_model,d_dict,k_row", [(4096, 128, 8192, 8), (4000, 192, 8000, 8), (4096, 64, 8192, 8)])
+def test_sae_encode_topk_several_tiles_per_workgroup(B, d_model, d_dict, k_row):
+    # more 256 x 256 filter tiles than workgroups: the next tile's loads
+    # overlap an epilogue, and a tile's survivors are appended during the
+    # next tile (an even d_model / 64), or each tile loads behind its own
+    # barrier (odd: 3 chunks, and 1); the last row and column tiles are
+    # partial in the second
+    m = workloads.sae_model(B=B, d_model=d_model, d_dict=d_dict, seed=23)
+    g = _dev(m)
+    K = B * k_row
+    p = pk.plan_sae(B, d_dict, k_row)
+    note(f"sae topk tiles B={B} d_model={d_model} d_dict={d_dict} K={K} S={p.S} t={p.t} M={p.M} mode={p.mode}")
+    vals, idx, info = pk.sae_encode_topk(g["x"], g["w_enc"], g["b_enc"], k_row, seed=3, p=p)
+    assert int(pk.read_info(info)[0]["status"]) == 0
+    dense = pk.sae_encode_dense(g["x"], g["w_enc"], g["b_enc"]).reshape(-1).cpu().numpy()
+    order, ov = _exact_topk_of(dense, K)
+    assert np.array_equal(idx.cpu().numpy(), order)
+    assert np.array_equal(vals.cpu().numpy().view(np.uint32), ov.view(np.uint32))
 
 
 def test_sae_encode_topk_default_plan():
