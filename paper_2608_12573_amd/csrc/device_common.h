@@ -541,6 +541,13 @@ __device__ __forceinline__ uint32_t log_bin(uint32_t d) {
   const uint32_t e = 31u - static_cast<uint32_t>(__clz(d));  // 7..31
   return (e - 6u) * 128u + ((d >> (e - 7u)) & 127u);
 }
+// The smallest d with log_bin(d) = b: log_bin(d) >= b exactly when
+// d >= log_bin_edge(b) (b < kLogBins).
+__device__ __forceinline__ uint32_t log_bin_edge(uint32_t b) {
+  if (b < 128u) return b;
+  const uint32_t e = b / 128u + 6u, m = b % 128u;
+  return (1u << e) | (m << (e - 7u));
+}
 
 // Bitonic sort, descending, of P = E*T 64-bit values held E per thread in
 // blocked order (thread t holds positions t*E .. t*E+E-1).  Strides below E

@@ -477,8 +477,9 @@ struct FinishArgs {
 // Refinement of a filtered call (k_req <= total <= M) by one block, from
 // the filter's histogram of log_bin(key - tau) over the candidates:
 //   1. find the bucket b* holding rank kk;
-//   2. when the candidates at or above b* are few and every such bucket is
-//      small, place them bucket by bucket in LDS and rank each one within its
+//   2. when the candidates at or above b* are few and ranking them within
+//      their buckets takes few comparisons (the squares of the bucket sizes),
+//      place them bucket by bucket in LDS and rank each one within its
 //      bucket by comparison: its output position is the bucket's first slot
 //      plus the number of larger composites in the bucket;
 //   3. otherwise run the general radix refinement.
@@ -514,44 +515,62 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
   }
   __syncthreads();
   const uint32_t bstar = fs.found[0], n_sel = fs.found[1] + fs.found[2];
-  uint32_t big = 0;
+  // comparisons the ranking takes: the squares of the bucket sizes at or
+  // above b* (each clamped so that the sum cannot wrap; a bucket that large
+  // fails n_sel <= kFastCap anyway)
+  uint32_t cost = 0;
   if (tid < kOwners) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      if (bbase + j >= bstar) big = max(big, h[j]);
+      if (bbase + j >= bstar) {
+        const uint32_t m = min(h[j], kFastCap + 1);
+        cost += m * m;
+      }
   }
-  big = block_max<kFinBS>(big, fs.wsum);
+  cost = block_sum<kFinBS>(cost, fs.wsum);
 
-  if (n_sel <= kFastCap && big <= kFastBucket) {
+  if (n_sel <= kFastCap && cost <= kFastCost) {
     // place (key, candidate number) of buckets >= b* ...: thread t takes
     // entries t % kPreThreads + kPreThreads * u of segment t / kPreThreads,
     // the first kPreU of them already in registers
     const uint32_t x = tid / kPreThreads, l = tid % kPreThreads;
     const uint32_t nx = seg_n[x], px = seg_pre[x];
+    // (every candidate's key is >= tau; a bucket >= b* is a distance from tau
+    // of at least its lower edge, so most keys take one compare)
+    const uint32_t edge = log_bin_edge(bstar);
     auto place = [&](uint32_t j, uint32_t key) {
-      const uint32_t bin = log_bin(key - tau);
-      if (bin >= bstar) {
+      const uint32_t d = key - tau;
+      if (d >= edge) {
+        const uint32_t bin = log_bin(d);
         const uint32_t slot = sh.bkt.off[bin] + atomicAdd(&sh.bkt.fill[bin], 1u);
         sh.bkt.comp[slot] = (static_cast<uint64_t>(key) << 32) | (px + j);
       }
     };
-#pragma unroll
-    for (int u = 0; u < kPreU; ++u) {
-      const uint32_t j = l + kPreThreads * u;
-      if (j < nx) place(j, pk[u]);
-    }
-    for (uint32_t base = kPreSeg; base < nx; base += kPreSeg) {
-      uint32_t kv[kPreU];
+    // sweep s + 1's keys are in flight while sweep s's are placed (two
+    // buffers taken in turn, so that placing one waits for its own loads only)
+    uint32_t ka[kPreU], kb[kPreU];
+    auto load_sweep = [&](uint32_t (&kv)[kPreU], uint32_t base) {
 #pragma unroll
       for (int u = 0; u < kPreU; ++u) {
         const uint32_t j = base + l + kPreThreads * u;
         kv[u] = j < nx ? a.seg_key[static_cast<size_t>(x) * a.seg_cap + j] : 0u;
       }
+    };
+    auto place_sweep = [&](const uint32_t (&kv)[kPreU], uint32_t base) {
 #pragma unroll
       for (int u = 0; u < kPreU; ++u) {
         const uint32_t j = base + l + kPreThreads * u;
         if (j < nx) place(j, kv[u]);
       }
+    };
+    if (kPreSeg < nx) load_sweep(ka, kPreSeg);
+    place_sweep(pk, 0);
+    for (uint32_t base = kPreSeg; base < nx; base += 2 * kPreSeg) {
+      if (base + kPreSeg < nx) load_sweep(kb, base + kPreSeg);
+      place_sweep(ka, base);
+      if (base + kPreSeg >= nx) break;
+      if (base + 2 * kPreSeg < nx) load_sweep(ka, base + 2 * kPreSeg);
+      place_sweep(kb, base + kPreSeg);
     }
     __syncthreads();
     // ... then turn them into composites, all index loads in flight at once

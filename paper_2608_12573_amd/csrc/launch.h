@@ -63,7 +63,10 @@ constexpr int kFbMaxBlocks = 256;
 constexpr int kFbGroup = 16;                  // fallback chunks merged together first
 static_assert(kFbMaxBlocks / kFbGroup <= 16, "group counters in CallState");
 constexpr uint32_t kFastCap = 8192;           // candidates the bucket refinement holds in LDS
-constexpr uint32_t kFastBucket = 128;         // largest bucket it ranks by comparison
+// It ranks each candidate within its bucket by comparison: sum over the
+// buckets at or above rank k of size^2 comparisons in all, at most this many.
+constexpr uint32_t kFastCost = 1u << 23;
+constexpr uint32_t kFastBucket = 128;         // the per-row kernel: largest bucket it ranks by comparison
 constexpr uint32_t kFbMinChunk = 8192;
 
 // Multi-block refinement for k > kFinMaxK.

@@ -125,6 +125,18 @@ def test_special_values_and_ties():
         _f32_case(x, k, 1, eps=1e-3, **SMALL)
 
 
+@pytest.mark.parametrize("k,plateau,value", [(1024, 1000, 3.2), (4096, 2800, 3.0)])
+def test_tie_plateau_at_rank_k(k, plateau, value):
+    # a plateau of equal values where rank k falls: one log-scale bucket at
+    # or above rank k holds the whole plateau, far more than 128 candidates;
+    # the one-workgroup refinement ranks it by comparison (ties by index)
+    x = workloads.normal_f32(2**20, seed=12)
+    rng = np.random.default_rng(12)
+    x[rng.choice(x.size, plateau, replace=False)] = np.float32(value)
+    rec, ref = _f32_case(x, k, 0)
+    assert ref.status == oprofk.STATUS_FILTERED
+
+
 @pytest.mark.parametrize("N,k", [(1, 1), (3, 2), (64, 64), (1000, 10), (1000, 1000), (30_000, 4096)])
 def test_direct_mode(N, k):
     x = workloads.special_f32(N, seed=N)
