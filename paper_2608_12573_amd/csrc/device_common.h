@@ -541,6 +541,21 @@ __device__ __forceinline__ uint32_t log_bin(uint32_t d) {
   const uint32_t e = 31u - static_cast<uint32_t>(__clz(d));  // 7..31
   return (e - 6u) * 128u + ((d >> (e - 7u)) & 127u);
 }
+// Number of values in v[s, e) greater than c (v in LDS): eight reads are in
+// flight per step, so a long run costs one LDS latency per eight values.
+__device__ __forceinline__ uint32_t count_greater(const uint64_t* v, uint32_t s, uint32_t e, uint64_t c) {
+  uint32_t r = 0, q = s;
+  for (; q + 8 <= e; q += 8) {
+    uint64_t t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = v[q + u];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) r += t[u] > c ? 1u : 0u;
+  }
+  for (; q < e; ++q) r += v[q] > c ? 1u : 0u;
+  return r;
+}
+
 // The smallest d with log_bin(d) = b: log_bin(d) >= b exactly when
 // d >= log_bin_edge(b) (b < kLogBins).
 __device__ __forceinline__ uint32_t log_bin_edge(uint32_t b) {

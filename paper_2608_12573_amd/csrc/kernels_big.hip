@@ -411,8 +411,7 @@ __global__ __launch_bounds__(kSortBS) void k_bkt_sort(BigArgs a) {
           const uint64_t c = Bv[p];
           const uint32_t sb = sub_bin(comp_key(c) - tau, b);
           const uint32_t s0 = off[sb], s1 = s0 + cnt[sb];
-          uint32_t r = 0;
-          for (uint32_t q = s0; q < s1; ++q) r += Bv[q] > c ? 1u : 0u;
+          const uint32_t r = count_greater(Bv, s0, s1, c);
           if (start + s0 + r < kk) bkt_write<DT>(a, start + s0 + r, c);
         }
       }

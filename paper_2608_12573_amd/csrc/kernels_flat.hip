@@ -259,11 +259,15 @@ __global__ void k_init_state(InitArgs a) {
 
 // ------------------------------------------------------------ stage 4 -----
 constexpr uint32_t kFinCache = 28672;
-// The bucket refinement reads the candidates segment by segment: kPreThreads
-// threads per segment, kPreU keys each per sweep (kPreSeg per segment).
+// The bucket refinement reads the candidate keys segment by segment as
+// aligned 16-byte vectors: kPreThreads threads per segment, kPreV vectors
+// each loaded before the segment counts are known, kSweepV per later sweep.
+// A vector may start up to 3 entries before its segment (the previous
+// segment's) or end up to 3 past its capacity (still within the workspace);
+// such entries are skipped by their index.
 constexpr uint32_t kPreThreads = kFinBS / kSegs;
-constexpr int kPreU = 8;
-constexpr uint32_t kPreSeg = kPreThreads * kPreU;
+constexpr int kPreV = 2;
+constexpr int kSweepV = 4;
 static_assert(kPreThreads * kSegs == kFinBS, "threads per segment");
 constexpr int kFinDigit = 12;
 
@@ -486,7 +490,7 @@ struct FinishArgs {
 template <int DT>
 __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh, const uint32_t* seg_pre,
                                                 const uint32_t* seg_n, uint32_t total, SelectScratch& fs,
-                                                const uint32_t (&h)[4], const uint32_t (&pk)[kPreU]) {
+                                                const uint32_t (&h)[4], const uint4 (&pv)[kPreV]) {
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t tid = threadIdx.x;
   const uint32_t tau = a.st->tau_key;
@@ -531,10 +535,12 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
 
   if (n_sel <= kFastCap && cost <= kFastCost) {
     // place (key, candidate number) of buckets >= b* ...: thread t takes
-    // entries t % kPreThreads + kPreThreads * u of segment t / kPreThreads,
-    // the first kPreU of them already in registers
+    // vectors t % kPreThreads + kPreThreads * u of segment t / kPreThreads,
+    // the first kPreV of them already in registers
     const uint32_t x = tid / kPreThreads, l = tid % kPreThreads;
     const uint32_t nx = seg_n[x], px = seg_pre[x];
+    const uint32_t b0 = x * a.seg_cap;                  // the segment's first entry
+    const uint32_t v0 = b0 / 4, v1 = (b0 + nx + 3) / 4;  // vectors that cover its entries
     // (every candidate's key is >= tau; a bucket >= b* is a distance from tau
     // of at least its lower edge, so most keys take one compare)
     const uint32_t edge = log_bin_edge(bstar);
@@ -546,31 +552,32 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
         sh.bkt.comp[slot] = (static_cast<uint64_t>(key) << 32) | (px + j);
       }
     };
-    // sweep s + 1's keys are in flight while sweep s's are placed (two
-    // buffers taken in turn, so that placing one waits for its own loads only)
-    uint32_t ka[kPreU], kb[kPreU];
-    auto load_sweep = [&](uint32_t (&kv)[kPreU], uint32_t base) {
+    auto place_vec = [&](uint32_t v, const uint4& q) {
+      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-      for (int u = 0; u < kPreU; ++u) {
-        const uint32_t j = base + l + kPreThreads * u;
-        kv[u] = j < nx ? a.seg_key[static_cast<size_t>(x) * a.seg_cap + j] : 0u;
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t i = 4 * v + e;
+        if (i >= b0 && i < b0 + nx) place(i - b0, w4[e]);
       }
     };
-    auto place_sweep = [&](const uint32_t (&kv)[kPreU], uint32_t base) {
 #pragma unroll
-      for (int u = 0; u < kPreU; ++u) {
-        const uint32_t j = base + l + kPreThreads * u;
-        if (j < nx) place(j, kv[u]);
+    for (int u = 0; u < kPreV; ++u) {
+      const uint32_t v = v0 + l + kPreThreads * u;
+      if (v < v1) place_vec(v, pv[u]);
+    }
+    const uint4* const kv4 = reinterpret_cast<const uint4*>(a.seg_key);
+    for (uint32_t vb = v0 + kPreThreads * kPreV; vb < v1; vb += kPreThreads * kSweepV) {
+      uint4 q[kSweepV];
+#pragma unroll
+      for (int u = 0; u < kSweepV; ++u) {
+        const uint32_t v = vb + l + kPreThreads * u;
+        q[u] = v < v1 ? kv4[v] : uint4{0u, 0u, 0u, 0u};
       }
-    };
-    if (kPreSeg < nx) load_sweep(ka, kPreSeg);
-    place_sweep(pk, 0);
-    for (uint32_t base = kPreSeg; base < nx; base += 2 * kPreSeg) {
-      if (base + kPreSeg < nx) load_sweep(kb, base + kPreSeg);
-      place_sweep(ka, base);
-      if (base + kPreSeg >= nx) break;
-      if (base + 2 * kPreSeg < nx) load_sweep(ka, base + 2 * kPreSeg);
-      place_sweep(kb, base + kPreSeg);
+#pragma unroll
+      for (int u = 0; u < kSweepV; ++u) {
+        const uint32_t v = vb + l + kPreThreads * u;
+        if (v < v1) place_vec(v, q[u]);
+      }
     }
     __syncthreads();
     // ... then turn them into composites, all index loads in flight at once
@@ -592,9 +599,7 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
       const uint64_t c = sh.bkt.comp[p];
       const uint32_t bin = log_bin(comp_key(c) - tau);
       const uint32_t s = sh.bkt.off[bin], m = sh.bkt.fill[bin];
-      uint32_t r = 0;
-      for (uint32_t q = s; q < s + m; ++q) r += sh.bkt.comp[q] > c ? 1u : 0u;
-      const uint32_t dst = s + r;
+      const uint32_t dst = s + count_greater(sh.bkt.comp, s, s + m, c);
       if (dst < kk) {
         const uint32_t bits = bits_of_key<DT>(comp_key(c));
         if (DT == 0) static_cast<uint32_t*>(a.out_vals)[dst] = bits;
@@ -635,22 +640,26 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t tid = threadIdx.x, b = blockIdx.x;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
-  // Block 0 loads the bucket histogram and the first kPreSeg candidate keys
+  // Block 0 loads the bucket histogram and the first kPreV vectors of candidate keys
   // of every segment together with the segment counts, before it knows
   // them, so the three latencies overlap (reads past a segment's count stay
   // within its capacity and are ignored).
-  uint32_t h[4] = {0u, 0u, 0u, 0u}, pk[kPreU];
+  uint32_t h[4] = {0u, 0u, 0u, 0u};
+  uint4 pv[kPreV];
   if (!a.direct && b == 0) {
     const uint32_t bbase = kLogBins - 4 * (tid + 1);
     if (tid < kLogBins / 4) {
       const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
       h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
     }
+    // vectors that start within the segment's capacity (they end at most 3
+    // entries past it)
     const uint32_t x = tid / kPreThreads, l = tid % kPreThreads;
+    const uint32_t v0 = x * a.seg_cap / 4;
 #pragma unroll
-    for (int u = 0; u < kPreU; ++u) {
-      const uint32_t j = l + kPreThreads * u;
-      pk[u] = j < a.seg_cap ? a.seg_key[static_cast<size_t>(x) * a.seg_cap + j] : 0u;
+    for (int u = 0; u < kPreV; ++u) {
+      const uint32_t v = v0 + l + kPreThreads * u;
+      pv[u] = 4 * v < (x + 1) * a.seg_cap ? reinterpret_cast<const uint4*>(a.seg_key)[v] : uint4{0u, 0u, 0u, 0u};
     }
   }
   if (!a.direct) {
@@ -669,7 +678,27 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
     status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
     if (status == PROFK_STATUS_FILTERED) {
-      if (b == 0) finish_filtered<DT>(a, sh, seg_pre, seg_n, total, fs, h, pk);
+      if (b == 0) {
+        finish_filtered<DT>(a, sh, seg_pre, seg_n, total, fs, h, pv);
+      } else {
+        // The other workgroups have no work here: they read the candidates'
+        // keys and indices once, so that block 0 finds them in L2 and not in
+        // HBM, which the filter's stream has flushed them to.  Each segment's
+        // vectors are those that cover its entries (they end at most 3
+        // entries past it, within the workspace).
+        const uint32_t nthr = (gridDim.x - 1) * kFinBS, g = (b - 1) * kFinBS + tid;
+        const uint4* const kv4 = reinterpret_cast<const uint4*>(a.seg_key);
+        const uint4* const iv4 = reinterpret_cast<const uint4*>(a.seg_idx);
+        uint32_t fold = 0;
+        for (int x = 0; x < kSegs; ++x) {
+          const uint32_t b0 = x * a.seg_cap, v0 = b0 / 4, v1 = (b0 + seg_n[x] + 3) / 4;
+          for (uint32_t v = v0 + g; v < v1; v += nthr) {
+            const uint4 q = kv4[v], r = iv4[v];
+            fold ^= q.x ^ r.x;
+          }
+        }
+        asm volatile("" : : "v"(fold));  // the loads are kept: their lines are the point
+      }
       return;
     }
   }
