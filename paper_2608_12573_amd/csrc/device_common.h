@@ -428,37 +428,47 @@ __device__ uint32_t tau_pair_index(Draws draws, uint32_t tau, uint32_t t, uint32
 // which of a lane's slots hold keys): t rounds of a wave-wide max; the lowest
 // lane holding the maximum gives up one copy and stores it to out[round]
 // (out may be null).  Returns got = min(t, number of keys); `last` receives
-// the got-th largest key in every lane.
+// the got-th largest key in every lane.  v is left as it was.
+//
+// Each lane first sorts a copy of its keys in descending order (empty slots
+// as 0, the lowest key: a lane's first n slots then hold its n keys, since a
+// key of 0 and an empty slot are alike), so a round reads every lane's head
+// and the lane that gives it up shifts its copy by one.
 template <int E>
-__device__ __forceinline__ uint32_t wave_top_t(uint32_t (&v)[E], uint32_t valid, uint32_t t,
+__device__ __forceinline__ uint32_t wave_top_t(const uint32_t (&v)[E], uint32_t valid, uint32_t t,
                                                uint32_t* out, uint32_t& last) {
   const int lane = threadIdx.x & (kWave - 1);
+  uint32_t s[E];
+  uint32_t n = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const bool in = (valid >> e) & 1u;
+    s[e] = in ? v[e] : 0u;
+    n += in ? 1u : 0u;
+  }
+  // odd-even transposition sort, descending (E rounds sort E values)
+#pragma unroll
+  for (int r = 0; r < E; ++r)
+#pragma unroll
+    for (int j = r & 1; j + 1 < E; j += 2) {
+      const uint32_t hi = max(s[j], s[j + 1]), lo = min(s[j], s[j + 1]);
+      s[j] = hi;
+      s[j + 1] = lo;
+    }
   uint32_t got = 0;
   for (; got < t; ++got) {
-    uint32_t m = 0;
-    bool have = false;
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-      if ((valid >> e) & 1u) {
-        m = have ? max(m, v[e]) : v[e];
-        have = true;
-      }
-    const uint64_t any = __ballot(have);
-    if (any == 0) break;
-    uint32_t wm = have ? m : 0u;
-    wm = wave_max_u32(wm);
+    const bool have = n > 0;
+    if (__ballot(have) == 0) break;
+    const uint32_t wm = wave_max_u32(have ? s[0] : 0u);
     last = wm;
-    // lanes whose maximum equals the wave maximum; the lowest one gives it up
-    const uint64_t holders = __ballot(have && m == wm);
+    // lanes whose head equals the wave maximum; the lowest one gives it up
+    const uint64_t holders = __ballot(have && s[0] == wm);
     const int owner = __ffsll(static_cast<unsigned long long>(holders)) - 1;
     if (lane == owner) {
-      bool done = false;
 #pragma unroll
-      for (int e = 0; e < E; ++e)
-        if (!done && ((valid >> e) & 1u) && v[e] == wm) {
-          valid &= ~(1u << e);
-          done = true;
-        }
+      for (int e = 0; e + 1 < E; ++e) s[e] = s[e + 1];
+      s[E - 1] = 0;
+      --n;
       if (out) out[got] = wm;
     }
   }
