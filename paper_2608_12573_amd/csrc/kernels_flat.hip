@@ -270,6 +270,15 @@ constexpr int kPreV = 2;
 constexpr int kSweepV = 4;
 static_assert(kPreThreads * kSegs == kFinBS, "threads per segment");
 constexpr int kFinDigit = 12;
+// The bucket refinement spreads the buckets at or above the bucket of rank k
+// over up to kFinRefMax workgroups, one per kFinRefWork units of work (a
+// bucket of m candidates weighs m^2 + kFinRankW*m: its ranking compares and
+// the placing, gathering and writing of its entries).  Every workgroup
+// derives the same partition from the histogram, scans all candidates and
+// keeps those of its own buckets: no workgroup hands anything to another.
+constexpr uint32_t kFinRefMax = 32;
+constexpr uint32_t kFinRefWork = 16384;
+constexpr uint32_t kFinRankW = 64;
 
 // LDS of the general refinement (radix select over the candidates).
 struct FinShared {
@@ -478,19 +487,23 @@ struct FinishArgs {
   profk_info_t* info;
 };
 
-// Refinement of a filtered call (k_req <= total <= M) by one block, from
-// the filter's histogram of log_bin(key - tau) over the candidates:
+// Refinement of a filtered call (k_req <= total <= M), from the filter's
+// histogram of log_bin(key - tau) over the candidates:
 //   1. find the bucket b* holding rank kk;
 //   2. when the candidates at or above b* are few and ranking them within
 //      their buckets takes few comparisons (the squares of the bucket sizes),
-//      place them bucket by bucket in LDS and rank each one within its
-//      bucket by comparison: its output position is the bucket's first slot
-//      plus the number of larger composites in the bucket;
-//   3. otherwise run the general radix refinement.
+//      share those buckets out among the first G' workgroups (b < G'); each
+//      places the candidates of its buckets in LDS, bucket by bucket, and
+//      ranks each one within its bucket by comparison: its output position
+//      is the bucket's first slot plus the number of larger composites in
+//      the bucket;
+//   3. otherwise workgroup 0 runs the general radix refinement.
+// Called by workgroups b < kFinRefMax; b = 0 also writes the report.
 template <int DT>
 __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh, const uint32_t* seg_pre,
                                                 const uint32_t* seg_n, uint32_t total, SelectScratch& fs,
-                                                const uint32_t (&h)[4], const uint4 (&pv)[kPreV]) {
+                                                const uint32_t (&h)[4], const uint4 (&pv)[kPreV], uint32_t b,
+                                                uint32_t* own) {
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t tid = threadIdx.x;
   const uint32_t tau = a.st->tau_key;
@@ -519,37 +532,93 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
   }
   __syncthreads();
   const uint32_t bstar = fs.found[0], n_sel = fs.found[1] + fs.found[2];
-  // comparisons the ranking takes: the squares of the bucket sizes at or
-  // above b* (each clamped so that the sum cannot wrap; a bucket that large
-  // fails n_sel <= kFastCap anyway)
-  uint32_t cost = 0;
-  if (tid < kOwners) {
+  // Weight of each bucket at or above b*: m^2, the compares that rank its m
+  // candidates, plus kFinRankW*m.  With n_sel <= kFastCap the sum is at most
+  // n_sel^2 + kFinRankW*n_sel and cannot wrap; otherwise it is not used.
+  uint32_t wt[4], wsum = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (bbase + j >= bstar) {
-        const uint32_t m = min(h[j], kFastCap + 1);
-        cost += m * m;
-      }
+  for (int j = 0; j < 4; ++j) {
+    wt[j] = (tid < kOwners && bbase + j >= bstar) ? h[j] * h[j] + kFinRankW * h[j] : 0u;
+    wsum += wt[j];
   }
-  cost = block_sum<kFinBS>(cost, fs.wsum);
+  if (tid == 0) {
+    own[0] = kLogBins;
+    own[1] = 0;
+    own[2] = 0xFFFFFFFFu;
+    own[3] = 0;
+  }
+  uint32_t W = 0;
+  const uint32_t wabove = block_excl_sum<kFinBS>(wsum, fs.wsum, &W);
 
-  if (n_sel <= kFastCap && cost <= kFastCost) {
-    // place (key, candidate number) of buckets >= b* ...: thread t takes
+  if (n_sel <= kFastCap && W - kFinRankW * n_sel <= kFastCost) {
+    // Partition: bucket j (descending order) goes to workgroup
+    // min(G' - 1, floor(G' * W_j / W)), W_j the weight of the buckets above
+    // it, so each workgroup holds a run of consecutive buckets: bins
+    // [own[0], own[1]] and output slots [own[2], own[3]).
+    const uint32_t G = min(min(gridDim.x, kFinRefMax), max(1u, (W + kFinRefWork - 1) / kFinRefWork));
+    if (b >= G) return;
+    uint32_t lo = kLogBins, hi = 0, s0 = 0xFFFFFFFFu, s1 = 0;
+    if (G == 1) {
+      // one workgroup: every bucket at or above b*, slots [0, n_sel)
+      lo = bstar;
+      hi = kLogBins - 1;
+      s0 = 0;
+      s1 = n_sel;
+    } else if (tid < kOwners) {
+      uint32_t run = above_me, wrun = wabove;
+      // part == b exactly when b*W <= G*W_j < (b+1)*W (the last part takes
+      // the rest); every product is below 2^32 since W <= 2^26 + 2^19
+      const uint32_t lo_w = b * W, hi_w = b + 1 < G ? (b + 1) * W : 0xFFFFFFFFu;
+#pragma unroll
+      for (int j = 3; j >= 0; --j) {
+        const uint32_t gw = wrun * G;
+        if (h[j] > 0 && bbase + j >= bstar && gw >= lo_w && (gw < hi_w || b + 1 == G)) {
+          lo = min(lo, bbase + j);
+          hi = max(hi, bbase + j);
+          s0 = min(s0, run);
+          s1 = max(s1, run + h[j]);
+        }
+        run += h[j];
+        wrun += wt[j];
+      }
+    }
+    if (G > 1) {
+      lo = ~wave_max_u32(~lo);
+      hi = wave_max_u32(hi);
+      s0 = ~wave_max_u32(~s0);
+      s1 = wave_max_u32(s1);
+      if ((tid & (kWave - 1)) == 0 && lo <= hi) {
+        atomicMin(&own[0], lo);
+        atomicMax(&own[1], hi);
+        atomicMin(&own[2], s0);
+        atomicMax(&own[3], s1);
+      }
+      __syncthreads();
+      lo = own[0];
+      hi = own[1];
+      s0 = own[2];
+      s1 = own[3];
+      if (lo > hi) return;  // every bucket of this share lies in a heavier neighbour's
+    }
+    const uint32_t bin_lo = lo, bin_hi = hi, slo = s0, n_own = s1 - s0;
+    // place (key, candidate number) of the buckets [bin_lo, bin_hi]: thread t takes
     // vectors t % kPreThreads + kPreThreads * u of segment t / kPreThreads,
     // the first kPreV of them already in registers
     const uint32_t x = tid / kPreThreads, l = tid % kPreThreads;
     const uint32_t nx = seg_n[x], px = seg_pre[x];
     const uint32_t b0 = x * a.seg_cap;                  // the segment's first entry
     const uint32_t v0 = b0 / 4, v1 = (b0 + nx + 3) / 4;  // vectors that cover its entries
-    // (every candidate's key is >= tau; a bucket >= b* is a distance from tau
-    // of at least its lower edge, so most keys take one compare)
-    const uint32_t edge = log_bin_edge(bstar);
+    // (every candidate's key is >= tau; a bucket >= bin_lo is a distance
+    // from tau of at least its lower edge, so most keys take one compare)
+    const uint32_t edge = log_bin_edge(bin_lo);
     auto place = [&](uint32_t j, uint32_t key) {
       const uint32_t d = key - tau;
       if (d >= edge) {
         const uint32_t bin = log_bin(d);
-        const uint32_t slot = sh.bkt.off[bin] + atomicAdd(&sh.bkt.fill[bin], 1u);
-        sh.bkt.comp[slot] = (static_cast<uint64_t>(key) << 32) | (px + j);
+        if (bin <= bin_hi) {
+          const uint32_t slot = sh.bkt.off[bin] - slo + atomicAdd(&sh.bkt.fill[bin], 1u);
+          sh.bkt.comp[slot] = (static_cast<uint64_t>(key) << 32) | (px + j);
+        }
       }
     };
     auto place_vec = [&](uint32_t v, const uint4& q) {
@@ -586,20 +655,20 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const uint32_t p = u * kFinBS + tid;
-      ix[u] = p < n_sel ? a.seg_idx[src.pos(static_cast<uint32_t>(sh.bkt.comp[p]))] : 0u;
+      ix[u] = p < n_own ? a.seg_idx[src.pos(static_cast<uint32_t>(sh.bkt.comp[p]))] : 0u;
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const uint32_t p = u * kFinBS + tid;
-      if (p < n_sel) sh.bkt.comp[p] = composite(static_cast<uint32_t>(sh.bkt.comp[p] >> 32), ix[u]);
+      if (p < n_own) sh.bkt.comp[p] = composite(static_cast<uint32_t>(sh.bkt.comp[p] >> 32), ix[u]);
     }
     __syncthreads();
     // rank within the bucket, write the kk largest
-    for (uint32_t p = tid; p < n_sel; p += kFinBS) {
+    for (uint32_t p = tid; p < n_own; p += kFinBS) {
       const uint64_t c = sh.bkt.comp[p];
       const uint32_t bin = log_bin(comp_key(c) - tau);
-      const uint32_t s = sh.bkt.off[bin], m = sh.bkt.fill[bin];
-      const uint32_t dst = s + count_greater(sh.bkt.comp, s, s + m, c);
+      const uint32_t s = sh.bkt.off[bin] - slo, m = sh.bkt.fill[bin];
+      const uint32_t dst = sh.bkt.off[bin] + count_greater(sh.bkt.comp, s, s + m, c);
       if (dst < kk) {
         const uint32_t bits = bits_of_key<DT>(comp_key(c));
         if (DT == 0) static_cast<uint32_t*>(a.out_vals)[dst] = bits;
@@ -607,12 +676,14 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
         a.out_idx[dst] = comp_idx(c);
       }
     }
-    for (uint32_t p = kk + tid; p < a.k; p += kFinBS) {  // relaxed recall: padding
-      if (DT == 0) static_cast<uint32_t*>(a.out_vals)[p] = 0xFF800000u;
-      else static_cast<uint16_t*>(a.out_vals)[p] = 0xFF80u;
-      a.out_idx[p] = -1;
-    }
+    if (b == 0)
+      for (uint32_t p = kk + tid; p < a.k; p += kFinBS) {  // relaxed recall: padding
+        if (DT == 0) static_cast<uint32_t*>(a.out_vals)[p] = 0xFF800000u;
+        else static_cast<uint16_t*>(a.out_vals)[p] = 0xFF80u;
+        a.out_idx[p] = -1;
+      }
   } else {
+    if (b != 0) return;
     __syncthreads();
     uint32_t bm = 0;
     for (uint32_t i = tid; i < a.G_f; i += kFinBS) bm = max(bm, a.blk_max[i]);
@@ -621,7 +692,7 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
     sort_write_any<DT, kFinBS>(sh.gen.sortbuf, kk, a.k, reinterpret_cast<uint64_t*>(sh.gen.cache),
                                a.out_vals, a.out_idx);
   }
-  if (tid == 0) {
+  if (b == 0 && tid == 0) {
     a.st->status = PROFK_STATUS_FILTERED;
     if (a.info) {
       a.info->count = total;
@@ -636,17 +707,17 @@ template <int DT>
 __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   __shared__ FinLds sh;
   __shared__ SelectScratch fs;
-  __shared__ uint32_t seg_n[kSegs], seg_pre[kSegs + 1], flag;
+  __shared__ uint32_t seg_n[kSegs], seg_pre[kSegs + 1], flag, own[4];
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t tid = threadIdx.x, b = blockIdx.x;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
-  // Block 0 loads the bucket histogram and the first kPreV vectors of candidate keys
+  // Blocks b < kFinRefMax load the bucket histogram and the first kPreV vectors of candidate keys
   // of every segment together with the segment counts, before it knows
   // them, so the three latencies overlap (reads past a segment's count stay
   // within its capacity and are ignored).
   uint32_t h[4] = {0u, 0u, 0u, 0u};
   uint4 pv[kPreV];
-  if (!a.direct && b == 0) {
+  if (!a.direct && b < kFinRefMax) {
     const uint32_t bbase = kLogBins - 4 * (tid + 1);
     if (tid < kLogBins / 4) {
       const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
@@ -678,15 +749,15 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
     status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
     if (status == PROFK_STATUS_FILTERED) {
-      if (b == 0) {
-        finish_filtered<DT>(a, sh, seg_pre, seg_n, total, fs, h, pv);
+      if (b < kFinRefMax) {
+        finish_filtered<DT>(a, sh, seg_pre, seg_n, total, fs, h, pv, b, own);
       } else {
         // The other workgroups have no work here: they read the candidates'
-        // keys and indices once, so that block 0 finds them in L2 and not in
-        // HBM, which the filter's stream has flushed them to.  Each segment's
-        // vectors are those that cover its entries (they end at most 3
-        // entries past it, within the workspace).
-        const uint32_t nthr = (gridDim.x - 1) * kFinBS, g = (b - 1) * kFinBS + tid;
+        // keys and indices once, so that the refining ones find them in L2
+        // and not in HBM, which the filter's stream has flushed them to.
+        // Each segment's vectors are those that cover its entries (they end
+        // at most 3 entries past it, within the workspace).
+        const uint32_t nthr = (gridDim.x - kFinRefMax) * kFinBS, g = (b - kFinRefMax) * kFinBS + tid;
         const uint4* const kv4 = reinterpret_cast<const uint4*>(a.seg_key);
         const uint4* const iv4 = reinterpret_cast<const uint4*>(a.seg_idx);
         uint32_t fold = 0;
