@@ -76,13 +76,17 @@ __device__ __forceinline__ uint32_t index_of_word(uint64_t u, uint64_t n) {
 }
 
 // ------------------------------------------------------------- scans ------
+// Inclusive prefix sum over the lanes of a wave, in lane order, by DPP:
+// shifts right by 1, 2, 4 and 8 lanes within each 16-lane row (lanes with no
+// source add 0) give each row's own prefix sums; a broadcast of lane 15 into
+// rows 1 and 3, then of lane 31 into rows 2 and 3, adds the rows below.
 __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
-  const int lane = threadIdx.x & (kWave - 1);
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t y = __shfl_up(x, o, kWave);
-    if (lane >= o) x += y;
-  }
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
   return x;
 }
 
@@ -128,6 +132,40 @@ __device__ __forceinline__ uint32_t block_excl_sum(uint32_t v, uint32_t* wsum, u
   if (total) *total = wsum[NW];
   __syncthreads();
   return r;
+}
+
+// The same for a pair of values in one pass (the same three barriers):
+// e0/e1 the exclusive sums, t0/t1 the totals; wsum holds 2*(BS/64 + 1) words.
+template <int BS>
+__device__ __forceinline__ void block_excl_sum2(uint32_t v0, uint32_t v1, uint32_t* wsum, uint32_t& e0,
+                                                uint32_t& e1, uint32_t& t0, uint32_t& t1) {
+  constexpr int NW = BS / kWave;
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const uint32_t i0 = wave_incl_sum(v0), i1 = wave_incl_sum(v1);
+  if (lane == kWave - 1) {
+    wsum[w] = i0;
+    wsum[NW + 1 + w] = i1;
+  }
+  __syncthreads();
+  if (w == 0) {
+    uint32_t a0 = lane < NW ? wsum[lane] : 0u, a1 = lane < NW ? wsum[NW + 1 + lane] : 0u;
+    a0 = wave_incl_sum(a0);
+    a1 = wave_incl_sum(a1);
+    if (lane < NW) {
+      wsum[lane] = a0;
+      wsum[NW + 1 + lane] = a1;
+    }
+    if (lane == NW - 1) {
+      wsum[NW] = a0;
+      wsum[2 * NW + 1] = a1;
+    }
+  }
+  __syncthreads();
+  e0 = (w ? wsum[w - 1] : 0u) + i0 - v0;
+  e1 = (w ? wsum[NW + 1 + w - 1] : 0u) + i1 - v1;
+  t0 = wsum[NW];
+  t1 = wsum[2 * NW + 1];
+  __syncthreads();
 }
 
 template <int BS>

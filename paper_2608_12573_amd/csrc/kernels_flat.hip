@@ -267,7 +267,7 @@ constexpr uint32_t kFinCache = 28672;
 // such entries are skipped by their index.
 constexpr uint32_t kPreThreads = kFinBS / kSegs;
 constexpr int kPreV = 2;
-constexpr int kSweepV = 4;
+constexpr int kSweepV = 8;
 static_assert(kPreThreads * kSegs == kFinBS, "threads per segment");
 constexpr int kFinDigit = 12;
 // The bucket refinement spreads the buckets at or above the bucket of rank k
@@ -294,8 +294,8 @@ struct FinShared {
 // LDS of the bucket refinement: the candidates at or above the bucket of
 // rank k, placed bucket by bucket in descending bucket order.
 struct BucketShared {
-  uint32_t off[kLogBins];          // first slot of each bucket
-  uint32_t fill[kLogBins];         // entries placed in each bucket
+  alignas(16) uint32_t off[kLogBins];   // first slot of each bucket
+  alignas(16) uint32_t fill[kLogBins];  // entries placed in each bucket
   uint64_t comp[kFastCap];         // (key, ~index) composites
 };
 
@@ -503,43 +503,50 @@ template <int DT>
 __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh, const uint32_t* seg_pre,
                                                 const uint32_t* seg_n, uint32_t total, SelectScratch& fs,
                                                 const uint32_t (&h)[4], const uint4 (&pv)[kPreV], uint32_t b,
-                                                uint32_t* own) {
+                                                uint32_t* tmp) {
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t tid = threadIdx.x;
   const uint32_t tau = a.st->tau_key;
   const SegSrc src{a.seg_key, a.seg_idx, a.seg_cap, seg_pre};
   const uint32_t kk = min(a.k, total);
 
-  // 1. bucket offsets in descending bucket order: thread t owns buckets
-  //    [kLogBins - 4(t+1), kLogBins - 4t)
+  // 1. bucket offsets and weight prefixes in descending bucket order:
+  //    thread t owns buckets [kLogBins - 4(t+1), kLogBins - 4t).  The weight
+  //    of a bucket of m candidates is m^2, the compares that rank them, plus
+  //    kFinRankW*m.  A prefix from the top covers higher buckets only, so the
+  //    prefixes and the total W through b* cannot wrap when
+  //    n_sel <= kFastCap (W <= n_sel^2 + kFinRankW*n_sel); the sums below b*
+  //    may, and are not used.
   constexpr uint32_t kOwners = kLogBins / 4;
   static_assert(kLogBins % 4 == 0 && kOwners <= kFinBS, "bucket ownership");
   const uint32_t bbase = kLogBins - 4 * (tid + 1);  // h: loaded by the caller
-  const uint32_t above_me = block_excl_sum<kFinBS>(h[0] + h[1] + h[2] + h[3], fs.wsum, nullptr);
+  uint32_t* const own = tmp;
+  uint32_t wt[4], wsum = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    wt[j] = h[j] * h[j] + kFinRankW * h[j];
+    wsum += wt[j];
+  }
+  uint32_t above_me, wabove, tot_n, tot_w;
+  block_excl_sum2<kFinBS>(h[0] + h[1] + h[2] + h[3], wsum, tmp + 4, above_me, wabove, tot_n, tot_w);
   if (tid < kOwners) {
-    uint32_t run = above_me;
+    uint32_t run = above_me, wrun = wabove, o[4];
 #pragma unroll
     for (int j = 3; j >= 0; --j) {
-      sh.bkt.off[bbase + j] = run;
-      sh.bkt.fill[bbase + j] = 0;
+      o[j] = run;
       if (run < kk && kk <= run + h[j]) {
         fs.found[0] = bbase + j;
         fs.found[1] = run;
         fs.found[2] = h[j];
+        fs.found[3] = wrun + wt[j];
       }
       run += h[j];
+      wrun += wt[j];
     }
-  }
-  __syncthreads();
-  const uint32_t bstar = fs.found[0], n_sel = fs.found[1] + fs.found[2];
-  // Weight of each bucket at or above b*: m^2, the compares that rank its m
-  // candidates, plus kFinRankW*m.  With n_sel <= kFastCap the sum is at most
-  // n_sel^2 + kFinRankW*n_sel and cannot wrap; otherwise it is not used.
-  uint32_t wt[4], wsum = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    wt[j] = (tid < kOwners && bbase + j >= bstar) ? h[j] * h[j] + kFinRankW * h[j] : 0u;
-    wsum += wt[j];
+    // one 16-byte write per array (4-byte writes at a 16-byte stride would
+    // collide on the LDS banks)
+    *reinterpret_cast<uint4*>(&sh.bkt.off[bbase]) = uint4{o[0], o[1], o[2], o[3]};
+    *reinterpret_cast<uint4*>(&sh.bkt.fill[bbase]) = uint4{0u, 0u, 0u, 0u};
   }
   if (tid == 0) {
     own[0] = kLogBins;
@@ -547,8 +554,8 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
     own[2] = 0xFFFFFFFFu;
     own[3] = 0;
   }
-  uint32_t W = 0;
-  const uint32_t wabove = block_excl_sum<kFinBS>(wsum, fs.wsum, &W);
+  __syncthreads();
+  const uint32_t bstar = fs.found[0], n_sel = fs.found[1] + fs.found[2], W = fs.found[3];
 
   if (n_sel <= kFastCap && W - kFinRankW * n_sel <= kFastCost) {
     // Partition: bucket j (descending order) goes to workgroup
@@ -608,25 +615,25 @@ __device__ __forceinline__ void finish_filtered(const FinishArgs& a, FinLds& sh,
     const uint32_t nx = seg_n[x], px = seg_pre[x];
     const uint32_t b0 = x * a.seg_cap;                  // the segment's first entry
     const uint32_t v0 = b0 / 4, v1 = (b0 + nx + 3) / 4;  // vectors that cover its entries
-    // (every candidate's key is >= tau; a bucket >= bin_lo is a distance
-    // from tau of at least its lower edge, so most keys take one compare)
-    const uint32_t edge = log_bin_edge(bin_lo);
-    auto place = [&](uint32_t j, uint32_t key) {
-      const uint32_t d = key - tau;
-      if (d >= edge) {
-        const uint32_t bin = log_bin(d);
-        if (bin <= bin_hi) {
-          const uint32_t slot = sh.bkt.off[bin] - slo + atomicAdd(&sh.bkt.fill[bin], 1u);
-          sh.bkt.comp[slot] = (static_cast<uint64_t>(key) << 32) | (px + j);
-        }
-      }
-    };
+    // Every candidate's key is >= tau, and one lies in a bucket >= bin_lo
+    // exactly when key - tau >= log_bin_edge(bin_lo), i.e. key >= thr: the
+    // sum cannot wrap, since bucket bin_lo holds a candidate.  Most vectors
+    // hold no such key and cost four compares.
+    const uint32_t thr = tau + log_bin_edge(bin_lo);
     auto place_vec = [&](uint32_t v, const uint4& q) {
-      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+      if (__builtin_expect((q.x >= thr) | (q.y >= thr) | (q.z >= thr) | (q.w >= thr), 0)) {
+        const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t i = 4 * v + e;
-        if (i >= b0 && i < b0 + nx) place(i - b0, w4[e]);
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t i = 4 * v + e, key = w4[e];
+          if (key >= thr && i >= b0 && i < b0 + nx) {
+            const uint32_t bin = log_bin(key - tau);
+            if (bin <= bin_hi) {
+              const uint32_t slot = sh.bkt.off[bin] - slo + atomicAdd(&sh.bkt.fill[bin], 1u);
+              sh.bkt.comp[slot] = (static_cast<uint64_t>(key) << 32) | (px + i - b0);
+            }
+          }
+        }
       }
     };
 #pragma unroll
@@ -707,14 +714,15 @@ template <int DT>
 __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
   __shared__ FinLds sh;
   __shared__ SelectScratch fs;
-  __shared__ uint32_t seg_n[kSegs], seg_pre[kSegs + 1], flag, own[4];
+  __shared__ uint32_t seg_n[kSegs], seg_pre[kSegs + 1], flag;
+  __shared__ uint32_t fin_tmp[4 + 2 * (kFinBS / kWave + 1)];
   constexpr int KB = Elem<DT>::KEYBITS;
   const uint32_t tid = threadIdx.x, b = blockIdx.x;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
-  // Blocks b < kFinRefMax load the bucket histogram and the first kPreV vectors of candidate keys
-  // of every segment together with the segment counts, before it knows
-  // them, so the three latencies overlap (reads past a segment's count stay
-  // within its capacity and are ignored).
+  // Blocks b < kFinRefMax load the bucket histogram and the first kPreV
+  // vectors of candidate keys of every segment together with the segment
+  // counts, before they know them, so the three latencies overlap (reads past
+  // a segment's count stay within its capacity and are ignored).
   uint32_t h[4] = {0u, 0u, 0u, 0u};
   uint4 pv[kPreV];
   if (!a.direct && b < kFinRefMax) {
@@ -734,15 +742,14 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
     }
   }
   if (!a.direct) {
-    if (tid < kSegs) seg_n[tid] = a.seg_cnt[tid * kSegStride];
-    __syncthreads();
-    if (tid == 0) {
-      uint32_t run = 0;
-      for (int x = 0; x < kSegs; ++x) {
-        seg_pre[x] = run;
-        run += seg_n[x];
+    if (tid < kWave) {
+      const uint32_t c = tid < kSegs ? a.seg_cnt[tid * kSegStride] : 0u;
+      const uint32_t incl = wave_incl_sum(c);
+      if (tid < kSegs) {
+        seg_n[tid] = c;
+        seg_pre[tid] = incl - c;
       }
-      seg_pre[kSegs] = run;
+      if (tid == kSegs - 1) seg_pre[kSegs] = incl;
     }
     __syncthreads();
     total = seg_pre[kSegs];
@@ -750,14 +757,19 @@ __global__ __launch_bounds__(kFinBS) void k_finish(FinishArgs a) {
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
     if (status == PROFK_STATUS_FILTERED) {
       if (b < kFinRefMax) {
-        finish_filtered<DT>(a, sh, seg_pre, seg_n, total, fs, h, pv, b, own);
+        finish_filtered<DT>(a, sh, seg_pre, seg_n, total, fs, h, pv, b, fin_tmp);
       } else {
         // The other workgroups have no work here: they read the candidates'
-        // keys and indices once, so that the refining ones find them in L2
-        // and not in HBM, which the filter's stream has flushed them to.
-        // Each segment's vectors are those that cover its entries (they end
-        // at most 3 entries past it, within the workspace).
-        const uint32_t nthr = (gridDim.x - kFinRefMax) * kFinBS, g = (b - kFinRefMax) * kFinBS + tid;
+        // keys and indices, so that the refining ones find them in L2 and
+        // not in HBM, which the filter's stream has flushed them to.  Each
+        // XCD has an L2 of its own and workgroup b runs on XCD b % kXcds
+        // (round-robin dispatch), so the idle workgroups of each XCD read
+        // every line between them.  Each segment's vectors are those that
+        // cover its entries (they end at most 3 entries past it, within the
+        // workspace).
+        static_assert(kFinRefMax % kXcds == 0, "idle workgroups start on XCD 0");
+        const uint32_t xcd = b % kXcds, nx = (gridDim.x - kFinRefMax - xcd + kXcds - 1) / kXcds;
+        const uint32_t nthr = nx * kFinBS, g = (b - kFinRefMax) / kXcds * kFinBS + tid;
         const uint4* const kv4 = reinterpret_cast<const uint4*>(a.seg_key);
         const uint4* const iv4 = reinterpret_cast<const uint4*>(a.seg_idx);
         uint32_t fold = 0;

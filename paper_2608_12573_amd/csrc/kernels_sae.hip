@@ -59,7 +59,6 @@ __device__ __forceinline__ float sae_relu(float pre) { return pre > 0.0f ? pre :
 // and walks all row tiles; its workgroups (b / V = 0, 1, ...) take the
 // group's tiles in row-major order with stride grid / V, so consecutive tiles
 // of an XCD share their row block of x.  Every column tile has one owner.
-constexpr uint32_t kXcds = 8;
 
 struct XcdTiles {
   uint32_t nlo, nx, count;  // the group's column tiles [nlo, nlo + nx), tiles in all

@@ -25,6 +25,7 @@ struct CallState {
 static_assert(sizeof(CallState) == 256, "call state size");
 
 // Launch geometry.
+constexpr uint32_t kXcds = 8;                 // MI355X: 8 XCDs of 32 CUs, each with its own L2
 constexpr int kSampBS = 256;                  // threads of a sample block
 constexpr int kSampPerBlock = 4 * kSampBS;    // draws per sample block
 // Sample blocks of plans with t > kWaveTopMax (key rule): 1024 threads and
