@@ -55,6 +55,30 @@ def test_graph_batchtopk_big_k():
     _replays_equal_eager(call, [out[0], out[1], info])
 
 
+@pytest.mark.parametrize("case", ["bucket", "radix"])
+def test_graph_flat_k_above_4096(case):
+    # k > 4096: the bucket refinement on the caller's stream and the radix
+    # refinement on the library's second stream, both inside the capture;
+    # a plateau of 20000 equal keys at rank 3000 puts more candidates in
+    # one bucket than the bucket path takes, so that the radix path works
+    t = torch()
+    if case == "bucket":
+        x, k, eps = workloads.normal_f32(2**21 + 7, seed=21), 20000, 1e-6
+    else:
+        x, k, eps = workloads.plateau_f32(2**21, seed=5, first_rank=3000, width=20_000), 8000, 1e-3
+    p = pk.plan(x.size, k, eps)
+    note(f"graph flat {case} N={x.size} k={k} S={p.S} t={p.t} M={p.M}")
+    g = gpu_f32(x)
+    ws = pk.workspace(p, pk.F32)
+    out = (t.empty(k, dtype=t.float32, device="cuda"), t.empty(k, dtype=t.int64, device="cuda"))
+    info = t.empty(pk.INFO_BYTES, dtype=t.uint8, device="cuda")
+    call = lambda: pk.topk(g, k, seed=1, p=p, ws=ws, out=out, info=info)
+    call()
+    ref = oprofk.run(okeys.f32_bits(x), "f32", k, oracle_plan_of(p), 1)
+    compare(out[0], out[1], info, ref, "f32")
+    _replays_equal_eager(call, [out[0], out[1], info])
+
+
 def test_graph_flat_small_k():
     t = torch()
     x = workloads.normal_f32(2**20 + 3, seed=5)
