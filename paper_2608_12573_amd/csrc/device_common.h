@@ -407,6 +407,40 @@ __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t k
   return res;
 }
 
+// The kk-th largest (1-based, with multiplicity) of m keys held in LDS, for
+// short lists: each key counts the keys above it and equal to it (m^2
+// compares in all, eight LDS reads in flight per step), and the keys with
+// #above < kk <= #above + #equal, all equal to the answer, write out[0] =
+// the key and out[1] = #above.  Requires 1 <= kk <= m; every thread of the
+// block calls it, and the caller syncs before reading out.
+constexpr uint32_t kListRankMax = 256;
+template <int BS>
+__device__ __forceinline__ void list_kth(const uint32_t* list, uint32_t m, uint32_t kk, uint32_t* out) {
+  for (uint32_t i = threadIdx.x; i < m; i += BS) {
+    const uint32_t c = list[i];
+    uint32_t gt = 0, ge = 0, j = 0;
+    for (; j + 8 <= m; j += 8) {
+      uint32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = list[j + u];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        gt += v[u] > c ? 1u : 0u;
+        ge += v[u] >= c ? 1u : 0u;
+      }
+    }
+    for (; j < m; ++j) {
+      const uint32_t v = list[j];
+      gt += v > c ? 1u : 0u;
+      ge += v >= c ? 1u : 0u;
+    }
+    if (gt < kk && kk <= ge) {
+      out[0] = c;
+      out[1] = gt;
+    }
+  }
+}
+
 // The common case: 11-bit digits in the SelectShared histogram.
 template <int BS, class Visit>
 __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t kk, int nbits,

@@ -162,11 +162,17 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
         if (take) tlist[p] = v;
       });
       __syncthreads();
-      r = block_select_kth<kTauBS>(
-          [&](auto f) {
-            for (uint32_t i = tid; i < eq; i += kTauBS) f(tlist[i]);
-          },
-          a.t - above, shift, pre | (d << shift), sel);
+      if (eq <= kListRankMax) {
+        list_kth<kTauBS>(tlist, eq, a.t - above, &list_n[1]);
+        __syncthreads();
+        r.kth = list_n[1];
+      } else {
+        r = block_select_kth<kTauBS>(
+            [&](auto f) {
+              for (uint32_t i = tid; i < eq; i += kTauBS) f(tlist[i]);
+            },
+            a.t - above, shift, pre | (d << shift), sel);
+      }
       done = true;
     }
   }

@@ -31,6 +31,8 @@ struct SampleUnionShared {
   uint32_t keys[4 * BS];
   uint32_t lists[BS / kWave][kWaveTopMax];
   uint32_t list_n[BS / kWave];
+  uint32_t bin_list[kListRankMax];  // t > kWaveTopMax: the keys of the bin holding rank t
+  uint32_t kth[2];
   SelectShared sel;
   uint32_t emitted;
 };
@@ -76,15 +78,51 @@ __device__ __forceinline__ void sample_block_top(uint32_t (&kv)[4], uint32_t val
     for (uint32_t j = tid; j < nb; j += BS) dst[j] = sh.keys[j];
     return;
   }
-  auto visit = [&](auto f) {
-    for (uint32_t j = tid; j < nb; j += BS) f(sh.keys[j]);
-  };
-  const SelectResult r = block_select_kth<BS>(visit, tl, KEYBITS, 0u, sh.sel);
-  if (tid == 0) sh.emitted = 0;
+  // One digit pass over the top key bits finds the bin holding rank tl;
+  // when it holds few keys they are ranked by counting, otherwise the
+  // remaining digits are taken over all keys.
+  constexpr int SHIFT = KEYBITS - kSelDigit;
+  for (uint32_t i = tid; i < static_cast<uint32_t>(kSelBins); i += BS) sh.sel.hist[i] = 0;
+  if (tid == 0) {
+    sh.emitted = 0;
+    sh.list_n[0] = 0;
+  }
   __syncthreads();
-  for (uint32_t j = tid; j < nb; j += BS)
-    if (sh.keys[j] > r.kth) dst[atomicAdd(&sh.emitted, 1u)] = sh.keys[j];
-  for (uint32_t j = r.above + tid; j < tl; j += BS) dst[j] = r.kth;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) hist_add(sh.sel.hist, kv[q] >> SHIFT, (valid >> q) & 1u);
+  __syncthreads();
+  if (tid < kWave) rank_bin_search(sh.sel.hist, kSelBins, tl, sh.sel.scratch());
+  __syncthreads();
+  const uint32_t d = sh.sel.found[0], above = sh.sel.found[1], eq = sh.sel.found[2];
+  uint32_t kth, above_kth;
+  if (eq <= kListRankMax) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool take = ((valid >> q) & 1u) && (kv[q] >> SHIFT) == d;
+      const uint32_t slot = lds_append(&sh.list_n[0], take);
+      if (take) sh.bin_list[slot] = kv[q];
+    }
+    __syncthreads();
+    list_kth<BS>(sh.bin_list, eq, tl - above, sh.kth);
+    __syncthreads();
+    kth = sh.kth[0];
+    above_kth = above + sh.kth[1];
+  } else {
+    auto visit = [&](auto f) {
+      for (uint32_t j = tid; j < nb; j += BS) f(sh.keys[j]);
+    };
+    const SelectResult r = block_select_kth<BS>(visit, tl - above, SHIFT, d << SHIFT, sh.sel);
+    kth = r.kth;
+    above_kth = above + r.above;
+  }
+  // the keys above the tl-th, then copies of it up to tl
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const bool take = ((valid >> q) & 1u) && kv[q] > kth;
+    const uint32_t slot = lds_append(&sh.emitted, take);
+    if (take) dst[slot] = kv[q];
+  }
+  for (uint32_t j = above_kth + tid; j < tl; j += BS) dst[j] = kth;
 }
 
 }  // namespace profk
