@@ -559,14 +559,15 @@ __device__ __forceinline__ int shared_prefix_bits(uint32_t lo, uint32_t hi, int 
 // e*BS + t (e < E) in v[e].  Compare-exchange partners at stride s are in the
 // same thread (s >= BS), in another wave (64 <= s < BS: through LDS, one
 // barrier per stage with two alternating buffers) or in the same wave
-// (s < 64: lane shuffles).  `lds` holds 2*P values.
+// (s < 64: lane shuffles).  `lds` holds 2*P values, or P with ONE_BUF (one
+// more barrier per LDS stage).
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m) {
   const uint32_t lo = __shfl_xor(static_cast<uint32_t>(x), m, kWave);
   const uint32_t hi = __shfl_xor(static_cast<uint32_t>(x >> 32), m, kWave);
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-template <int BS, int E>
+template <int BS, int E, bool ONE_BUF = false>
 __device__ __forceinline__ void bitonic_sort_regs_desc(uint64_t (&v)[E], uint64_t* lds) {
   constexpr uint32_t P = static_cast<uint32_t>(E) * BS;
   const uint32_t t = threadIdx.x;
@@ -586,8 +587,9 @@ __device__ __forceinline__ void bitonic_sort_regs_desc(uint64_t (&v)[E], uint64_
           }
         }
       } else if (stride >= static_cast<uint32_t>(kWave)) {
-        uint64_t* cur = lds + (buf ? P : 0);
+        uint64_t* cur = lds + (ONE_BUF ? 0 : (buf ? P : 0));
         buf ^= 1;
+        if (ONE_BUF) __syncthreads();  // the previous stage's reads are done
 #pragma unroll
         for (int e = 0; e < E; ++e) cur[static_cast<uint32_t>(e) * BS + t] = v[e];
         __syncthreads();

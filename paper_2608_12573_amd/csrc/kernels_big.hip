@@ -21,7 +21,7 @@
 //                  tie class at the k-th key is split, digits of ~index.
 //   k_big_collect  every item of the top k, as a composite key, into a
 //                  staging array (one atomic per block).
-//   k_big_tile     sorts tiles of 4096 composites in LDS.
+//   k_big_tile     sorts tiles of 16384 composites in LDS.
 //   k_big_merge    merge-path passes doubling the sorted run length.
 //   k_big_write    values, indices and the per-call report.
 #include "device_common.h"
@@ -71,7 +71,7 @@ struct BigArgs {
   uint32_t* boff;      // kLogBins: first slot of each bucket (descending order)
   uint32_t* bcur;      // kLogBins * kBktPad: entries placed in bucket b at b * kBktPad
   uint32_t* blist;     // kLogBins: the non-empty buckets >= b*, descending
-  uint32_t P;          // padded length: k rounded up to kBigTile
+  uint32_t P;          // padded length: k rounded up to kBigSortTile
   void* out_vals;
   int64_t* out_idx;
   profk_info_t* info;
@@ -566,21 +566,21 @@ __global__ __launch_bounds__(kBigBS) void k_big_collect(BigArgs a) {
 }
 
 // ----------------------------------------------------------------- sort ---
-// Sorts each tile of kBigTile composites descending; entries past kk are
-// padding (0, below every real composite).
+// Sorts each tile of kBigSortTile composites descending; entries past kk are
+// zero (they sort last).  One LDS buffer of the tile (128 KiB).
 __global__ __launch_bounds__(1024) void k_big_tile(BigArgs a) {
-  __shared__ uint64_t exch[2 * kBigTile];
+  __shared__ uint64_t exch[kBigSortTile];
   if (a.bs->mode == kModeBucket) return;
   const uint32_t kk = a.bs->kk;
-  const uint32_t t0 = blockIdx.x * kBigTile;
-  constexpr int E = kBigTile / 1024;
+  const uint32_t t0 = blockIdx.x * kBigSortTile;
+  constexpr int E = kBigSortTile / 1024;
   uint64_t v[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const uint32_t p = t0 + e * 1024 + threadIdx.x;
     v[e] = p < kk ? a.staging[p] : 0ull;
   }
-  bitonic_sort_regs_desc<1024, E>(v, exch);
+  bitonic_sort_regs_desc<1024, E, true>(v, exch);
 #pragma unroll
   for (int e = 0; e < E; ++e) a.runs[t0 + e * 1024 + threadIdx.x] = v[e];
 }
@@ -701,7 +701,7 @@ static inline uint32_t cdiv_u(uint64_t a, uint64_t b) { return static_cast<uint3
 template <int DT>
 static hipError_t launch_big_t(const BigCall& c) {
   constexpr int KB = Elem<DT>::KEYBITS;
-  const uint32_t P = cdiv_u(c.k, kBigTile) * kBigTile;
+  const uint32_t P = cdiv_u(c.k, kBigSortTile) * kBigSortTile;
   BigArgs a{c.values, c.n, c.k, c.k_req, c.M, c.direct, c.seg_cnt, c.seg_key, c.seg_idx, c.blk_max,
             c.seg_cap, c.G_f, c.st, reinterpret_cast<BigState*>(c.big_state), c.ghist, c.staging, c.runs,
             c.fhist, c.boff, c.bcur, c.blist, P, c.out_vals, c.out_idx, c.info};
@@ -715,10 +715,10 @@ static hipError_t launch_big_t(const BigCall& c) {
     hipLaunchKernelGGL((k_big_pass<DT, 1>), dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
   hipLaunchKernelGGL(k_big_collect<DT>, dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
   const uint32_t tiles = P / kBigTile;
-  hipLaunchKernelGGL(k_big_tile, dim3(tiles), dim3(1024), 0, c.stream, a);
+  hipLaunchKernelGGL(k_big_tile, dim3(P / kBigSortTile), dim3(1024), 0, c.stream, a);
   uint64_t* src = c.runs;
   uint64_t* dst = c.staging;
-  for (uint32_t L = kBigTile; L < P; L *= 2) {
+  for (uint32_t L = kBigSortTile; L < P; L *= 2) {
     hipLaunchKernelGGL(k_big_merge, dim3(tiles), dim3(1024), 0, c.stream, a.bs, src, dst, P, L);
     uint64_t* t = src;
     src = dst;

@@ -942,7 +942,7 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   L.off_seg_idx = take(static_cast<size_t>(kSegs) * M * 4);
   L.big = k > static_cast<uint32_t>(kFinMaxK);
   if (L.big) {
-    const size_t P = static_cast<size_t>(cdiv(k, kBigTile)) * kBigTile;
+    const size_t P = static_cast<size_t>(cdiv(k, kBigSortTile)) * kBigSortTile;
     L.G_big = static_cast<uint32_t>(num_cus < kBigMaxBlocks ? num_cus : kBigMaxBlocks);
     L.off_big_state = take(256);
     L.off_ghist = take(static_cast<size_t>(kBigBins) * 4);

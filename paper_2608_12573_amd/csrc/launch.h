@@ -75,7 +75,8 @@ constexpr int kBigBS = 256;
 constexpr int kBigDigit = 11;
 constexpr uint32_t kBigBins = 1u << kBigDigit;
 constexpr int kBigStage = 4096;               // composites a collect block stages in LDS
-constexpr uint32_t kBigTile = 4096;           // composites sorted per block
+constexpr uint32_t kBigTile = 4096;           // composites a merge block writes
+constexpr uint32_t kBigSortTile = 16384;      // composites sorted per block before the merges
 constexpr int kBigMaxBlocks = 256;
 constexpr uint32_t kBktCap = 4096;            // largest bucket one sort block holds
 constexpr uint32_t kBktPad = 32;              // words between bucket fill counters (own 128-byte line)
