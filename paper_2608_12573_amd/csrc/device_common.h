@@ -271,14 +271,18 @@ __device__ __forceinline__ void acquire_agent() { __builtin_amdgcn_fence(__ATOMI
 // serialise every lane on one LDS address.  May be called from divergent
 // code: only the lanes that execute it take part.
 __device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
-  const uint64_t act = __ballot(active);
-  if (act == 0) return;
-  const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
-  const uint32_t lb = __shfl(bin, leader, kWave);
-  const bool same = active && bin == lb;
+  if (!active) return;
+  // only the active lanes run this: the first of them is the leader, and its
+  // bin is read as a scalar
+  const uint32_t lb = __builtin_amdgcn_readfirstlane(bin);
+  const bool same = bin == lb;
   const uint64_t sm = __ballot(same);
-  if (static_cast<int>(threadIdx.x & (kWave - 1)) == leader) atomicAdd(&hist[lb], static_cast<uint32_t>(__popcll(sm)));
-  if (active && !same) atomicAdd(&hist[bin], 1u);
+  if (same) {
+    if (static_cast<int>(threadIdx.x & (kWave - 1)) == __ffsll(static_cast<unsigned long long>(sm)) - 1)
+      atomicAdd(&hist[lb], static_cast<uint32_t>(__popcll(sm)));
+  } else {
+    atomicAdd(&hist[bin], 1u);
+  }
 }
 
 // Slot in an LDS list for each calling lane with `take` set: one atomic on

@@ -63,6 +63,28 @@ __global__ __launch_bounds__(BS) void k_sample(SampleArgs a) {
   sample_block_top<BS, Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
 }
 
+// Per-block top-t of keys already in memory (the SAE path's sampled
+// latents, 32-bit keys): block b takes keys [4*BS*b, 4*BS*(b+1)) and writes
+// its top min(t, nb) to union_keys + b * tcap, as k_sample does for its
+// draws, so that one block then selects tau from a union much smaller than
+// the sample.
+template <int BS>
+__global__ __launch_bounds__(BS) void k_key_union(const uint32_t* keys, uint32_t n, uint32_t t, uint32_t tcap,
+                                                  uint32_t* union_keys) {
+  __shared__ SampleUnionShared<BS> sh;
+  const uint32_t b = blockIdx.x, tid = threadIdx.x;
+  const uint32_t j0 = b * 4 * BS, nb = min(4u * BS, n - j0);
+  uint32_t kv[4];
+  uint32_t valid = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t j = 4 * tid + q;
+    kv[q] = j < nb ? keys[j0 + j] : 0u;
+    if (j < nb) valid |= 1u << q;
+  }
+  sample_block_top<BS, 32>(kv, valid, nb, t, union_keys + static_cast<size_t>(b) * tcap, sh);
+}
+
 // ------------------------------------------------------------ stage 2 -----
 // tau = t-th largest key of the union.  Used when the union is too large
 // for the filter blocks to select from it themselves.
@@ -126,7 +148,7 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
     else for_items<kTauBS, 8>(a.n, gload, [&](uint32_t, uint32_t v) { f(v); });
   };
   uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-  for_items<kTauBS, 8>(a.n, gload, [&](uint32_t i, uint32_t v) {
+  for_items<kTauBS, 16>(a.n, gload, [&](uint32_t i, uint32_t v) {
     if (cached) cache[i] = v;
     mn = min(mn, v);
     mx = max(mx, v);
@@ -148,7 +170,16 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
     const uint32_t pre = mn & hmask;
     for (uint32_t i = tid; i < static_cast<uint32_t>(kSelBins); i += kTauBS) sel.hist[i] = 0;
     __syncthreads();
-    all([&](uint32_t v) { hist_add(sel.hist, (v >> shift) & (kSelBins - 1), true); });
+    // Keys equal to the minimum (a sample of ReLU outputs is mostly +0) are
+    // counted apart and added to their bin once: on one LDS address every
+    // wave's increment would wait for the others'.
+    uint32_t n_min = 0;
+    all([&](uint32_t v) {
+      if (v == mn) ++n_min;
+      else hist_add(sel.hist, (v >> shift) & (kSelBins - 1), true);
+    });
+    n_min = block_sum<kTauBS>(n_min, sel.wsum);
+    if (tid == 0 && n_min) sel.hist[(mn >> shift) & (kSelBins - 1)] += n_min;
     __syncthreads();
     if (tid < kWave) rank_bin_search(sel.hist, kSelBins, a.t, sel.scratch());
     __syncthreads();
@@ -1059,6 +1090,18 @@ hipError_t launch_select_tau(const uint32_t* union_keys, uint32_t n, uint32_t t,
   TauArgs ta{union_keys, n, t, keybits, st};
   hipLaunchKernelGGL(k_select_tau, dim3(1), dim3(kTauBS), 0, s, ta);
   return hipGetLastError();
+}
+
+hipError_t launch_select_tau_keys(const uint32_t* keys, uint32_t n, uint32_t t, uint32_t* union_keys,
+                                  size_t union_words, CallState* st, hipStream_t s) {
+  constexpr uint32_t spb = 4u * kSampWideBS;
+  const uint32_t G = cdiv(n, spb), tcap = t < spb ? t : spb;
+  const uint32_t last_nb = n - (G - 1) * spb;
+  const uint32_t un = (G - 1) * tcap + (t < last_nb ? t : last_nb);
+  if (static_cast<uint64_t>(un) * 2 > n || static_cast<size_t>(G) * tcap > union_words)
+    return launch_select_tau(keys, n, t, 32, st, s);  // no real reduction: select over the keys
+  hipLaunchKernelGGL(k_key_union<kSampWideBS>, dim3(G), dim3(kSampWideBS), 0, s, keys, n, t, tcap, union_keys);
+  return launch_select_tau(union_keys, un, t, 32, st, s);
 }
 
 hipError_t launch_sample_indices(uint64_t seed, uint64_t row, uint32_t S, uint64_t N, int64_t* out,

@@ -843,9 +843,11 @@ hipError_t launch_sae_topk(const SaeCall& c) {
   const SaeGemm g = gemm_of(c);
   hipError_t e = launch_sae_sample(c);
   if (e != hipSuccess) return e;
-  // tau: the t-th largest of the S sampled keys, selected by one block
-  if ((e = launch_select_tau(reinterpret_cast<const uint32_t*>(ws + c.L.off_skeys), static_cast<uint32_t>(p.S),
-                             static_cast<uint32_t>(p.t), 32, st, c.stream)) != hipSuccess)
+  // tau: the t-th largest of the S sampled keys (per-block top-t lists in
+  // the vector path's union space, then one block)
+  if ((e = launch_select_tau_keys(reinterpret_cast<const uint32_t*>(ws + c.L.off_skeys), static_cast<uint32_t>(p.S),
+                                  static_cast<uint32_t>(p.t), reinterpret_cast<uint32_t*>(ws + L.off_union),
+                                  static_cast<size_t>(L.G_s) * L.tcap, st, c.stream)) != hipSuccess)
     return e;
   float2* col = reinterpret_cast<float2*>(ws + c.L.off_thr);
   const uint32_t d_pad = cdiv_s(c.d_dict, kSaeFBN) * kSaeFBN;

@@ -134,6 +134,10 @@ int filter_blocks_per_cu(int dtype, int want);
 hipError_t launch_refine(const FlatCall& c, uint32_t G_f);
 hipError_t launch_select_tau(const uint32_t* union_keys, uint32_t n, uint32_t t, int keybits, CallState* st,
                              hipStream_t s);
+// tau over n 32-bit keys in memory: per-block top-t lists into union_keys
+// (union_words long) first when that shrinks the set, then one block.
+hipError_t launch_select_tau_keys(const uint32_t* keys, uint32_t n, uint32_t t, uint32_t* union_keys,
+                                  size_t union_words, CallState* st, hipStream_t s);
 
 struct BigCall {
   int dtype;
