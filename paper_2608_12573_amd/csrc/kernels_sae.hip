@@ -9,7 +9,8 @@
 //   k_sae_sample   stage 1: the S sampled latents, each computed with the same
 //                  MFMA sequence as the GEMM (so its value is the GEMM's, bit
 //                  for bit);
-//   k_select_tau   stage 2 (shared with the vector path), over the S keys;
+//   k_key_union,   stage 2 (shared with the vector path): per-block top-t
+//   k_select_tau   lists of the S keys, then one block over their union;
 //   k_sae_thresholds  each column's accumulator threshold for tau, with its
 //                  bias;
 //   k_sae_filter   the GEMM with stage 3 in its epilogue: survivors are
@@ -76,8 +77,8 @@ struct XcdTiles {
 
 
 // ------------------------------------------------------------ stage 1 -----
-// k_sae_sample: every draw's latent key, into skeys[S]; k_select_tau then
-// takes the t-th largest of them.
+// k_sae_sample: every draw's latent key, into skeys[S]; k_key_union and
+// k_select_tau then take the t-th largest of them.
 
 struct SaeSampleArgs {
   SaeGemm g;
@@ -217,14 +218,14 @@ constexpr uint32_t kSaeSlice = kStage / (kSaeBS / kWave);  // survivors a wave s
 
 // The filter's GEMM: 256 x 256 tiles (waves in a 4 x 2 grid, 64 x 128 each
 // as 2 x 4 32x32 accumulators), twice the arithmetic per loaded byte and per
-// LDS fragment read of the 256 x 128 tiles above.  d_model is consumed in
+// LDS fragment read of 256 x 128 tiles with 64 x 64 wave blocks.  d_model is consumed in
 // chunks of kSaeFK, in two LDS stages that direct-to-LDS loads fill
 // (global_load_lds, 16 bytes per lane: lane L of a wave's instruction fills
 // the granule at the instruction's base + L), so no registers stage them.
 // Fragments are double-buffered in registers: the reads of a k-step are in
 // flight during the previous k-step's MFMAs, and a chunk's last MFMAs are in
 // flight during the wait and barrier for the next chunk.  The k-steps are the
-// same 32x32x16 MFMAs in the same ascending order as sae_tile_mma, so every
+// same 32x32x16 MFMAs in the same ascending order as k_sae_sample's, so every
 // latent is bit-identical to the sample's and the dense kernel's.
 constexpr uint32_t kSaeFBM = 256, kSaeFBN = 256, kSaeFK = 64;
 constexpr uint32_t kSaeFSeg = kSaeFK / 8;              // 16-byte granules of a row in a chunk
