@@ -296,7 +296,7 @@ __device__ __forceinline__ uint32_t lds_append(uint32_t* counter, bool take) {
   const uint32_t lane = threadIdx.x & (kWave - 1);
   uint32_t base = 0;
   if (static_cast<int>(lane) == leader) base = atomicAdd(counter, static_cast<uint32_t>(__popcll(m)));
-  base = __shfl(base, leader, kWave);
+  base = __builtin_amdgcn_readlane(base, leader);
   const uint64_t below = lane == 0 ? 0ull : (m & (~0ull >> (kWave - lane)));
   return base + static_cast<uint32_t>(__popcll(below));
 }

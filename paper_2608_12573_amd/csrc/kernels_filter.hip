@@ -144,16 +144,16 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   // stage go straight to the block's segment.
   auto reserve = [&](uint32_t cnt, uint32_t& slot, uint32_t& first_over, uint32_t& gbase) {
     const uint32_t incl = wave_incl_sum(cnt);
-    const uint32_t total = __shfl(incl, kWave - 1, kWave);
+    const uint32_t total = __builtin_amdgcn_readlane(incl, kWave - 1);  // (scalar reads, no lane permute)
     uint32_t base = 0;
     if (lane == 0) base = atomicAdd(&s_cnt, total);
-    base = __shfl(base, 0, kWave);
+    base = __builtin_amdgcn_readlane(base, 0);
     const uint32_t n_in = base < kStage ? min(total, kStage - base) : 0u;
     const uint32_t n_over = total - n_in;
     gbase = 0;
     if (n_over) {
       if (lane == 0) gbase = atomicAdd(seg_counter, n_over);
-      gbase = __shfl(gbase, 0, kWave);
+      gbase = __builtin_amdgcn_readlane(gbase, 0);
     }
     first_over = base + n_in;
     slot = base + incl - cnt;

@@ -173,10 +173,10 @@ __global__ __launch_bounds__(kRowBS) void k_rows(RowArgs a) {
     uint32_t my_max = 0;
     auto reserve = [&](uint32_t cnt) {
       const uint32_t incl = wave_incl_sum(cnt);
-      const uint32_t total = __shfl(incl, kWave - 1, kWave);
+      const uint32_t total = __builtin_amdgcn_readlane(incl, kWave - 1);
       uint32_t base = 0;
       if (lane == 0) base = atomicAdd(&s_cnt, total);
-      return __shfl(base, 0, kWave) + incl - cnt;
+      return __builtin_amdgcn_readlane(base, 0) + incl - cnt;
     };
     auto store = [&](uint32_t slot, uint32_t key, uint32_t idx) {
       my_max = max(my_max, key);
