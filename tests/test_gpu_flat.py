@@ -185,6 +185,25 @@ def test_relaxed_recall_flat():
         rec, ref = _f32_case(x, 2000, seed, recall=0.9)
 
 
+@pytest.mark.parametrize("survivors", [1900, 1801])
+def test_relaxed_partial_output_small_k(survivors):
+    # k_req <= count < k at k <= 4096: every candidate is refined (rank k
+    # lies past them), shared out among several refining workgroups, and
+    # workgroup 0 writes the padding after the count
+    x = workloads.normal_f32(2**20, seed=26)
+    bits = okeys.f32_bits(x)
+    key = np.sort(okeys.key_u32(bits).astype(np.int64))
+    k = 2000
+    p = pk.plan(x.size, k, 1e-3, 0.9, S_min=8192, S_max=8192, force_mode=pk.FORCE_FILTER)
+    q = plan_from_lib(p)
+    tau = int(key[-survivors])
+    note(f"flat relaxed partial k={k} survivors={survivors} k_req={p.k_req}")
+    vals, idx, info = pk.topk_tau(gpu_f32(x), k, tau, p)
+    ref = oprofk.run(bits, "f32", k, q, 0, tau_override=tau)
+    assert ref.status == oprofk.STATUS_FILTERED and ref.n_valid == survivors
+    compare(vals, idx, info, ref, "f32")
+
+
 # ------------------------------------------------------- forced failures --
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_forced_underflow_and_overflow(dtype):
