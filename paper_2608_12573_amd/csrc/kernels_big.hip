@@ -4,12 +4,12 @@
 // Same result as the one-block path -- the exact top-k under the total
 // order, sorted -- computed across the GPU.  A filtered call whose
 // candidates spread over small buckets takes the bucket path:
-//   k_bkt_plan     status; bucket offsets in descending bucket order from
-//                  the filter's histogram of log_bin(key - tau), and the
-//                  bucket b* holding rank k; when the bucket path does not
-//                  apply, the radix path's state instead;
-//   k_bkt_scatter  every candidate of a bucket >= b* into its bucket's range
-//                  of the staging array;
+//   k_bkt_scatter  in every block, the status, bucket offsets in descending
+//                  bucket order from the filter's histogram of
+//                  log_bin(key - tau) and the bucket b* holding rank k
+//                  (block 0 records them, or the radix path's state when the
+//                  bucket path does not apply); then every candidate of a
+//                  bucket >= b* into its bucket's range of the staging array;
 //   k_bkt_sort     one block per bucket sorts it in LDS and writes the
 //                  outputs at the bucket's offset.
 // Every other call (a fallback, DIRECT, or a bucket larger than kBktCap)
@@ -22,8 +22,9 @@
 //   k_big_collect  every item of the top k, as a composite key, into a
 //                  staging array (one atomic per block).
 //   k_big_tile     sorts tiles of 16384 composites in LDS.
-//   k_big_merge    merge-path passes doubling the sorted run length.
-//   k_big_write    values, indices and the per-call report.
+//   k_big_merge    merge-path passes doubling the sorted run length; the
+//                  last pass (or the tile sort, for a single tile) writes
+//                  values, indices and the per-call report.
 #include "device_common.h"
 #include "filter_tile.h"
 #include "launch.h"
@@ -144,8 +145,8 @@ __device__ __forceinline__ void load_segn(const BigArgs& a, uint32_t* segn) {
 }
 
 // ---------------------------------------------------------------- begin ---
-// The radix path's state, from the call's status (run by k_bkt_plan's
-// workgroup of 1024 when the bucket path does not apply).
+// The radix path's state, from the call's status (run by block 0 of
+// k_bkt_scatter, 1024 threads, when the bucket path does not apply).
 template <int DT>
 __device__ __forceinline__ void big_begin(const BigArgs& a, uint32_t status, uint32_t total, uint32_t* wsum) {
   constexpr int KB = Elem<DT>::KEYBITS;
@@ -195,46 +196,65 @@ __device__ __forceinline__ void big_begin(const BigArgs& a, uint32_t status, uin
 }
 
 // ----------------------------------------------------------- bucket path ---
+// Candidates are placed sweep by sweep: a block counts one sweep's items per
+// bucket in LDS, reserves each bucket's range with one global atomic, and
+// writes every item at its range base plus its rank within the block.
+//
+// The plan comes first, in every block: the status from the segment
+// counters, then, for a filtered call, bucket offsets in descending bucket
+// order from the filter's histogram of log_bin(key - tau), the bucket b*
+// holding rank kk, and whether every bucket >= b* fits one sort block.  All
+// blocks read the same counts and so derive the same plan; none waits for
+// another.  Block 0 also records it for the kernels after this one: the
+// bucket path's state, offsets, bucket list, padding and report, or, when
+// the bucket path does not apply, the radix path's state.  The fill
+// counters (bcur) are zeroed at the start of the call.
+constexpr int kScatBS = 1024, kScatU = 4;
+
 template <int DT>
-__global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
+__global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
+  __shared__ uint32_t hist[kLogBins];  // counts of the sweep, then its range bases
+  __shared__ uint32_t boff[kLogBins];  // first slot of each bucket (descending bucket order)
+  __shared__ uint32_t segn[kSegs];
   __shared__ SelectScratch fs;
   __shared__ uint32_t s_total;
   BigState* s = a.bs;
   const uint32_t tid = threadIdx.x;
+  const bool lead = blockIdx.x == 0;
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
   if (!a.direct) {
     if (tid == 0) {
       uint32_t t = 0;
       for (int x = 0; x < kSegs; ++x) t += a.seg_cnt[x * kSegStride];
       s_total = t;
+      fs.found[0] = 0;
     }
     __syncthreads();
     total = s_total;
     status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
   }
-  if (status != PROFK_STATUS_FILTERED) {
-    big_begin<DT>(a, status, total, fs.wsum);
+  if (status != PROFK_STATUS_FILTERED) {  // uniform over the grid
+    if (lead) big_begin<DT>(a, status, total, fs.wsum);
     return;
   }
   const uint32_t kk = min(a.k, total);
-  // Bucket offsets in descending bucket order: thread t owns buckets
-  // [kLogBins - 4(t+1), kLogBins - 4t).
+  // thread t owns buckets [kLogBins - 4(t+1), kLogBins - 4t)
   constexpr uint32_t kOwners = kLogBins / 4;
-  static_assert(kLogBins % 4 == 0 && kOwners <= 1024, "bucket ownership");
+  static_assert(kLogBins % 4 == 0 && kOwners <= kScatBS, "bucket ownership");
+  const bool owner = tid < kOwners;
+  const uint32_t bbase = owner ? kLogBins - 4 * (tid + 1) : 0u;
   uint32_t h[4] = {0u, 0u, 0u, 0u};
-  const uint32_t bbase = kLogBins - 4 * (tid + 1);
-  if (tid < kOwners) {
+  if (owner) {
     const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
     h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
   }
-  const uint32_t above_me = block_excl_sum<1024>(h[0] + h[1] + h[2] + h[3], fs.wsum, nullptr);
-  if (tid < kOwners) {
+  const uint32_t above_me = block_excl_sum<kScatBS>(h[0] + h[1] + h[2] + h[3], fs.wsum, nullptr);
+  if (owner) {
     uint32_t run = above_me;
 #pragma unroll
     for (int j = 3; j >= 0; --j) {
-      a.boff[bbase + j] = run;
-      a.bcur[(bbase + j) * kBktPad] = 0;
+      boff[bbase + j] = run;
       if (run < kk && kk <= run + h[j]) fs.found[0] = bbase + j;
       run += h[j];
     }
@@ -242,7 +262,7 @@ __global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
   __syncthreads();
   const uint32_t bstar = fs.found[0];
   uint32_t big = 0, nonempty = 0;
-  if (tid < kOwners) {
+  if (owner) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       if (bbase + j >= bstar) {
@@ -250,56 +270,47 @@ __global__ __launch_bounds__(1024) void k_bkt_plan(BigArgs a) {
         nonempty += h[j] ? 1u : 0u;
       }
   }
-  // the list of non-empty buckets >= b*, in descending bucket order
-  uint32_t nlist = 0;
-  uint32_t lpos = block_excl_sum<1024>(nonempty, fs.wsum, &nlist);
-  if (tid < kOwners) {
-#pragma unroll
-    for (int j = 3; j >= 0; --j)
-      if (bbase + j >= bstar && h[j]) a.blist[lpos++] = bbase + j;
-  }
-  big = block_max<1024>(big, fs.wsum);
-  const bool bucket = big <= kBktCap;
-  if (!bucket) {
-    big_begin<DT>(a, status, total, fs.wsum);
+  big = block_max<kScatBS>(big, fs.wsum);
+  if (big > kBktCap) {  // uniform over the grid: the radix path
+    if (lead) big_begin<DT>(a, status, total, fs.wsum);
     return;
   }
-  if (tid == 0) {
-    s->mode = kModeBucket;
-    s->bstar = bstar;
-    s->nlist = nlist;
-    s->status = status;
-    s->total = total;
-    s->tau = a.st->tau_key;
-    s->n_src = total;
-    s->from_input = 0;
-    s->kk = kk;
+  const uint32_t tau = a.st->tau_key;
+  if (lead) {
+    // the non-empty buckets >= b*, in descending bucket order
+    uint32_t nlist = 0;
+    uint32_t lpos = block_excl_sum<kScatBS>(nonempty, fs.wsum, &nlist);
+    if (owner) {
+#pragma unroll
+      for (int j = 3; j >= 0; --j) {
+        a.boff[bbase + j] = boff[bbase + j];
+        if (bbase + j >= bstar && h[j]) a.blist[lpos++] = bbase + j;
+      }
+    }
+    if (tid == 0) {
+      s->mode = kModeBucket;
+      s->bstar = bstar;
+      s->nlist = nlist;
+      s->status = status;
+      s->total = total;
+      s->tau = tau;
+      s->n_src = total;
+      s->from_input = 0;
+      s->kk = kk;
+    }
+    for (uint32_t p = kk + tid; p < a.k; p += kScatBS) {  // relaxed recall: padding
+      if (DT == 0) static_cast<uint32_t*>(a.out_vals)[p] = 0xFF800000u;
+      else static_cast<uint16_t*>(a.out_vals)[p] = 0xFF80u;
+      a.out_idx[p] = -1;
+    }
+    if (tid == 0 && a.info) {
+      a.info->count = total;
+      a.info->tau_key = tau;
+      a.info->status = static_cast<int32_t>(status);
+      a.info->n_valid = kk;
+    }
   }
-  for (uint32_t p = kk + tid; p < a.k; p += 1024) {  // relaxed recall: padding
-    if (DT == 0) static_cast<uint32_t*>(a.out_vals)[p] = 0xFF800000u;
-    else static_cast<uint16_t*>(a.out_vals)[p] = 0xFF80u;
-    a.out_idx[p] = -1;
-  }
-  if (tid == 0 && a.info) {
-    a.info->count = total;
-    a.info->tau_key = a.st->tau_key;
-    a.info->status = static_cast<int32_t>(status);
-    a.info->n_valid = kk;
-  }
-}
-
-// Candidates are placed sweep by sweep: a block counts one sweep's items per
-// bucket in LDS, reserves each bucket's range with one global atomic, and
-// writes every item at its range base plus its rank within the block.
-constexpr int kScatBS = 1024, kScatU = 4;
-
-template <int DT>
-__global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
-  __shared__ uint32_t hist[kLogBins];  // counts of the sweep, then its range bases
-  __shared__ uint32_t segn[kSegs];
-  const BigState* s = a.bs;
-  if (s->mode != kModeBucket) return;
-  const uint32_t tid = threadIdx.x, n = s->total, tau = s->tau, bstar = s->bstar;
+  const uint32_t n = total;
   load_segn(a, segn);
   const SegPos pos{segn, a.seg_cap};
   constexpr uint32_t per = kScatBS * kScatU;
@@ -327,7 +338,7 @@ __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
     __syncthreads();
     for (uint32_t b = tid; b < kLogBins; b += kScatBS) {
       const uint32_t c = hist[b];
-      if (c) hist[b] = a.boff[b] + atomicAdd(&a.bcur[b * kBktPad], c);
+      if (c) hist[b] = boff[b] + atomicAdd(&a.bcur[b * kBktPad], c);
     }
     __syncthreads();
 #pragma unroll
@@ -565,13 +576,43 @@ __global__ __launch_bounds__(kBigBS) void k_big_collect(BigArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- write ---
+// Output i of the radix path from the i-th composite of the sorted order
+// (the last sorting pass calls it): value and index for i < kk, the padding
+// of a relaxed call after that, and the per-call report from output 0.
+template <int DT>
+__device__ __forceinline__ void big_out(const BigArgs& a, const BigState* s, uint32_t kk, uint32_t i, uint64_t c) {
+  if (i >= a.k) return;
+  uint32_t bits;
+  int64_t id;
+  if (i < kk) {
+    bits = bits_of_key<DT>(comp_key(c));
+    id = comp_idx(c);
+  } else {
+    bits = DT == 0 ? 0xFF800000u : 0xFF80u;
+    id = -1;
+  }
+  if (DT == 0) static_cast<uint32_t*>(a.out_vals)[i] = bits;
+  else static_cast<uint16_t*>(a.out_vals)[i] = static_cast<uint16_t>(bits);
+  a.out_idx[i] = id;
+  if (i == 0 && a.info) {
+    a.info->count = s->total;
+    a.info->tau_key = s->tau;
+    a.info->status = static_cast<int32_t>(s->status);
+    a.info->n_valid = kk;
+  }
+}
+
 // ----------------------------------------------------------------- sort ---
 // Sorts each tile of kBigSortTile composites descending; entries past kk are
-// zero (they sort last).  One LDS buffer of the tile (128 KiB).
+// zero (they sort last).  One LDS buffer of the tile (128 KiB).  FINAL (a
+// single tile, no merge after it): the outputs are written from the tile.
+template <int DT, bool FINAL>
 __global__ __launch_bounds__(1024) void k_big_tile(BigArgs a) {
   __shared__ uint64_t exch[kBigSortTile];
-  if (a.bs->mode == kModeBucket) return;
-  const uint32_t kk = a.bs->kk;
+  const BigState* s = a.bs;
+  if (s->mode == kModeBucket) return;
+  const uint32_t kk = s->kk;
   const uint32_t t0 = blockIdx.x * kBigSortTile;
   constexpr int E = kBigSortTile / 1024;
   uint64_t v[E];
@@ -582,14 +623,19 @@ __global__ __launch_bounds__(1024) void k_big_tile(BigArgs a) {
   }
   bitonic_sort_regs_desc<1024, E, true>(v, exch);
 #pragma unroll
-  for (int e = 0; e < E; ++e) a.runs[t0 + e * 1024 + threadIdx.x] = v[e];
+  for (int e = 0; e < E; ++e) {
+    const uint32_t p = t0 + e * 1024 + threadIdx.x;
+    if constexpr (FINAL) big_out<DT>(a, s, kk, p, v[e]);
+    else a.runs[p] = v[e];
+  }
 }
 
 // One merge-path pass: sorted runs of length L in `in` become runs of 2L in
 // `out`.  Block b writes outputs [b*kBigTile, (b+1)*kBigTile), which lie in
 // one pair of runs; the split points are found by a wave-parallel search
 // on the runs in memory, the block's slices are staged in LDS, and each
-// thread merges kBigTile/1024 outputs from its own split.
+// thread merges kBigTile/1024 outputs from its own split.  FINAL (the last
+// pass, one run of P after it): the outputs are written instead of `out`.
 __device__ __forceinline__ bool take_more_a(const uint64_t* A, uint32_t la, const uint64_t* B, uint32_t lb,
                                             uint32_t o, uint32_t i) {
   // With i items from A among the first o outputs, should there be more?
@@ -622,11 +668,13 @@ __device__ __forceinline__ uint32_t corank_wave(const uint64_t* A, uint32_t la, 
   return lo;
 }
 
-__global__ __launch_bounds__(1024) void k_big_merge(const BigState* bs, const uint64_t* in, uint64_t* out,
-                                                    uint32_t P, uint32_t L) {
+template <int DT, bool FINAL>
+__global__ __launch_bounds__(1024) void k_big_merge(BigArgs a, const uint64_t* in, uint64_t* out, uint32_t L) {
   __shared__ uint64_t sa[kBigTile], sb[kBigTile];
   __shared__ uint32_t s_i[2];
-  if (bs->mode == kModeBucket) return;
+  const BigState* s = a.bs;
+  if (s->mode == kModeBucket) return;
+  const uint32_t P = a.P;
   const uint32_t tid = threadIdx.x;
   const uint32_t o_begin = blockIdx.x * kBigTile;
   const uint32_t pair0 = (o_begin / (2 * L)) * (2 * L);
@@ -661,37 +709,8 @@ __global__ __launch_bounds__(1024) void k_big_merge(const BigState* bs, const ui
     uint64_t v;
     if (ib >= nbb || (ia < na && sa[ia] > sb[ib])) v = sa[ia++];
     else v = sb[ib++];
-    out[o_begin + q0 + q] = v;
-  }
-}
-
-// ---------------------------------------------------------------- write ---
-template <int DT>
-__global__ void k_big_write(BigArgs a, const uint64_t* sorted) {
-  const BigState* s = a.bs;
-  if (s->mode == kModeBucket) return;
-  const uint32_t kk = s->kk;
-  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < a.k) {
-    uint32_t bits;
-    int64_t id;
-    if (i < kk) {
-      const uint64_t c = sorted[i];
-      bits = bits_of_key<DT>(comp_key(c));
-      id = comp_idx(c);
-    } else {
-      bits = DT == 0 ? 0xFF800000u : 0xFF80u;
-      id = -1;
-    }
-    if (DT == 0) static_cast<uint32_t*>(a.out_vals)[i] = bits;
-    else static_cast<uint16_t*>(a.out_vals)[i] = static_cast<uint16_t>(bits);
-    a.out_idx[i] = id;
-  }
-  if (i == 0 && a.info) {
-    a.info->count = s->total;
-    a.info->tau_key = s->tau;
-    a.info->status = static_cast<int32_t>(s->status);
-    a.info->n_valid = kk;
+    if constexpr (FINAL) big_out<DT>(a, s, s->kk, o_begin + q0 + q, v);
+    else out[o_begin + q0 + q] = v;
   }
 }
 
@@ -705,7 +724,6 @@ static hipError_t launch_big_t(const BigCall& c) {
   BigArgs a{c.values, c.n, c.k, c.k_req, c.M, c.direct, c.seg_cnt, c.seg_key, c.seg_idx, c.blk_max,
             c.seg_cap, c.G_f, c.st, reinterpret_cast<BigState*>(c.big_state), c.ghist, c.staging, c.runs,
             c.fhist, c.boff, c.bcur, c.blist, P, c.out_vals, c.out_idx, c.info};
-  hipLaunchKernelGGL(k_bkt_plan<DT>, dim3(1), dim3(1024), 0, c.stream, a);
   hipLaunchKernelGGL(k_bkt_scatter<DT>, dim3(c.G_big), dim3(kScatBS), 0, c.stream, a);
   hipLaunchKernelGGL(k_bkt_sort<DT>, dim3(kBktSortBlocks), dim3(kSortBS), 0, c.stream, a);
   const uint32_t key_passes = cdiv_u(KB, kBigDigit);
@@ -714,18 +732,22 @@ static hipError_t launch_big_t(const BigCall& c) {
   for (uint32_t p = 0; p < cdiv_u(32, kBigDigit); ++p)
     hipLaunchKernelGGL((k_big_pass<DT, 1>), dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
   hipLaunchKernelGGL(k_big_collect<DT>, dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
+  // tile sorts, then merge passes; the last of them writes the outputs
   const uint32_t tiles = P / kBigTile;
-  hipLaunchKernelGGL(k_big_tile, dim3(P / kBigSortTile), dim3(1024), 0, c.stream, a);
-  uint64_t* src = c.runs;
-  uint64_t* dst = c.staging;
-  for (uint32_t L = kBigSortTile; L < P; L *= 2) {
-    hipLaunchKernelGGL(k_big_merge, dim3(tiles), dim3(1024), 0, c.stream, a.bs, src, dst, P, L);
-    uint64_t* t = src;
-    src = dst;
-    dst = t;
+  if (P == kBigSortTile) {
+    hipLaunchKernelGGL((k_big_tile<DT, true>), dim3(1), dim3(1024), 0, c.stream, a);
+  } else {
+    hipLaunchKernelGGL((k_big_tile<DT, false>), dim3(P / kBigSortTile), dim3(1024), 0, c.stream, a);
+    uint64_t* src = c.runs;
+    uint64_t* dst = c.staging;
+    for (uint32_t L = kBigSortTile; L < P; L *= 2) {
+      if (2 * L < P) hipLaunchKernelGGL((k_big_merge<DT, false>), dim3(tiles), dim3(1024), 0, c.stream, a, src, dst, L);
+      else hipLaunchKernelGGL((k_big_merge<DT, true>), dim3(tiles), dim3(1024), 0, c.stream, a, src, dst, L);
+      uint64_t* t = src;
+      src = dst;
+      dst = t;
+    }
   }
-  hipLaunchKernelGGL(k_big_write<DT>, dim3(cdiv_u(c.k, 256)), dim3(256), 0, c.stream, a,
-                     static_cast<const uint64_t*>(src));
   return hipGetLastError();
 }
 

@@ -35,6 +35,7 @@ struct SampleArgs {
   CallState* st;
   uint32_t* seg_cnt;
   uint32_t* fhist;
+  uint32_t* bcur;  // null unless the call takes the large-k path
 };
 
 template <int DT, int BS>
@@ -42,7 +43,7 @@ __global__ __launch_bounds__(BS) void k_sample(SampleArgs a) {
   constexpr uint32_t kPer = 4 * BS;  // four draws per thread
   __shared__ SampleUnionShared<BS> sh;
   const uint32_t b = blockIdx.x, tid = threadIdx.x;
-  if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist);
+  if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist, a.bcur);
   const uint32_t j0 = b * kPer;
   const uint32_t nb = min(kPer, a.S - j0);
   uint32_t kv[4];
@@ -286,11 +287,12 @@ struct InitArgs {
   CallState* st;
   uint32_t* seg_cnt;
   uint32_t* fhist;
+  uint32_t* bcur;  // null unless the call takes the large-k path
   uint32_t tau_key;
 };
 
 __global__ void k_init_state(InitArgs a) {
-  reset_state(a.st, a.seg_cnt, a.fhist);
+  reset_state(a.st, a.seg_cnt, a.fhist, a.bcur);
   if (threadIdx.x == 0) a.st->tau_key = a.tau_key;
 }
 
@@ -1048,15 +1050,16 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   const bool direct = p.mode == PROFK_MODE_DIRECT && !c.use_tau;
   const bool lex = p.lexicographic && !direct && !c.use_tau;  // a caller's tau: the key rule
   uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
+  uint32_t* bcur = L.big ? at<uint32_t>(c.ws, L.off_bcur) : nullptr;
   const uint32_t* union_for_filter = nullptr;
   hipError_t e;
   if (direct || c.use_tau) {
     hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream,
-                       InitArgs{st, seg_cnt, fhist, c.use_tau ? c.tau_key : 0u});
+                       InitArgs{st, seg_cnt, fhist, bcur, c.use_tau ? c.tau_key : 0u});
   } else {
     uint32_t* uk = at<uint32_t>(c.ws, L.off_union);
     SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
-                  L.tcap, uk, st, seg_cnt, fhist};
+                  L.tcap, uk, st, seg_cnt, fhist, bcur};
     if (L.samp_bs == kSampWideBS) hipLaunchKernelGGL((k_sample<DT, kSampWideBS>), dim3(L.G_s), dim3(kSampWideBS), 0, c.stream, sa);
     else hipLaunchKernelGGL((k_sample<DT, kSampBS>), dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
     if (!lex && L.union_n <= kFiltTauMax && static_cast<uint32_t>(p.t) <= kFiltTauInMaxT) {
@@ -1119,7 +1122,8 @@ hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* b
   uint32_t* seg_cnt = at<uint32_t>(c.ws, L.off_segcnt);
   (void)hipGetLastError();
   uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
-  hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream, InitArgs{st, seg_cnt, fhist, c.tau_key});
+  hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream,
+                     InitArgs{st, seg_cnt, fhist, L.big ? at<uint32_t>(c.ws, L.off_bcur) : nullptr, c.tau_key});
   hipError_t e = launch_filter(c, st, nullptr, false);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_gather_buffer, dim3(1), dim3(1024), 0, c.stream, L.seg_cap, seg_cnt,
