@@ -17,6 +17,7 @@
 //                 the last of each group of 16 chunks to finish merges the
 //                 group's, and the last group to finish merges the groups'.
 #include <climits>
+#include <cmath>
 
 #include "device_common.h"
 #include "filter_tile.h"
@@ -36,6 +37,10 @@ struct SampleArgs {
   uint32_t* seg_cnt;
   uint32_t* fhist;
   uint32_t* bcur;  // null unless the call takes the large-k path
+  // capped lists (t is then their length): each block's cut key, and every
+  // draw's key at its draw number; null otherwise
+  uint32_t* cut;
+  uint32_t* all_keys;
 };
 
 template <int DT, int BS>
@@ -61,7 +66,17 @@ __global__ __launch_bounds__(BS) void k_sample(SampleArgs a) {
       }
     }
   }
-  sample_block_top<BS, Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh);
+  if (a.all_keys) {
+    if (4 * tid + 3 < nb) {
+      *reinterpret_cast<uint4*>(a.all_keys + j0 + 4 * tid) = uint4{kv[0], kv[1], kv[2], kv[3]};
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((valid >> q) & 1u) a.all_keys[j0 + 4 * tid + q] = kv[q];
+    }
+  }
+  sample_block_top<BS, Elem<DT>::KEYBITS>(kv, valid, nb, a.t, a.union_keys + static_cast<size_t>(b) * a.tcap, sh,
+                                           a.cut ? a.cut + b : nullptr);
 }
 
 // Per-block top-t of keys already in memory (the SAE path's sampled
@@ -97,6 +112,12 @@ struct TauArgs {
   uint32_t n, t;
   int keybits;
   CallState* st;
+  // capped sample lists (null otherwise): the n_cut blocks' cut keys, and
+  // all n_all sample keys to select from when a cut key reaches the result
+  const uint32_t* cut;
+  uint32_t n_cut;
+  const uint32_t* all_keys;
+  uint32_t n_all;
 };
 
 __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
@@ -140,16 +161,46 @@ __global__ __launch_bounds__(kTauBS) void k_select_tau(TauArgs a) {
     }
     return;
   }
-  auto gload = [&](uint32_t i) { return a.keys[i]; };
-  const bool cached = a.n <= kTauCache;
+  // Capped sample lists: the t-th largest of the union is the sample's
+  // unless a block that dropped keys has its cut key at or above it (every
+  // dropped key is at most its block's cut key).  With C the largest cut
+  // key, that is the case exactly when fewer than t union keys exceed C; the
+  // select then takes all sample keys instead.
+  const uint32_t* keys = a.keys;
+  uint32_t n = a.n;
+  if (a.cut) {
+    // the first 4*kTauBS union keys are loaded with the cut keys
+    constexpr int U = 4;
+    uint32_t u[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const uint32_t i = j * kTauBS + tid;
+      u[j] = i < a.n ? a.keys[i] : 0u;
+    }
+    uint32_t c = 0;
+    for (uint32_t i = tid; i < a.n_cut; i += kTauBS) c = max(c, a.cut[i]);
+    c = block_max<kTauBS>(c, sel.wsum);
+    uint32_t above = 0;
+#pragma unroll
+    for (int j = 0; j < U; ++j) above += (j * kTauBS + tid < a.n && u[j] > c) ? 1u : 0u;
+    for (uint32_t i = U * kTauBS + tid; i < a.n; i += kTauBS) above += a.keys[i] > c ? 1u : 0u;
+    // (the same in every thread: readfirstlane keeps the source uniform for
+    // the compiler)
+    if (__builtin_amdgcn_readfirstlane(block_sum<kTauBS>(above, sel.wsum)) < a.t) {
+      keys = a.all_keys;
+      n = a.n_all;
+    }
+  }
+  auto gload = [&](uint32_t i) { return keys[i]; };
+  const bool cached = n <= kTauCache;
   // every key of the union, from LDS when it fits (eight reads per thread
   // issued before any visitor runs)
   auto all = [&](auto f) {
-    if (cached) for_items<kTauBS, 8>(a.n, [&](uint32_t i) { return cache[i]; }, [&](uint32_t, uint32_t v) { f(v); });
-    else for_items<kTauBS, 8>(a.n, gload, [&](uint32_t, uint32_t v) { f(v); });
+    if (cached) for_items<kTauBS, 8>(n, [&](uint32_t i) { return cache[i]; }, [&](uint32_t, uint32_t v) { f(v); });
+    else for_items<kTauBS, 8>(n, gload, [&](uint32_t, uint32_t v) { f(v); });
   };
   uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-  for_items<kTauBS, 16>(a.n, gload, [&](uint32_t i, uint32_t v) {
+  for_items<kTauBS, 16>(n, gload, [&](uint32_t i, uint32_t v) {
     if (cached) cache[i] = v;
     mn = min(mn, v);
     mx = max(mx, v);
@@ -941,18 +992,30 @@ __global__ __launch_bounds__(1024) void k_gather_buffer(uint32_t cap, const uint
 static inline uint32_t cdiv(uint64_t a, uint64_t b) { return static_cast<uint32_t>((a + b - 1) / b); }
 static inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Length of the capped sample lists for a key-rule plan with t >
+// kWaveTopMax, or 0 when the draws of a block in the top t are too many for
+// kWaveTopMax to hold them with a margin of eight standard deviations.
+static uint32_t capped_list_len(uint32_t S, uint32_t t, bool lex) {
+  if (lex || t <= kWaveTopMax || S < 2u * kSampPerBlock) return 0;
+  const double mu = static_cast<double>(kSampPerBlock) * t / S;
+  const double need = mu + 8.0 * std::sqrt(mu) + 2.0;
+  return need <= kCapListSmall ? kCapListSmall : (need <= kWaveTopMax ? kWaveTopMax : 0u);
+}
+
 FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   FlatLayout L;
   const uint64_t N = static_cast<uint64_t>(p.N);
   const uint32_t epv = dtype == PROFK_F32 ? 4 : 8;
   const uint32_t S = static_cast<uint32_t>(p.S), t = static_cast<uint32_t>(p.t);
   const uint32_t M = static_cast<uint32_t>(p.M), k = static_cast<uint32_t>(p.k);
-  L.samp_bs = (!p.lexicographic && t > kWaveTopMax) ? kSampWideBS : kSampBS;
+  L.cap_list = capped_list_len(S, t, p.lexicographic != 0);
+  L.samp_bs = (!p.lexicographic && t > kWaveTopMax && !L.cap_list) ? kSampWideBS : kSampBS;
   const uint32_t spb = 4u * L.samp_bs;
+  const uint32_t tl = L.cap_list ? L.cap_list : t;  // length of a block's list
   L.G_s = cdiv(S, spb);
-  L.tcap = t < spb ? t : spb;
+  L.tcap = tl < spb ? tl : spb;
   const uint32_t last_nb = S - (L.G_s - 1) * spb;
-  L.union_n = (L.G_s - 1) * L.tcap + (t < last_nb ? t : last_nb);
+  L.union_n = (L.G_s - 1) * L.tcap + (tl < last_nb ? tl : last_nb);
   // Expected survivors per element are about t / (S + 1).
   const bool sparse = N * (dtype == PROFK_F32 ? 4u : 2u) >= kFiltSparseMinBytes &&
                       static_cast<uint64_t>(t) * kFiltSparseInvDensity < static_cast<uint64_t>(S) + 1;
@@ -970,6 +1033,10 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   L.off_state = take(sizeof(CallState));
   L.off_segcnt = take(static_cast<size_t>(kSegs) * kSegStride * 4);
   L.off_union = take(static_cast<size_t>(L.G_s) * L.tcap * 4);
+  if (L.cap_list) {
+    L.off_cut = take(static_cast<size_t>(L.G_s) * 4);
+    L.off_all_keys = take(static_cast<size_t>(S) * 4);
+  }
   L.off_blk_max = take(static_cast<size_t>(L.G_f) * 4);
   L.off_seg_key = take(static_cast<size_t>(kSegs) * M * 4);
   L.off_seg_idx = take(static_cast<size_t>(kSegs) * M * 4);
@@ -1058,14 +1125,18 @@ static hipError_t launch_flat_t(const FlatCall& c) {
                        InitArgs{st, seg_cnt, fhist, bcur, c.use_tau ? c.tau_key : 0u});
   } else {
     uint32_t* uk = at<uint32_t>(c.ws, L.off_union);
-    SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t),
-                  L.tcap, uk, st, seg_cnt, fhist, bcur};
+    SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S),
+                  L.cap_list ? L.cap_list : static_cast<uint32_t>(p.t), L.tcap, uk, st, seg_cnt, fhist, bcur,
+                  L.cap_list ? at<uint32_t>(c.ws, L.off_cut) : nullptr,
+                  L.cap_list ? at<uint32_t>(c.ws, L.off_all_keys) : nullptr};
     if (L.samp_bs == kSampWideBS) hipLaunchKernelGGL((k_sample<DT, kSampWideBS>), dim3(L.G_s), dim3(kSampWideBS), 0, c.stream, sa);
     else hipLaunchKernelGGL((k_sample<DT, kSampBS>), dim3(L.G_s), dim3(kSampBS), 0, c.stream, sa);
     if (!lex && L.union_n <= kFiltTauMax && static_cast<uint32_t>(p.t) <= kFiltTauInMaxT) {
       union_for_filter = uk;
     } else {
-      TauArgs ta{uk, L.union_n, static_cast<uint32_t>(p.t), Elem<DT>::KEYBITS, st};
+      TauArgs ta{uk, L.union_n, static_cast<uint32_t>(p.t), Elem<DT>::KEYBITS, st,
+                 L.cap_list ? at<uint32_t>(c.ws, L.off_cut) : nullptr, L.G_s,
+                 L.cap_list ? at<uint32_t>(c.ws, L.off_all_keys) : nullptr, static_cast<uint32_t>(p.S)};
       hipLaunchKernelGGL(k_select_tau, dim3(1), dim3(kTauBS), 0, c.stream, ta);
       if (lex) {
         TauIdxArgs ti{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S), static_cast<uint32_t>(p.t), st,

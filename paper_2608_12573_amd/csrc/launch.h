@@ -33,6 +33,14 @@ constexpr int kSampPerBlock = 4 * kSampBS;    // draws per sample block
 // workgroup selects tau from, is four times smaller.
 constexpr int kSampWideBS = 1024;
 constexpr uint32_t kWaveTopMax = 32;          // largest t of the wave-level top-t
+// Capped sample lists (key rule, t > kWaveTopMax): when the draws of one
+// 1024-draw block that lie in the sample's top t are few (mean mu = 1024 t /
+// S), each block keeps only its top c (c = 16 or 32, at least mu + 8
+// sqrt(mu) + 2) and its c-th largest key, and the blocks store every key.
+// The t-th largest of the union of the lists is the sample's t-th largest
+// whenever no block that dropped keys has its c-th key at or above it;
+// otherwise tau is selected again from all S keys.
+constexpr uint32_t kCapListSmall = 16;
 constexpr int kTauBS = 1024;
 constexpr int kFiltBS = 256;                  // threads of a filter block
 // 16-byte loads in flight per lane of a filter step: 4 for inputs of at
@@ -86,6 +94,8 @@ constexpr int kBktSortBlocks = 512;           // bucket-sort grid (loops over th
 struct FlatLayout {
   uint32_t G_s = 0, tcap = 0, union_n = 0;    // sampling
   uint32_t samp_bs = 0;                       // threads of a sample block (four draws each)
+  uint32_t cap_list = 0;                      // capped sample lists: their length, else 0
+  size_t off_cut = 0, off_all_keys = 0;       // capped lists: each block's cut key, every sample key
   uint32_t G_f = 0;                           // filter blocks
   int filt_u = 0;                             // 16-byte loads per lane and filter step
   uint32_t seg_cap = 0;                       // entries per candidate segment (= M)

@@ -43,9 +43,12 @@ struct SampleUnionShared {
 
 // Writes the workgroup's top-min(t, nb) draws to dst (nb: draws it holds,
 // valid bit q of `valid` for kv[q]).  Every thread of the workgroup calls it.
+// With t <= kWaveTopMax, *cut (when not null) receives the t-th largest
+// draw if the workgroup dropped any (nb > t), else 0.
 template <int BS, int KEYBITS>
 __device__ __forceinline__ void sample_block_top(uint32_t (&kv)[4], uint32_t valid, uint32_t nb, uint32_t t,
-                                                 uint32_t* dst, SampleUnionShared<BS>& sh) {
+                                                 uint32_t* dst, SampleUnionShared<BS>& sh,
+                                                 uint32_t* cut = nullptr) {
   constexpr int NW = BS / kWave;
   static_assert(NW * kWaveTopMax % kWave == 0, "union of the wave lists");
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
@@ -71,6 +74,7 @@ __device__ __forceinline__ void sample_block_top(uint32_t (&kv)[4], uint32_t val
         if (li < NW) { v2[e] = sh.lists[li][c]; valid2 |= 1u << e; }
       }
       wave_top_t<E2>(v2, valid2, tl, dst, last);
+      if (cut && lane == 0) *cut = nb > tl ? last : 0u;
     }
     return;
   }
