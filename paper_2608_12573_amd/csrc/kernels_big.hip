@@ -69,9 +69,8 @@ struct BigArgs {
   uint64_t* staging;   // P
   uint64_t* runs;      // P
   const uint32_t* fhist;  // kLogBins: the filter's histogram of log_bin(key - tau)
-  uint32_t* boff;      // kLogBins: first slot of each bucket (descending order)
   uint32_t* bcur;      // kLogBins * kBktPad: entries placed in bucket b at b * kBktPad
-  uint32_t* blist;     // kLogBins: the non-empty buckets >= b*, descending
+  uint4* blist;        // kLogBins: the non-empty buckets >= b*, descending: {bucket, first slot, size, 0}
   uint32_t P;          // padded length: k rounded up to kBigSortTile
   void* out_vals;
   int64_t* out_idx;
@@ -215,22 +214,28 @@ template <int DT>
 __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
   __shared__ uint32_t hist[kLogBins];  // counts of the sweep, then its range bases
   __shared__ uint32_t boff[kLogBins];  // first slot of each bucket (descending bucket order)
-  __shared__ uint32_t segn[kSegs];
+  __shared__ uint32_t segn[kSegs], s_cnt[kSegs];
   __shared__ SelectScratch fs;
-  __shared__ uint32_t s_total;
   BigState* s = a.bs;
   const uint32_t tid = threadIdx.x;
   const bool lead = blockIdx.x == 0;
+  // thread t owns buckets [kLogBins - 4(t+1), kLogBins - 4t)
+  constexpr uint32_t kOwners = kLogBins / 4;
+  static_assert(kLogBins % 4 == 0 && kOwners <= kScatBS, "bucket ownership");
+  const bool owner = tid < kOwners;
+  const uint32_t bbase = owner ? kLogBins - 4 * (tid + 1) : 0u;
+  // the segment counters and the histogram in one round trip
+  uint4 hv{0u, 0u, 0u, 0u};
+  if (!a.direct) {
+    if (owner) hv = *reinterpret_cast<const uint4*>(a.fhist + bbase);
+    if (tid < kSegs) s_cnt[tid] = a.seg_cnt[tid * kSegStride];
+    if (tid == 0) fs.found[0] = 0;
+  }
+  __syncthreads();
   uint32_t total = 0, status = PROFK_STATUS_DIRECT;
   if (!a.direct) {
-    if (tid == 0) {
-      uint32_t t = 0;
-      for (int x = 0; x < kSegs; ++x) t += a.seg_cnt[x * kSegStride];
-      s_total = t;
-      fs.found[0] = 0;
-    }
-    __syncthreads();
-    total = s_total;
+#pragma unroll
+    for (int x = 0; x < kSegs; ++x) total += s_cnt[x];
     status = total < a.k_req ? PROFK_STATUS_UNDERFLOW
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
   }
@@ -238,17 +243,30 @@ __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
     if (lead) big_begin<DT>(a, status, total, fs.wsum);
     return;
   }
+  if (tid < kSegs) segn[tid] = min(s_cnt[tid], a.seg_cap);
+  __syncthreads();
+  const uint32_t n = total;
+  const SegPos pos{segn, a.seg_cap};
+  constexpr uint32_t per = kScatBS * kScatU;
+  uint32_t key[kScatU], idx[kScatU];
+  auto load_sweep = [&](uint32_t base) {
+#pragma unroll
+    for (int u = 0; u < kScatU; ++u) {
+      const uint32_t i = base + u * kScatBS + tid;
+      key[u] = 0;
+      idx[u] = 0;
+      if (i < n) {
+        const size_t p = pos(i);
+        key[u] = a.seg_key[p];
+        idx[u] = a.seg_idx[p];
+      }
+    }
+  };
+  // the first sweep's candidates load while the plan is computed
+  const uint32_t base0 = blockIdx.x * per;
+  if (base0 < n) load_sweep(base0);
   const uint32_t kk = min(a.k, total);
-  // thread t owns buckets [kLogBins - 4(t+1), kLogBins - 4t)
-  constexpr uint32_t kOwners = kLogBins / 4;
-  static_assert(kLogBins % 4 == 0 && kOwners <= kScatBS, "bucket ownership");
-  const bool owner = tid < kOwners;
-  const uint32_t bbase = owner ? kLogBins - 4 * (tid + 1) : 0u;
-  uint32_t h[4] = {0u, 0u, 0u, 0u};
-  if (owner) {
-    const uint4 v = *reinterpret_cast<const uint4*>(a.fhist + bbase);
-    h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
-  }
+  const uint32_t h[4] = {hv.x, hv.y, hv.z, hv.w};
   const uint32_t above_me = block_excl_sum<kScatBS>(h[0] + h[1] + h[2] + h[3], fs.wsum, nullptr);
   if (owner) {
     uint32_t run = above_me;
@@ -277,15 +295,14 @@ __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
   }
   const uint32_t tau = a.st->tau_key;
   if (lead) {
-    // the non-empty buckets >= b*, in descending bucket order
+    // the non-empty buckets >= b*, in descending bucket order, with their
+    // first slot and size (every candidate of such a bucket is placed)
     uint32_t nlist = 0;
     uint32_t lpos = block_excl_sum<kScatBS>(nonempty, fs.wsum, &nlist);
     if (owner) {
 #pragma unroll
-      for (int j = 3; j >= 0; --j) {
-        a.boff[bbase + j] = boff[bbase + j];
-        if (bbase + j >= bstar && h[j]) a.blist[lpos++] = bbase + j;
-      }
+      for (int j = 3; j >= 0; --j)
+        if (bbase + j >= bstar && h[j]) a.blist[lpos++] = uint4{bbase + j, boff[bbase + j], h[j], 0u};
     }
     if (tid == 0) {
       s->mode = kModeBucket;
@@ -310,25 +327,11 @@ __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
       a.info->n_valid = kk;
     }
   }
-  const uint32_t n = total;
-  load_segn(a, segn);
-  const SegPos pos{segn, a.seg_cap};
-  constexpr uint32_t per = kScatBS * kScatU;
-  for (uint32_t base = blockIdx.x * per; base < n; base += gridDim.x * per) {
+  for (uint32_t base = base0; base < n; base += gridDim.x * per) {
+    if (base != base0) load_sweep(base);
     for (uint32_t b = tid; b < kLogBins; b += kScatBS) hist[b] = 0;
     __syncthreads();
-    uint32_t key[kScatU], idx[kScatU], bin[kScatU], rank[kScatU];
-#pragma unroll
-    for (int u = 0; u < kScatU; ++u) {
-      const uint32_t i = base + u * kScatBS + tid;
-      key[u] = 0;
-      idx[u] = 0;
-      if (i < n) {
-        const size_t p = pos(i);
-        key[u] = a.seg_key[p];
-        idx[u] = a.seg_idx[p];
-      }
-    }
+    uint32_t bin[kScatU], rank[kScatU];
 #pragma unroll
     for (int u = 0; u < kScatU; ++u) {
       const uint32_t i = base + u * kScatBS + tid;
@@ -383,11 +386,15 @@ __global__ __launch_bounds__(kSortBS) void k_bkt_sort(BigArgs a) {
   __shared__ uint32_t cnt[kSubBins], off[kSubBins];
   __shared__ SelectScratch scr;
   const BigState* s = a.bs;
+  // this block's first list entry loads with the state: it is read before
+  // the list length is known (the list has kLogBins entries, so the read is
+  // in bounds) and used only when it is in the list
+  const uint4 e0 = blockIdx.x < kLogBins ? a.blist[blockIdx.x] : uint4{0u, 0u, 0u, 0u};
   if (s->mode != kModeBucket) return;
   const uint32_t kk = s->kk, nlist = s->nlist, tau = s->tau, t = threadIdx.x;
   for (uint32_t l = blockIdx.x; l < nlist; l += gridDim.x) {
-    const uint32_t b = a.blist[l];
-    const uint32_t m = a.bcur[b * kBktPad], start = a.boff[b];
+    const uint4 e = l == blockIdx.x ? e0 : a.blist[l];
+    const uint32_t b = e.x, start = e.y, m = e.z;
     if (start >= kk) continue;
     cnt[t] = 0;
     __syncthreads();
@@ -723,7 +730,7 @@ static hipError_t launch_big_t(const BigCall& c) {
   const uint32_t P = cdiv_u(c.k, kBigSortTile) * kBigSortTile;
   BigArgs a{c.values, c.n, c.k, c.k_req, c.M, c.direct, c.seg_cnt, c.seg_key, c.seg_idx, c.blk_max,
             c.seg_cap, c.G_f, c.st, reinterpret_cast<BigState*>(c.big_state), c.ghist, c.staging, c.runs,
-            c.fhist, c.boff, c.bcur, c.blist, P, c.out_vals, c.out_idx, c.info};
+            c.fhist, c.bcur, reinterpret_cast<uint4*>(c.blist), P, c.out_vals, c.out_idx, c.info};
   hipLaunchKernelGGL(k_bkt_scatter<DT>, dim3(c.G_big), dim3(kScatBS), 0, c.stream, a);
   hipLaunchKernelGGL(k_bkt_sort<DT>, dim3(kBktSortBlocks), dim3(kSortBS), 0, c.stream, a);
   const uint32_t key_passes = cdiv_u(KB, kBigDigit);

@@ -1048,9 +1048,8 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
     L.off_ghist = take(static_cast<size_t>(kBigBins) * 4);
     L.off_staging = take((P + kBktCap) * 8);
     L.off_runs = take(P * 8);
-    L.off_boff = take(static_cast<size_t>(kLogBins) * 4);
     L.off_bcur = take(static_cast<size_t>(kLogBins) * kBktPad * 4);
-    L.off_blist = take(static_cast<size_t>(kLogBins) * 4);
+    L.off_blist = take(static_cast<size_t>(kLogBins) * 16);
   } else {
     // the merges read keys as aligned 16-byte vectors: 4 words of slack
     const size_t NG = (L.G_fb + kFbGroup - 1) / kFbGroup;
@@ -1081,7 +1080,7 @@ static hipError_t launch_refine_t(const FlatCall& c, bool direct, uint32_t G_f) 
                direct ? 1 : 0, seg_cnt, at<uint32_t>(c.ws, L.off_seg_key), at<uint32_t>(c.ws, L.off_seg_idx),
                at<uint32_t>(c.ws, L.off_blk_max), L.seg_cap, G_f, st, c.ws + L.off_big_state,
                at<uint32_t>(c.ws, L.off_ghist), at<uint64_t>(c.ws, L.off_staging), at<uint64_t>(c.ws, L.off_runs),
-               fhist, at<uint32_t>(c.ws, L.off_boff), at<uint32_t>(c.ws, L.off_bcur),
+               fhist, at<uint32_t>(c.ws, L.off_bcur),
                at<uint32_t>(c.ws, L.off_blist),
                L.G_big, c.out_vals, c.out_idx, c.info, c.stream};
     return launch_big(bc);

@@ -108,8 +108,8 @@ struct FlatLayout {
   bool big = false;                           // k > kFinMaxK: multi-block refinement
   uint32_t G_big = 0;
   size_t off_big_state = 0, off_ghist = 0, off_staging = 0, off_runs = 0;
-  size_t off_boff = 0, off_bcur = 0;          // bucket offsets and fill counts
-  size_t off_blist = 0;                       // non-empty buckets at or above b*
+  size_t off_bcur = 0;                        // bucket fill counts
+  size_t off_blist = 0;                       // non-empty buckets at or above b*: 16 bytes each
   size_t bytes = 0;
 };
 
@@ -161,7 +161,7 @@ struct BigCall {
   uint32_t* ghist;
   uint64_t *staging, *runs;
   const uint32_t* fhist;
-  uint32_t *boff, *bcur, *blist;
+  uint32_t *bcur, *blist;
   uint32_t G_big;
   void* out_vals;
   int64_t* out_idx;
