@@ -15,10 +15,12 @@
 // Every other call (a fallback, DIRECT, or a bucket larger than kBktCap)
 // takes the radix path, whose kernels return at once after a bucket call
 // (its source is the candidate segments, or the whole input on fallback):
-//   k_big_pass     one radix digit per launch: block histograms are merged
+//   radix passes   one radix digit per launch: block histograms are merged
 //                  into a global histogram and the last block (ticket) picks
 //                  the digit holding rank k.  Key digits first, then, if the
-//                  tie class at the k-th key is split, digits of ~index.
+//                  tie class at the k-th key is split, digits of ~index.  The
+//                  first two key digits are taken by the k_bkt_scatter and
+//                  k_bkt_sort launches, the others by k_big_pass.
 //   k_big_collect  every item of the top k, as a composite key, into a
 //                  staging array (one atomic per block).
 //   k_big_tile     sorts tiles of 16384 composites in LDS.
@@ -47,12 +49,11 @@ struct BigState {
   uint32_t iprefix, ikrem;
   int32_t ihi;
   uint32_t istar;
-  uint32_t ticket;
   uint32_t out_count;
   uint32_t mode;       // kModeRadix or kModeBucket
   uint32_t bstar;      // bucket path: the bucket holding rank kk
   uint32_t nlist;      // bucket path: entries of the bucket list
-  uint32_t pad[42];
+  uint32_t pad[43];
 };
 constexpr uint32_t kModeRadix = 0, kModeBucket = 1;
 static_assert(sizeof(BigState) <= 256, "state size");
@@ -63,7 +64,7 @@ struct BigArgs {
   int direct;
   const uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
   uint32_t seg_cap, G_f;
-  const CallState* st;
+  CallState* st;
   BigState* bs;
   uint32_t* ghist;     // kBigBins
   uint64_t* staging;   // P
@@ -95,10 +96,10 @@ struct SegPos {
 // Offsets are compared with the remaining count and a block stops before
 // its next sweep could pass n, so n may be as large as 2^32 - 1.
 template <int DT, int BS, class F>
-__device__ __forceinline__ void big_visit(const BigArgs& a, const BigState& s, const uint32_t* segn, F f) {
-  const uint32_t n = s.n_src;
+__device__ __forceinline__ void big_visit(const BigArgs& a, uint32_t n, uint32_t from_input, const uint32_t* segn,
+                                          F f) {
   const uint32_t stride = gridDim.x * BS * 8;
-  if (s.from_input) {
+  if (from_input) {
     for (uint32_t base = blockIdx.x * BS * 8; base < n; base += stride) {
       const uint32_t rem = n - base;
       uint32_t kv[8];
@@ -143,54 +144,189 @@ __device__ __forceinline__ void load_segn(const BigArgs& a, uint32_t* segn) {
   __syncthreads();
 }
 
-// ---------------------------------------------------------------- begin ---
-// The radix path's state, from the call's status (run by block 0 of
-// k_bkt_scatter, 1024 threads, when the bucket path does not apply).
-template <int DT>
-__device__ __forceinline__ void big_begin(const BigArgs& a, uint32_t status, uint32_t total, uint32_t* wsum) {
+// ------------------------------------------------------------ radix path ---
+// The radix path's state: what is selected from where (the header), and the
+// digit state of the key stage and of the index stage (digits of ~index
+// among the items whose key is kstar, when that tie class is split).
+struct RadixHead {
+  uint32_t status, total, tau, from_input, n_src, kk;
+};
+struct RadixVals {
+  uint32_t prefix, krem, above, equal;
+  int32_t hi;
+  uint32_t kstar, cut, iprefix, ikrem;
+  int32_t ihi;
+  uint32_t istar;
+};
+
+__device__ __forceinline__ RadixHead radix_load_head(const BigState* s) {
+  return RadixHead{s->status, s->total, s->tau, s->from_input, s->n_src, s->kk};
+}
+__device__ __forceinline__ RadixVals radix_load(const BigState* s) {
+  return RadixVals{s->prefix, s->krem, s->above, s->equal, s->hi, s->kstar,
+                   s->cut, s->iprefix, s->ikrem, s->ihi, s->istar};
+}
+__device__ __forceinline__ void radix_store_head(BigState* s, const RadixHead& h) {
+  s->mode = kModeRadix;
+  s->status = h.status;
+  s->total = h.total;
+  s->tau = h.tau;
+  s->from_input = h.from_input;
+  s->n_src = h.n_src;
+  s->kk = h.kk;
+  s->out_count = 0;
+}
+__device__ __forceinline__ void radix_store(BigState* s, const RadixVals& v) {
+  s->prefix = v.prefix;
+  s->krem = v.krem;
+  s->above = v.above;
+  s->equal = v.equal;
+  s->hi = v.hi;
+  s->kstar = v.kstar;
+  s->cut = v.cut;
+  s->iprefix = v.iprefix;
+  s->ikrem = v.ikrem;
+  s->ihi = v.ihi;
+  s->istar = v.istar;
+}
+
+// The starting state from the call's status.  Every thread of a block of
+// BS calls it, and every block derives the same values.
+template <int DT, int BS>
+__device__ __forceinline__ void radix_init(const BigArgs& a, uint32_t status, uint32_t total, uint32_t* wsum,
+                                           RadixHead& h, RadixVals& v) {
   constexpr int KB = Elem<DT>::KEYBITS;
-  const uint32_t tid = threadIdx.x;
-  BigState* s = a.bs;
-  for (uint32_t i = tid; i < kBigBins; i += 1024) a.ghist[i] = 0;
   const uint32_t key_max = KB == 32 ? 0xFFFFFFFFu : 0xFFFFu;
+  const bool filtered = status == PROFK_STATUS_FILTERED;
   uint32_t lo = 0, hi = key_max;
-  if (status == PROFK_STATUS_FILTERED) {
+  if (filtered) {
     lo = a.st->tau_key;
     uint32_t bm = 0;
-    for (uint32_t i = tid; i < a.G_f; i += 1024) bm = max(bm, a.blk_max[i]);
-    hi = max(lo, block_max<1024>(bm, wsum));
+    for (uint32_t i = threadIdx.x; i < a.G_f; i += BS) bm = max(bm, a.blk_max[i]);
+    hi = max(lo, block_max<BS>(bm, wsum));
   }
-  if (tid == 0) {
-    const bool filtered = status == PROFK_STATUS_FILTERED;
-    s->mode = kModeRadix;
-    s->status = status;
-    s->total = total;
-    s->tau = a.direct ? 0u : a.st->tau_key;
-    s->from_input = filtered ? 0u : 1u;
-    s->n_src = filtered ? total : a.n;
-    s->kk = filtered ? min(a.k, total) : a.k;
-    s->prefix = lo;
-    s->krem = s->kk;
-    s->above = 0;
-    s->equal = 0;
-    s->hi = KB - shared_prefix_bits(lo, hi, KB);
-    s->kstar = lo;
-    s->cut = 0;
-    s->iprefix = 0;
-    s->ikrem = 0;
-    s->ihi = 0;
-    s->istar = 0xFFFFFFFFu;
-    s->ticket = 0;
-    s->out_count = 0;
-    if (s->hi == 0) {
-      // every candidate carries the same key: only the index cut is left
-      s->equal = s->n_src;
-      if (s->kk < s->n_src) {
-        s->cut = 1;
-        s->ikrem = s->kk;
-        s->ihi = 32;
-      }
+  h.status = status;
+  h.total = total;
+  h.tau = a.direct ? 0u : a.st->tau_key;
+  h.from_input = filtered ? 0u : 1u;
+  h.n_src = filtered ? total : a.n;
+  h.kk = filtered ? min(a.k, total) : a.k;
+  v.prefix = lo;
+  v.krem = h.kk;
+  v.above = 0;
+  v.equal = 0;
+  v.hi = KB - shared_prefix_bits(lo, hi, KB);
+  v.kstar = lo;
+  v.cut = 0;
+  v.iprefix = 0;
+  v.ikrem = 0;
+  v.ihi = 0;
+  v.istar = 0xFFFFFFFFu;
+  if (v.hi == 0) {
+    // every candidate carries the same key: only the index cut is left
+    v.equal = h.n_src;
+    if (h.kk < h.n_src) {
+      v.cut = 1;
+      v.ikrem = h.kk;
+      v.ihi = 32;
     }
+  }
+}
+
+struct PassShared {
+  uint32_t hist[1 << kBigDigit];
+  uint32_t segn[kSegs];
+  uint32_t wsum[20];
+  uint32_t last, found[3];
+};
+
+// Whether a digit pass of STAGE has work in state v.
+template <int STAGE>
+__device__ __forceinline__ bool radix_pending(const RadixVals& v) {
+  return STAGE == 0 ? v.hi > 0 : (v.cut && v.ihi > 0);
+}
+
+// One radix digit pass by a grid of BS-thread blocks from the state (h, v)
+// that every block holds (STAGE 0: a digit of the key; STAGE 1: a digit of
+// ~index among the items whose key is kstar).  Block histograms are merged
+// into ghist (zero on entry); the last block to finish (ticket) picks the
+// digit holding the remaining rank, clears ghist and the ticket, and writes
+// the state after the pass: the digit state, and the header too when
+// `head` (nothing had written the state before this pass).
+template <int DT, int STAGE, int BS>
+__device__ void radix_pass(const BigArgs& a, const RadixHead& h, RadixVals v, bool head, PassShared& sh) {
+  const int hi = STAGE == 0 ? v.hi : v.ihi;
+  const uint32_t tid = threadIdx.x;
+  const int bits = hi < kBigDigit ? hi : kBigDigit;
+  const int shift = hi - bits;
+  const uint32_t nb = 1u << bits;
+  const uint32_t hmask = hi >= 32 ? 0u : ~((1u << hi) - 1u);
+  const uint32_t pre = (STAGE == 0 ? v.prefix : v.iprefix) & hmask;
+  const uint32_t kstar = v.kstar;
+  for (uint32_t b = tid; b < nb; b += BS) sh.hist[b] = 0;
+  if (!h.from_input) load_segn(a, sh.segn); else __syncthreads();
+  big_visit<DT, BS>(a, h.n_src, h.from_input, sh.segn, [&](uint32_t key, uint32_t idx) {
+    uint32_t x = key;
+    if (STAGE == 1) {
+      if (key != kstar) return;
+      x = ~idx;
+    }
+    if ((x & hmask) == pre) atomicAdd(&sh.hist[(x >> shift) & (nb - 1)], 1u);
+  });
+  __syncthreads();
+  for (uint32_t b = tid; b < nb; b += BS)
+    if (sh.hist[b]) atomicAdd(&a.ghist[b], sh.hist[b]);
+  wait_memory();  // the histogram is handed over through atomics
+  __syncthreads();
+  if (tid == 0) sh.last = (atomicAdd(&a.st->big_ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
+  __syncthreads();
+  if (!sh.last) return;
+  acquire_agent();
+  // The last block finds the digit holding the remaining rank.
+  const uint32_t krem = STAGE == 0 ? v.krem : v.ikrem;
+  const uint32_t per = (nb + BS - 1) / BS;  // bins per thread, descending
+  uint32_t loc = 0;
+  for (uint32_t r = tid * per; r < (tid + 1) * per && r < nb; ++r) loc += a.ghist[nb - 1 - r];
+  uint32_t run = block_excl_sum<BS>(loc, sh.wsum, nullptr);
+  for (uint32_t r = tid * per; r < (tid + 1) * per && r < nb; ++r) {
+    const uint32_t c = a.ghist[nb - 1 - r];
+    if (run < krem && krem <= run + c) {
+      sh.found[0] = nb - 1 - r;
+      sh.found[1] = run;
+      sh.found[2] = c;
+    }
+    run += c;
+  }
+  __syncthreads();
+  for (uint32_t b = tid; b < nb; b += BS) a.ghist[b] = 0;
+  if (tid == 0) {
+    const uint32_t d = sh.found[0], ab = sh.found[1], eq = sh.found[2];
+    const uint32_t np = (pre & hmask) | (d << shift);
+    if (STAGE == 0) {
+      v.prefix = np;
+      v.krem = krem - ab;
+      v.above += ab;
+      v.equal = eq;
+      v.hi = shift;
+      if (shift == 0) {
+        v.kstar = np;
+        const bool cut = v.krem < eq;
+        v.cut = cut ? 1u : 0u;
+        if (cut) {
+          v.ikrem = v.krem;
+          v.ihi = 32;
+          v.iprefix = 0;
+        }
+      }
+    } else {
+      v.iprefix = np;
+      v.ikrem = krem - ab;
+      v.ihi = shift;
+      if (shift == 0) v.istar = ~np;
+    }
+    if (head) radix_store_head(a.bs, h);
+    radix_store(a.bs, v);
+    a.st->big_ticket = 0;
   }
 }
 
@@ -205,10 +341,27 @@ __device__ __forceinline__ void big_begin(const BigArgs& a, uint32_t status, uin
 // holding rank kk, and whether every bucket >= b* fits one sort block.  All
 // blocks read the same counts and so derive the same plan; none waits for
 // another.  Block 0 also records it for the kernels after this one: the
-// bucket path's state, offsets, bucket list, padding and report, or, when
-// the bucket path does not apply, the radix path's state.  The fill
-// counters (bcur) are zeroed at the start of the call.
+// bucket path's state, bucket list, padding and report.  When the bucket
+// path does not apply, the blocks run the radix path's first key digit pass
+// instead (the sort launch runs the second).  The fill counters (bcur), the
+// digit histogram and its ticket are zeroed at the start of the call.
 constexpr int kScatBS = 1024, kScatU = 4;
+
+// The radix path from the scatter's blocks: its first key digit pass runs
+// there, or, when no key digit is left, block 0 records the starting state.
+template <int DT>
+__device__ __forceinline__ void radix_start(const BigArgs& a, uint32_t status, uint32_t total, uint32_t* wsum,
+                                            PassShared& ps) {
+  RadixHead h;
+  RadixVals v;
+  radix_init<DT, kScatBS>(a, status, total, wsum, h, v);
+  if (radix_pending<0>(v)) {
+    radix_pass<DT, 0, kScatBS>(a, h, v, true, ps);
+  } else if (blockIdx.x == 0 && threadIdx.x == 0) {
+    radix_store_head(a.bs, h);
+    radix_store(a.bs, v);
+  }
+}
 
 template <int DT>
 __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
@@ -216,6 +369,7 @@ __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
   __shared__ uint32_t boff[kLogBins];  // first slot of each bucket (descending bucket order)
   __shared__ uint32_t segn[kSegs], s_cnt[kSegs];
   __shared__ SelectScratch fs;
+  __shared__ PassShared ps;  // the radix path's first key digit pass
   BigState* s = a.bs;
   const uint32_t tid = threadIdx.x;
   const bool lead = blockIdx.x == 0;
@@ -240,7 +394,7 @@ __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
                              : (total > a.M ? PROFK_STATUS_OVERFLOW : PROFK_STATUS_FILTERED);
   }
   if (status != PROFK_STATUS_FILTERED) {  // uniform over the grid
-    if (lead) big_begin<DT>(a, status, total, fs.wsum);
+    radix_start<DT>(a, status, total, fs.wsum, ps);
     return;
   }
   if (tid < kSegs) segn[tid] = min(s_cnt[tid], a.seg_cap);
@@ -290,7 +444,7 @@ __global__ __launch_bounds__(kScatBS) void k_bkt_scatter(BigArgs a) {
   }
   big = block_max<kScatBS>(big, fs.wsum);
   if (big > kBktCap) {  // uniform over the grid: the radix path
-    if (lead) big_begin<DT>(a, status, total, fs.wsum);
+    radix_start<DT>(a, status, total, fs.wsum, ps);
     return;
   }
   const uint32_t tau = a.st->tau_key;
@@ -385,12 +539,17 @@ __global__ __launch_bounds__(kSortBS) void k_bkt_sort(BigArgs a) {
   __shared__ uint64_t A[kBktCap], Bv[kBktCap];
   __shared__ uint32_t cnt[kSubBins], off[kSubBins];
   __shared__ SelectScratch scr;
+  __shared__ PassShared ps;  // the radix path's second key digit pass
   const BigState* s = a.bs;
   // this block's first list entry loads with the state: it is read before
   // the list length is known (the list has kLogBins entries, so the read is
   // in bounds) and used only when it is in the list
   const uint4 e0 = blockIdx.x < kLogBins ? a.blist[blockIdx.x] : uint4{0u, 0u, 0u, 0u};
-  if (s->mode != kModeBucket) return;
+  if (s->mode != kModeBucket) {
+    const RadixVals v = radix_load(s);
+    if (radix_pending<0>(v)) radix_pass<DT, 0, kSortBS>(a, radix_load_head(s), v, false, ps);
+    return;
+  }
   const uint32_t kk = s->kk, nlist = s->nlist, tau = s->tau, t = threadIdx.x;
   for (uint32_t l = blockIdx.x; l < nlist; l += gridDim.x) {
     const uint4 e = l == blockIdx.x ? e0 : a.blist[l];
@@ -454,89 +613,16 @@ __global__ __launch_bounds__(kSortBS) void k_bkt_sort(BigArgs a) {
 }
 
 // ------------------------------------------------------------ one digit ---
-// STAGE 0: a digit of the key; STAGE 1: a digit of ~index among the items
-// whose key is kstar.
+// One radix digit pass per launch (radix_pass), after the two that the
+// scatter and the sort launches run.
 template <int DT, int STAGE>
 __global__ __launch_bounds__(kBigBS) void k_big_pass(BigArgs a) {
-  constexpr int NB = 1 << kBigDigit;
-  __shared__ uint32_t hist[NB];
-  __shared__ uint32_t segn[kSegs];
-  __shared__ uint32_t wsum[20];
-  __shared__ uint32_t s_last, s_found[3];
-  BigState* s = a.bs;
+  __shared__ PassShared sh;
+  const BigState* s = a.bs;
   if (s->mode == kModeBucket) return;
-  const int hi = STAGE == 0 ? s->hi : s->ihi;
-  if (hi <= 0 || (STAGE == 1 && !s->cut)) return;  // uniform: nothing left to resolve
-  const uint32_t tid = threadIdx.x;
-  const int bits = hi < kBigDigit ? hi : kBigDigit;
-  const int shift = hi - bits;
-  const uint32_t nb = 1u << bits;
-  const uint32_t hmask = hi >= 32 ? 0u : ~((1u << hi) - 1u);
-  const uint32_t pre = (STAGE == 0 ? s->prefix : s->iprefix) & hmask;
-  const uint32_t kstar = s->kstar;
-  for (uint32_t b = tid; b < nb; b += kBigBS) hist[b] = 0;
-  if (!s->from_input) load_segn(a, segn); else __syncthreads();
-  big_visit<DT, kBigBS>(a, *s, segn, [&](uint32_t key, uint32_t idx) {
-    uint32_t v = key;
-    if (STAGE == 1) {
-      if (key != kstar) return;
-      v = ~idx;
-    }
-    if ((v & hmask) == pre) atomicAdd(&hist[(v >> shift) & (nb - 1)], 1u);
-  });
-  __syncthreads();
-  for (uint32_t b = tid; b < nb; b += kBigBS)
-    if (hist[b]) atomicAdd(&a.ghist[b], hist[b]);
-  wait_memory();  // the histogram is handed over through atomics
-  __syncthreads();
-  if (tid == 0) s_last = (atomicAdd(&s->ticket, 1u) == gridDim.x - 1) ? 1u : 0u;
-  __syncthreads();
-  if (!s_last) return;
-  acquire_agent();
-  // The last block finds the digit holding the remaining rank.
-  const uint32_t krem = STAGE == 0 ? s->krem : s->ikrem;
-  const uint32_t per = (nb + kBigBS - 1) / kBigBS;  // bins per thread, descending
-  uint32_t loc = 0;
-  for (uint32_t r = tid * per; r < (tid + 1) * per && r < nb; ++r) loc += a.ghist[nb - 1 - r];
-  uint32_t run = block_excl_sum<kBigBS>(loc, wsum, nullptr);
-  for (uint32_t r = tid * per; r < (tid + 1) * per && r < nb; ++r) {
-    const uint32_t c = a.ghist[nb - 1 - r];
-    if (run < krem && krem <= run + c) {
-      s_found[0] = nb - 1 - r;
-      s_found[1] = run;
-      s_found[2] = c;
-    }
-    run += c;
-  }
-  __syncthreads();
-  for (uint32_t b = tid; b < nb; b += kBigBS) a.ghist[b] = 0;
-  if (tid == 0) {
-    const uint32_t d = s_found[0], ab = s_found[1], eq = s_found[2];
-    const uint32_t np = (pre & hmask) | (d << shift);
-    if (STAGE == 0) {
-      s->prefix = np;
-      s->krem = krem - ab;
-      s->above += ab;
-      s->equal = eq;
-      s->hi = shift;
-      if (shift == 0) {
-        s->kstar = np;
-        const bool cut = s->krem < eq;
-        s->cut = cut ? 1u : 0u;
-        if (cut) {
-          s->ikrem = s->krem;
-          s->ihi = 32;
-          s->iprefix = 0;
-        }
-      }
-    } else {
-      s->iprefix = np;
-      s->ikrem = krem - ab;
-      s->ihi = shift;
-      if (shift == 0) s->istar = ~np;
-    }
-    s->ticket = 0;
-  }
+  const RadixVals v = radix_load(s);
+  if (!radix_pending<STAGE>(v)) return;  // uniform: nothing left to resolve
+  radix_pass<DT, STAGE, kBigBS>(a, radix_load_head(s), v, false, sh);
 }
 
 // -------------------------------------------------------------- collect ---
@@ -552,7 +638,7 @@ __global__ __launch_bounds__(kBigBS) void k_big_collect(BigArgs a) {
   if (tid == 0) s_cnt = 0;
   if (!s->from_input) load_segn(a, segn); else __syncthreads();
   BigState* sw = a.bs;
-  big_visit<DT, kBigBS>(a, *s, segn, [&](uint32_t key, uint32_t idx) {
+  big_visit<DT, kBigBS>(a, s->n_src, s->from_input, segn, [&](uint32_t key, uint32_t idx) {
     const bool take = key > kstar || (key == kstar && (!cut || idx <= istar));
     const uint64_t bal = __ballot(take);
     if (bal == 0) return;
@@ -733,7 +819,8 @@ static hipError_t launch_big_t(const BigCall& c) {
             c.fhist, c.bcur, reinterpret_cast<uint4*>(c.blist), P, c.out_vals, c.out_idx, c.info};
   hipLaunchKernelGGL(k_bkt_scatter<DT>, dim3(c.G_big), dim3(kScatBS), 0, c.stream, a);
   hipLaunchKernelGGL(k_bkt_sort<DT>, dim3(kBktSortBlocks), dim3(kSortBS), 0, c.stream, a);
-  const uint32_t key_passes = cdiv_u(KB, kBigDigit);
+  // key digit passes after the scatter's and the sort's (one each)
+  const uint32_t key_passes = cdiv_u(KB, kBigDigit) > 2 ? cdiv_u(KB, kBigDigit) - 2 : 0u;
   for (uint32_t p = 0; p < key_passes; ++p)
     hipLaunchKernelGGL((k_big_pass<DT, 0>), dim3(c.G_big), dim3(kBigBS), 0, c.stream, a);
   for (uint32_t p = 0; p < cdiv_u(32, kBigDigit); ++p)

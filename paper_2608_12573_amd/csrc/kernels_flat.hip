@@ -36,7 +36,8 @@ struct SampleArgs {
   CallState* st;
   uint32_t* seg_cnt;
   uint32_t* fhist;
-  uint32_t* bcur;  // null unless the call takes the large-k path
+  uint32_t* bcur;   // null unless the call takes the large-k path
+  uint32_t* ghist;  // null unless the call takes the large-k path
   // capped lists (t is then their length): each block's cut key, and every
   // draw's key at its draw number; null otherwise
   uint32_t* cut;
@@ -48,7 +49,7 @@ __global__ __launch_bounds__(BS) void k_sample(SampleArgs a) {
   constexpr uint32_t kPer = 4 * BS;  // four draws per thread
   __shared__ SampleUnionShared<BS> sh;
   const uint32_t b = blockIdx.x, tid = threadIdx.x;
-  if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist, a.bcur);
+  if (b == 0) reset_state(a.st, a.seg_cnt, a.fhist, a.bcur, a.ghist);
   const uint32_t j0 = b * kPer;
   const uint32_t nb = min(kPer, a.S - j0);
   uint32_t kv[4];
@@ -338,12 +339,13 @@ struct InitArgs {
   CallState* st;
   uint32_t* seg_cnt;
   uint32_t* fhist;
-  uint32_t* bcur;  // null unless the call takes the large-k path
+  uint32_t* bcur;   // null unless the call takes the large-k path
+  uint32_t* ghist;  // null unless the call takes the large-k path
   uint32_t tau_key;
 };
 
 __global__ void k_init_state(InitArgs a) {
-  reset_state(a.st, a.seg_cnt, a.fhist, a.bcur);
+  reset_state(a.st, a.seg_cnt, a.fhist, a.bcur, a.ghist);
   if (threadIdx.x == 0) a.st->tau_key = a.tau_key;
 }
 
@@ -1117,15 +1119,16 @@ static hipError_t launch_flat_t(const FlatCall& c) {
   const bool lex = p.lexicographic && !direct && !c.use_tau;  // a caller's tau: the key rule
   uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
   uint32_t* bcur = L.big ? at<uint32_t>(c.ws, L.off_bcur) : nullptr;
+  uint32_t* ghist = L.big ? at<uint32_t>(c.ws, L.off_ghist) : nullptr;
   const uint32_t* union_for_filter = nullptr;
   hipError_t e;
   if (direct || c.use_tau) {
     hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream,
-                       InitArgs{st, seg_cnt, fhist, bcur, c.use_tau ? c.tau_key : 0u});
+                       InitArgs{st, seg_cnt, fhist, bcur, ghist, c.use_tau ? c.tau_key : 0u});
   } else {
     uint32_t* uk = at<uint32_t>(c.ws, L.off_union);
     SampleArgs sa{c.values, c.n, c.seed, c.row, static_cast<uint32_t>(p.S),
-                  L.cap_list ? L.cap_list : static_cast<uint32_t>(p.t), L.tcap, uk, st, seg_cnt, fhist, bcur,
+                  L.cap_list ? L.cap_list : static_cast<uint32_t>(p.t), L.tcap, uk, st, seg_cnt, fhist, bcur, ghist,
                   L.cap_list ? at<uint32_t>(c.ws, L.off_cut) : nullptr,
                   L.cap_list ? at<uint32_t>(c.ws, L.off_all_keys) : nullptr};
     if (L.samp_bs == kSampWideBS) hipLaunchKernelGGL((k_sample<DT, kSampWideBS>), dim3(L.G_s), dim3(kSampWideBS), 0, c.stream, sa);
@@ -1193,7 +1196,8 @@ hipError_t launch_debug_filter(const FlatCall& c, uint32_t* buf_key, uint32_t* b
   (void)hipGetLastError();
   uint32_t* fhist = at<uint32_t>(c.ws, L.off_fhist);
   hipLaunchKernelGGL(k_init_state, dim3(1), dim3(64), 0, c.stream,
-                     InitArgs{st, seg_cnt, fhist, L.big ? at<uint32_t>(c.ws, L.off_bcur) : nullptr, c.tau_key});
+                     InitArgs{st, seg_cnt, fhist, L.big ? at<uint32_t>(c.ws, L.off_bcur) : nullptr,
+                              L.big ? at<uint32_t>(c.ws, L.off_ghist) : nullptr, c.tau_key});
   hipError_t e = launch_filter(c, st, nullptr, false);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_gather_buffer, dim3(1), dim3(1024), 0, c.stream, L.seg_cap, seg_cnt,

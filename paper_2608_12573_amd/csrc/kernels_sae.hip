@@ -88,7 +88,8 @@ struct SaeSampleArgs {
   CallState* st;
   uint32_t* seg_cnt;
   uint32_t* fhist;
-  uint32_t* bcur;  // null unless the call takes the large-k path
+  uint32_t* bcur;   // null unless the call takes the large-k path
+  uint32_t* ghist;  // null unless the call takes the large-k path
 };
 
 // Draw j is word j%4 of Philox block j/4 (row 0) over the N = B*d_dict
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
   __shared__ __align__(16) uint16_t s_x[NW][32 * kSaeLd];
   __shared__ __align__(16) uint16_t s_w[NW][32 * kSaeLd];
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-  if (blockIdx.x == 0) reset_state(a.st, a.seg_cnt, a.fhist, a.bcur);
+  if (blockIdx.x == 0) reset_state(a.st, a.seg_cnt, a.fhist, a.bcur, a.ghist);
   const uint32_t j = (blockIdx.x * NW + w) * 32 + (lane & 31);
   const bool in = j < a.S;
   uint32_t r = 0, c = 0;
@@ -877,7 +878,8 @@ hipError_t launch_sae_sample(const SaeCall& c) {
   const uint32_t S = static_cast<uint32_t>(c.plan->S);
   SaeSampleArgs sa{gemm_of(c), c.seed, S, skeys, reinterpret_cast<CallState*>(c.ws + L.off_state),
                    reinterpret_cast<uint32_t*>(c.ws + L.off_segcnt), reinterpret_cast<uint32_t*>(c.ws + L.off_fhist),
-                   L.big ? reinterpret_cast<uint32_t*>(c.ws + L.off_bcur) : nullptr};
+                   L.big ? reinterpret_cast<uint32_t*>(c.ws + L.off_bcur) : nullptr,
+                   L.big ? reinterpret_cast<uint32_t*>(c.ws + L.off_ghist) : nullptr};
   hipLaunchKernelGGL(k_sae_sample, dim3(cdiv_s(S, 32 * (kSampBS / kWave))), dim3(kSampBS), 0, c.stream, sa);
   return hipGetLastError();
 }

@@ -20,7 +20,8 @@ struct CallState {
   uint32_t tie_n;      // draws equal to tau, listed in the workspace
   uint32_t tie_ticket; // last-block-done counter of k_tau_index
   uint32_t grp_ticket[16];  // last-block-done counters of the fallback's chunk groups
-  uint32_t pad[41];
+  uint32_t big_ticket;  // last-block-done counter of the large-k radix digit passes
+  uint32_t pad[40];
 };
 static_assert(sizeof(CallState) == 256, "call state size");
 
@@ -156,7 +157,7 @@ struct BigCall {
   int direct;
   const uint32_t *seg_cnt, *seg_key, *seg_idx, *blk_max;
   uint32_t seg_cap, G_f;
-  const CallState* st;
+  CallState* st;
   void* big_state;
   uint32_t* ghist;
   uint64_t *staging, *runs;

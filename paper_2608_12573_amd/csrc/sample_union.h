@@ -12,20 +12,25 @@ namespace profk {
 
 // Clears the per-call counters; fhist (kLogBins words, or null) is the
 // refinement histogram the filter accumulates into.
-// (bcur: the large-k path's bucket fill counters, one per kBktPad words, or
-// null when the call does not take that path)
-__device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt, uint32_t* fhist, uint32_t* bcur) {
+// (bcur: the large-k path's bucket fill counters, one per kBktPad words, and
+// ghist its radix digit histogram, kBigBins words; both null when the call
+// does not take that path)
+__device__ __forceinline__ void reset_state(CallState* st, uint32_t* seg_cnt, uint32_t* fhist, uint32_t* bcur,
+                                            uint32_t* ghist) {
   if (threadIdx.x < kSegs) seg_cnt[threadIdx.x * kSegStride] = 0;
   if (fhist)
     for (uint32_t i = threadIdx.x; i < kLogBins; i += blockDim.x) fhist[i] = 0;
   if (bcur)
     for (uint32_t i = threadIdx.x; i < kLogBins; i += blockDim.x) bcur[i * kBktPad] = 0;
+  if (ghist)
+    for (uint32_t i = threadIdx.x; i < kBigBins; i += blockDim.x) ghist[i] = 0;
   if (threadIdx.x == 0) {
     st->ticket = 0;
     st->status = 0;
     st->tie_above = 0;
     st->tie_n = 0;
     st->tie_ticket = 0;
+    st->big_ticket = 0;
   }
   if (threadIdx.x < 16) st->grp_ticket[threadIdx.x] = 0;
 }
