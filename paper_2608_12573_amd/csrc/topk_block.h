@@ -84,24 +84,17 @@ struct TopkSmem {
 // candidate key lies in [lo_key, hi_key], so the leading bits they share
 // are skipped.  The collection first reserves slots for (key, candidate
 // number) and then loads all selected indices at once.
+//
+// block_topk_core is the selection itself over `src` (keys cached in
+// sm.cache when they fit); block_topk first copies keys and indices to LDS
+// when both fit.  The two are separate functions so that neither calls
+// itself: a recursive call could not be inlined, and its LDS arrays would
+// then be reached through generic pointers (flat loads and atomics) from a
+// stack frame.
 template <int BS, int DIGIT, class Src>
-__device__ __forceinline__ void block_topk(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
-                                           uint32_t hi_key, int keybits, const TopkSmem& sm) {
+__device__ __forceinline__ void block_topk_core(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
+                                                uint32_t hi_key, int keybits, const TopkSmem& sm) {
   const uint32_t tid = threadIdx.x;
-  if (sm.cache != nullptr && 2 * n <= sm.cache_cap) {
-    // keys and indices both fit: copy them to LDS once (index loads batched)
-    // and select there, so the passes on tied keys read no global memory
-    uint32_t* const pk = sm.cache;
-    uint32_t* const pi = sm.cache + n;
-    src.template visit<BS>(n, nullptr, [&](uint32_t i, uint32_t key, auto) { pk[i] = key; });
-    for_items<BS, 8>(n, [&](uint32_t i) { return src.idx_at(i); }, [&](uint32_t i, uint32_t v) { pi[i] = v; });
-    __syncthreads();
-    TopkSmem lds = sm;
-    lds.cache = nullptr;
-    lds.cache_cap = 0;
-    block_topk<BS, DIGIT>(LdsSrc<uint32_t>{pk, pi}, n, kk, lo_key, hi_key, keybits, lds);
-    return;
-  }
   const bool cached = sm.cache != nullptr && n <= sm.cache_cap;
   if (cached) {
     src.template visit<BS>(n, nullptr, [&](uint32_t i, uint32_t key, auto) { sm.cache[i] = key; });
@@ -146,6 +139,26 @@ __device__ __forceinline__ void block_topk(const Src& src, uint32_t n, uint32_t 
     sm.collect[p] = composite(static_cast<uint32_t>(e >> 32), src.idx_at(static_cast<uint32_t>(e)));
   }
   __syncthreads();
+}
+
+template <int BS, int DIGIT, class Src>
+__device__ __forceinline__ void block_topk(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
+                                           uint32_t hi_key, int keybits, const TopkSmem& sm) {
+  if (sm.cache != nullptr && 2 * n <= sm.cache_cap) {
+    // keys and indices both fit: copy them to LDS once (index loads batched)
+    // and select there, so the passes on tied keys read no global memory
+    uint32_t* const pk = sm.cache;
+    uint32_t* const pi = sm.cache + n;
+    src.template visit<BS>(n, nullptr, [&](uint32_t i, uint32_t key, auto) { pk[i] = key; });
+    for_items<BS, 8>(n, [&](uint32_t i) { return src.idx_at(i); }, [&](uint32_t i, uint32_t v) { pi[i] = v; });
+    __syncthreads();
+    TopkSmem lds = sm;
+    lds.cache = nullptr;
+    lds.cache_cap = 0;
+    block_topk_core<BS, DIGIT>(LdsSrc<uint32_t>{pk, pi}, n, kk, lo_key, hi_key, keybits, lds);
+    return;
+  }
+  block_topk_core<BS, DIGIT>(src, n, kk, lo_key, hi_key, keybits, sm);
 }
 
 // Exact top-kk of an item set too large for LDS, read in a few passes.
@@ -218,7 +231,7 @@ __device__ __forceinline__ void window_topk(const Src& src, uint32_t kk, int key
   TopkSmem lds = sm;
   lds.cache = nullptr;
   lds.cache_cap = 0;
-  block_topk<BS, DIGIT>(LdsSrc<uint32_t>{pk, pi}, n2, kk, prefix, mx, keybits, lds);
+  block_topk_core<BS, DIGIT>(LdsSrc<uint32_t>{pk, pi}, n2, kk, prefix, mx, keybits, lds);
 }
 
 // Sorts collect[0..kk) descending (E*BS >= max(kk, n_out), a power of two)
