@@ -111,7 +111,11 @@ __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
   uint32_t r = 0, c = 0;
   if (in) {
     const U64x4 p = philox4x64_10(j >> 2, 0, 0, 0, a.seed, 0);
-    const uint64_t flat = index_of_word(p.w[j & 3], static_cast<uint64_t>(a.g.B) * a.g.d_dict);
+    // word j % 4, chosen in registers (indexing p.w by a lane-varying value
+    // would place it in scratch memory)
+    const uint32_t q = j & 3;
+    const uint64_t word = q == 0 ? p.w[0] : q == 1 ? p.w[1] : q == 2 ? p.w[2] : p.w[3];
+    const uint64_t flat = index_of_word(word, static_cast<uint64_t>(a.g.B) * a.g.d_dict);
     r = static_cast<uint32_t>(flat / a.g.d_dict);
     c = static_cast<uint32_t>(flat % a.g.d_dict);
   }
