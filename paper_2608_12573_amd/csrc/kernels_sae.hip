@@ -131,8 +131,8 @@ __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
   }
   const uint32_t seg = lane & 7;
   f32x16 acc{};
-  for (uint32_t k0 = 0; k0 < a.g.d_model; k0 += kSaeBK) {
-    u32x4v vx[4], vw[4];
+  // chunk k0 of the wave's 32 rows of x and of W_enc, into registers
+  auto load_chunk = [&](uint32_t k0, u32x4v (&vx)[4], u32x4v (&vw)[4]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       vx[s] = pin[s] ? *reinterpret_cast<const u32x4v*>(a.g.x + static_cast<size_t>(pr[s]) * a.g.d_model + k0 + seg * 8)
@@ -140,6 +140,18 @@ __global__ __launch_bounds__(kSampBS) void k_sae_sample(SaeSampleArgs a) {
       vw[s] = pin[s] ? *reinterpret_cast<const u32x4v*>(a.g.w + static_cast<size_t>(pc[s]) * a.g.d_model + k0 + seg * 8)
                      : u32x4v{0u, 0u, 0u, 0u};
     }
+  };
+  // the next chunk's loads are in flight while this chunk's MFMAs run
+  u32x4v nx[4], nw[4];
+  load_chunk(0, nx, nw);
+  for (uint32_t k0 = 0; k0 < a.g.d_model; k0 += kSaeBK) {
+    u32x4v vx[4], vw[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      vx[s] = nx[s];
+      vw[s] = nw[s];
+    }
+    if (k0 + kSaeBK < a.g.d_model) load_chunk(k0 + kSaeBK, nx, nw);
     // (the wave's previous chunk was read by this wave's own earlier LDS
     // reads, which complete in order before these writes)
 #pragma unroll
