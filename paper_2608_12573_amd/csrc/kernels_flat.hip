@@ -358,7 +358,7 @@ constexpr uint32_t kFinCache = 28672;
 // segment's) or end up to 3 past its capacity (still within the workspace);
 // such entries are skipped by their index.
 constexpr uint32_t kPreThreads = kFinBS / kSegs;
-constexpr int kPreV = 2;
+constexpr int kPreV = 4;
 constexpr int kSweepV = 8;
 static_assert(kPreThreads * kSegs == kFinBS, "threads per segment");
 constexpr int kFinDigit = 12;
