@@ -125,32 +125,44 @@ def test_special_values_and_ties():
         _f32_case(x, k, 1, eps=1e-3, **SMALL)
 
 
-# Plans with t > 32: every sample block keeps its top t draws and one block
-# selects tau from the union of those lists (k_select_tau).  A constant
-# input makes every key equal (the select's shared-prefix trim takes all
-# bits), small integers leave thousands of ties in the union, S = 40000
-# leaves a partial last sample block.
+# Plans with t > 32: sample blocks keep lists of their largest draws and
+# one block selects tau from the union of those lists (k_select_tau).  Two
+# regimes, told apart by mu = 1024 t / S, the mean number of a 1024-draw
+# block's draws in the sample's top t: at k = 4096 (mu about 5) blocks of
+# 1024 draws keep capped lists of 32 and the select checks them against
+# their cut keys, falling back to all sample keys on ties; at k = 8192 (mu
+# about 10) blocks of 4096 draws keep their whole top t.  A constant input
+# makes every key equal (the select's shared-prefix trim takes all bits),
+# small integers leave thousands of ties in the union, S = 40000 leaves a
+# partial last sample block.
 @pytest.mark.parametrize("case", ["normal", "constant", "ints", "S40000", "bf16"])
+@pytest.mark.parametrize("k", [4096, 8192])
 @pytest.mark.parametrize("seed", [0, 3])
-def test_large_t_threshold(case, seed):
+def test_large_t_threshold(case, k, seed):
     N = 2**20
     rng = np.random.default_rng(31)
+
+    def regime(p):
+        mu = 1024 * p.t / p.S
+        assert p.t > 32 and (mu < 6 if k == 4096 else mu > 7), (p.S, p.t)
+
     if case == "bf16":
+        kb = 2048 if k == 4096 else 8192
         b = workloads.relu_normal_bf16(N, seed=31)
-        p = pk.plan(N, 2000)
-        assert p.t > 32
+        p = pk.plan(N, kb, 1e-3, 1.0)
+        regime(p)
         q = oracle_plan_of(p)
-        note(f"large t bf16 N={N} k=2000 seed={seed} S={p.S} t={p.t}")
-        vals, idx, info = pk.topk(gpu_bf16(b), 2000, seed=seed, p=p)
-        compare(vals, idx, info, oprofk.run(b, "bf16", 2000, q, seed), "bf16")
+        note(f"large t bf16 N={N} k={kb} seed={seed} S={p.S} t={p.t}")
+        vals, idx, info = pk.topk(gpu_bf16(b), kb, seed=seed, p=p)
+        compare(vals, idx, info, oprofk.run(b, "bf16", kb, q, seed), "bf16")
         return
     x = {"normal": lambda: rng.standard_normal(N).astype(np.float32),
          "constant": lambda: np.full(N, 1.5, dtype=np.float32),
          "ints": lambda: rng.integers(0, 300, N).astype(np.float32),
          "S40000": lambda: rng.standard_normal(N).astype(np.float32)}[case]()
     kw = dict(S_min=40000, S_max=40000) if case == "S40000" else {}
-    rec, ref = _f32_case(x, 4096, seed, eps=1e-3, **kw)
-    assert oracle_plan_of(pk.plan(N, 4096, 1e-3, 1.0, **kw), **kw).t > 32
+    regime(pk.plan(N, k, 1e-3, 1.0, **kw))
+    rec, ref = _f32_case(x, k, seed, eps=1e-3, **kw)
 
 
 @pytest.mark.parametrize("k,plateau,value", [(1024, 1000, 3.2), (4096, 2800, 3.0)])
