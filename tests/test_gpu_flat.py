@@ -133,9 +133,10 @@ def test_special_values_and_ties():
 # their cut keys, falling back to all sample keys on ties; at k = 8192 (mu
 # about 10) blocks of 4096 draws keep their whole top t.  A constant input
 # makes every key equal (the select's shared-prefix trim takes all bits),
-# small integers leave thousands of ties in the union, S = 40000 leaves a
-# partial last sample block.
-@pytest.mark.parametrize("case", ["normal", "constant", "ints", "S40000", "bf16"])
+# small integers leave thousands of ties in the union, S = 40002 leaves a
+# partial last sample block (66 draws with capped lists: not a multiple of
+# a thread's four, so the last keys are stored one by one).
+@pytest.mark.parametrize("case", ["normal", "constant", "ints", "S40002", "bf16"])
 @pytest.mark.parametrize("k", [4096, 8192])
 @pytest.mark.parametrize("seed", [0, 3])
 def test_large_t_threshold(case, k, seed):
@@ -159,8 +160,8 @@ def test_large_t_threshold(case, k, seed):
     x = {"normal": lambda: rng.standard_normal(N).astype(np.float32),
          "constant": lambda: np.full(N, 1.5, dtype=np.float32),
          "ints": lambda: rng.integers(0, 300, N).astype(np.float32),
-         "S40000": lambda: rng.standard_normal(N).astype(np.float32)}[case]()
-    kw = dict(S_min=40000, S_max=40000) if case == "S40000" else {}
+         "S40002": lambda: rng.standard_normal(N).astype(np.float32)}[case]()
+    kw = dict(S_min=40002, S_max=40002) if case == "S40002" else {}
     regime(pk.plan(N, k, 1e-3, 1.0, **kw))
     rec, ref = _f32_case(x, k, seed, eps=1e-3, **kw)
 
