@@ -7,9 +7,10 @@
 //   k_bkt_scatter  in every block, the status, bucket offsets in descending
 //                  bucket order from the filter's histogram of
 //                  log_bin(key - tau) and the bucket b* holding rank k
-//                  (block 0 records them, or the radix path's state when the
-//                  bucket path does not apply); then every candidate of a
-//                  bucket >= b* into its bucket's range of the staging array;
+//                  (block 0 records the plan); then every candidate of a
+//                  bucket >= b* into its bucket's range of the staging array.
+//                  When the bucket path does not apply, the blocks run the
+//                  radix path's first key digit pass instead;
 //   k_bkt_sort     one block per bucket sorts it in LDS and writes the
 //                  outputs at the bucket's offset.
 // Every other call (a fallback, DIRECT, or a bucket larger than kBktCap)
