@@ -415,6 +415,10 @@ struct SegSrc {
                      [&](uint32_t i, uint32_t v) { f(i, v, LoadIdx{idx + pos(i)}); });
   }
   __device__ __forceinline__ uint32_t idx_at(uint32_t i) const { return idx[pos(i)]; }
+  __device__ __forceinline__ uint2 pair_at(uint32_t i) const {
+    const size_t p = pos(i);
+    return uint2{key[p], idx[p]};
+  }
 };
 
 // The part of the input one fallback block owns, in index order: chunk b

@@ -10,6 +10,9 @@
 // top-k of the total order: larger key first, then smaller index.
 #pragma once
 
+#include <type_traits>
+#include <utility>
+
 #include "device_common.h"
 #include "filter_tile.h"
 
@@ -141,6 +144,13 @@ __device__ __forceinline__ void block_topk_core(const Src& src, uint32_t n, uint
   __syncthreads();
 }
 
+// Sources with pair_at(i) (key and index of candidate i) give both in one
+// load sweep.
+template <class S, class = void>
+struct HasPairAt : std::false_type {};
+template <class S>
+struct HasPairAt<S, std::void_t<decltype(std::declval<const S&>().pair_at(0u))>> : std::true_type {};
+
 template <int BS, int DIGIT, class Src>
 __device__ __forceinline__ void block_topk(const Src& src, uint32_t n, uint32_t kk, uint32_t lo_key,
                                            uint32_t hi_key, int keybits, const TopkSmem& sm) {
@@ -149,8 +159,30 @@ __device__ __forceinline__ void block_topk(const Src& src, uint32_t n, uint32_t 
     // and select there, so the passes on tied keys read no global memory
     uint32_t* const pk = sm.cache;
     uint32_t* const pi = sm.cache + n;
-    src.template visit<BS>(n, nullptr, [&](uint32_t i, uint32_t key, auto) { pk[i] = key; });
-    for_items<BS, 8>(n, [&](uint32_t i) { return src.idx_at(i); }, [&](uint32_t i, uint32_t v) { pi[i] = v; });
+    if constexpr (HasPairAt<Src>::value) {
+      // eight pairs per thread in flight per sweep (n is at most half the
+      // cache, far below 2^32)
+      constexpr int U = 8;
+      for (uint32_t base = 0; base < n; base += BS * U) {
+        uint2 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const uint32_t i = base + u * BS + threadIdx.x;
+          v[u] = i < n ? src.pair_at(i) : uint2{0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const uint32_t i = base + u * BS + threadIdx.x;
+          if (i < n) {
+            pk[i] = v[u].x;
+            pi[i] = v[u].y;
+          }
+        }
+      }
+    } else {
+      src.template visit<BS>(n, nullptr, [&](uint32_t i, uint32_t key, auto) { pk[i] = key; });
+      for_items<BS, 8>(n, [&](uint32_t i) { return src.idx_at(i); }, [&](uint32_t i, uint32_t v) { pi[i] = v; });
+    }
     __syncthreads();
     TopkSmem lds = sm;
     lds.cache = nullptr;
