@@ -463,7 +463,7 @@ __device__ __forceinline__ SelectResult block_select_kth(Visit visit, uint32_t k
 // Returns 0xFFFFFFFF when no draw carries tau (not for a tau taken from the
 // same draws).
 template <int BS, int DIGIT, class Draws>
-__device__ uint32_t tau_pair_index(Draws draws, uint32_t tau, uint32_t t, uint32_t* list, uint32_t cap,
+__device__ __forceinline__ uint32_t tau_pair_index(Draws draws, uint32_t tau, uint32_t t, uint32_t* list, uint32_t cap,
                                    uint32_t* hist, SelectScratch& scr, uint32_t* s_n) {
   if (threadIdx.x == 0) *s_n = 0;
   __syncthreads();

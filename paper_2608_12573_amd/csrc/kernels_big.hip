@@ -255,7 +255,7 @@ __device__ __forceinline__ bool radix_pending(const RadixVals& v) {
 // the state after the pass: the digit state, and the header too when
 // `head` (nothing had written the state before this pass).
 template <int DT, int STAGE, int BS>
-__device__ void radix_pass(const BigArgs& a, const RadixHead& h, RadixVals v, bool head, PassShared& sh) {
+__device__ __forceinline__ void radix_pass(const BigArgs& a, const RadixHead& h, RadixVals v, bool head, PassShared& sh) {
   const int hi = STAGE == 0 ? v.hi : v.ihi;
   const uint32_t tid = threadIdx.x;
   const int bits = hi < kBigDigit ? hi : kBigDigit;
