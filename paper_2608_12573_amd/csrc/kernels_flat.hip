@@ -411,8 +411,11 @@ struct SegSrc {
   }
   template <int BS, class F>
   __device__ __forceinline__ void visit(uint32_t n, const uint32_t* cache, F f) const {
-    for_items<BS, 8>(n, [&](uint32_t i) { return cache ? cache[i] : key[pos(i)]; },
-                     [&](uint32_t i, uint32_t v) { f(i, v, LoadIdx{idx + pos(i)}); });
+    // two loops, so that each load has one address space (a pointer chosen
+    // between the LDS cache and the segments would be loaded as generic)
+    auto body = [&](uint32_t i, uint32_t v) { f(i, v, LoadIdx{idx + pos(i)}); };
+    if (cache) for_items<BS, 8>(n, [&](uint32_t i) { return cache[i]; }, body);
+    else for_items<BS, 8>(n, [&](uint32_t i) { return key[pos(i)]; }, body);
   }
   __device__ __forceinline__ uint32_t idx_at(uint32_t i) const { return idx[pos(i)]; }
   __device__ __forceinline__ uint2 pair_at(uint32_t i) const {
