@@ -100,3 +100,30 @@ def test_lex_rows_constant_values():
     assert (q.S, q.t, q.M) == (p.S, p.t, p.M)
     statuses = _check_rows(bits, "bf16", k, p, q, seed=11)
     assert all(s == oprofk.STATUS_FILTERED for s in statuses)
+
+
+def test_lex_rows_config4_256_rows():
+    """The C4 batch (bf16 [4096, 131072], k = 32) under the lexicographic
+    rule: the whole batch on the GPU, 256 fixed rows checked against the
+    oracle (bf16 has few distinct values near the threshold, so ties at tau
+    are common), each with its own row stream."""
+    b = workloads.relu_normal_bf16((4096, 131072), seed=3)
+    B, D, k = b.shape[0], b.shape[1], 32
+    p = pk.plan_rows(D, k, 1e-6, 1.0, lexicographic=1)
+    q = oplan.plan_rows(D, k, 1e-6, 1.0, dataclasses.replace(oplan.ROW_OPTS, lexicographic=True))
+    assert (q.S, q.t, q.M) == (p.S, p.t, p.M) and p.lexicographic
+    note(f"lex config4 S={p.S} t={p.t} M={p.M}")
+    g = torch().from_numpy(b.view(np.int16)).cuda().view(torch().bfloat16)
+    vals, idx, info = pk.topk_rows(g, k, seed=0, p=p)
+    torch().cuda.synchronize()
+    gv = vals.view(torch().int16).cpu().numpy().view(np.uint16)
+    gi = idx.cpu().numpy()
+    recs = pk.read_info(info)
+    for r in np.arange(0, B, 16):
+        ref = oprofk.run(b[r], "bf16", k, q, 0, row=int(r))
+        rec = recs[r]
+        assert int(rec["status"]) == ref.status, r
+        assert int(rec["tau_key"]) == ref.tau_key and int(rec["count"]) == ref.count, r
+        assert int(rec["n_valid"]) == ref.n_valid, r
+        assert np.array_equal(gi[r], ref.idx), r
+        assert np.array_equal(gv[r], ref.vals), r
