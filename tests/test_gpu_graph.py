@@ -57,10 +57,11 @@ def test_graph_batchtopk_big_k():
 
 @pytest.mark.parametrize("case", ["bucket", "radix"])
 def test_graph_flat_k_above_4096(case):
-    # k > 4096: the bucket refinement on the caller's stream and the radix
-    # refinement on the library's second stream, both inside the capture;
-    # a plateau of 20000 equal keys at rank 3000 puts more candidates in
-    # one bucket than the bucket path takes, so that the radix path works
+    # k > 4096: the bucket refinement, and the radix refinement (whose first
+    # two digit passes run in the scatter and sort launches), each inside the
+    # capture; a plateau of 20000 equal keys at rank 3000 puts more
+    # candidates in one bucket than the bucket path takes, so that the radix
+    # path works (its plan, t = 164, also takes the capped sample lists)
     t = torch()
     if case == "bucket":
         x, k, eps = workloads.normal_f32(2**21 + 7, seed=21), 20000, 1e-6
