@@ -33,8 +33,10 @@ struct FilterArgs {
 };
 
 // The filter pass; the survival test is in filter_tile.h.
-// U: 16-byte loads in flight per lane and step.
-template <int DT, bool LEX, int U>
+// U: 16-byte loads per lane and step.  DB: the next step's loads are issued
+// before the current step is tested, which pays where most steps take the
+// survivor path and costs a little on the sparse stream of a large input.
+template <int DT, bool LEX, int U, bool DB>
 __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   constexpr int EPV = Elem<DT>::EPV;
   constexpr int ES = Elem<DT>::ES;
@@ -174,14 +176,23 @@ __global__ __launch_bounds__(kFiltBS) void k_filter(FilterArgs a) {
   };
 
   for (uint32_t vb = vbeg; vb < vend; vb += vstride) {
-    if (vb != vbeg) load_step(vb, th.neutral);
-    if (__ballot(tile_any<DT, U>(v, th)) == 0) continue;
+    u32x4 cur[U];
+    if constexpr (DB) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) cur[u] = v[u];
+      load_step(vb + vstride, th.neutral);
+    } else {
+      if (vb != vbeg) load_step(vb, th.neutral);
+#pragma unroll
+      for (int u = 0; u < U; ++u) cur[u] = v[u];
+    }
+    if (__ballot(tile_any<DT, U>(cur, th)) == 0) continue;
     // Rare path: per-vector survivor masks, one slot reservation per wave,
     // then a short loop over each lane's set bits.
-    const TileSparse<DT, U, kFiltBS, LEX> ts(v, th, vb, vend, tid, a.head);
+    const TileSparse<DT, U, kFiltBS, LEX> ts(cur, th, vb, vend, tid, a.head);
     uint32_t slot, first_over, gbase;
     reserve(ts.count(), slot, first_over, gbase);
-    ts.emit(v, [&](uint32_t key, uint32_t idx) { store(slot++, first_over, gbase, key, idx); });
+    ts.emit(cur, [&](uint32_t key, uint32_t idx) { store(slot++, first_over, gbase, key, idx); });
   }
 
   // Elements before the first aligned vector and after the last one.
@@ -242,8 +253,8 @@ int filter_blocks_per_cu(int dtype, int want) {
   if (cached[d] == 0) {
     int n = 0;
     const hipError_t e = d == 0
-        ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0, false, kFiltUSmall>, kFiltBS, 0)
-        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1, false, kFiltUSmall>, kFiltBS, 0);
+        ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<0, false, kFiltUSmall, true>, kFiltBS, 0)
+        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_filter<1, false, kFiltUSmall, true>, kFiltBS, 0);
     cached[d] = (e == hipSuccess && n > 0) ? n : kFiltPerCuDense;
   }
   return cached[d] < want ? cached[d] : want;
@@ -264,11 +275,18 @@ static hipError_t launch_filter_t(const FlatCall& c, CallState* st, const uint32
                 at<uint32_t>(c.ws, L.off_seg_idx), at<uint32_t>(c.ws, L.off_blk_max),
                 at<uint32_t>(c.ws, L.off_fhist)};
   if (c.ev_before) (void)hipEventRecord(c.ev_before, c.stream);
-  const bool large = L.filt_u == kFiltULarge;
-  if (lex && large) hipLaunchKernelGGL((k_filter<DT, true, kFiltULarge>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
-  else if (lex) hipLaunchKernelGGL((k_filter<DT, true, kFiltUSmall>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
-  else if (large) hipLaunchKernelGGL((k_filter<DT, false, kFiltULarge>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
-  else hipLaunchKernelGGL((k_filter<DT, false, kFiltUSmall>), dim3(L.G_f), dim3(kFiltBS), 0, c.stream, fa);
+  // small inputs are never sparse: their steps are always double-buffered
+  const bool large = L.filt_u == kFiltULarge, db = L.filt_db;
+  const dim3 G(L.G_f), BS(kFiltBS);
+  if (lex) {
+    if (!large) hipLaunchKernelGGL((k_filter<DT, true, kFiltUSmall, true>), G, BS, 0, c.stream, fa);
+    else if (db) hipLaunchKernelGGL((k_filter<DT, true, kFiltULarge, true>), G, BS, 0, c.stream, fa);
+    else hipLaunchKernelGGL((k_filter<DT, true, kFiltULarge, false>), G, BS, 0, c.stream, fa);
+  } else {
+    if (!large) hipLaunchKernelGGL((k_filter<DT, false, kFiltUSmall, true>), G, BS, 0, c.stream, fa);
+    else if (db) hipLaunchKernelGGL((k_filter<DT, false, kFiltULarge, true>), G, BS, 0, c.stream, fa);
+    else hipLaunchKernelGGL((k_filter<DT, false, kFiltULarge, false>), G, BS, 0, c.stream, fa);
+  }
   if (c.ev_after) (void)hipEventRecord(c.ev_after, c.stream);
   return hipGetLastError();
 }

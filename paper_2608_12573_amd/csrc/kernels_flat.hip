@@ -1031,6 +1031,7 @@ FlatLayout flat_layout(const profk_plan_t& p, int dtype, int num_cus) {
   const int per_cu = filter_blocks_per_cu(dtype, sparse ? kFiltPerCuSparse : kFiltPerCuDense);
   const uint32_t maxg = static_cast<uint32_t>(num_cus * per_cu < kFiltMaxBlocks ? num_cus * per_cu : kFiltMaxBlocks);
   L.filt_u = N * (dtype == PROFK_F32 ? 4u : 2u) >= kFiltSparseMinBytes ? kFiltULarge : kFiltUSmall;
+  L.filt_db = !sparse;
   uint32_t g = cdiv(cdiv(N, epv), kFiltBS * static_cast<uint32_t>(L.filt_u));
   L.G_f = g < 1 ? 1 : (g > maxg ? maxg : g);
   L.seg_cap = M;

@@ -99,6 +99,7 @@ struct FlatLayout {
   size_t off_cut = 0, off_all_keys = 0;       // capped lists: each block's cut key, every sample key
   uint32_t G_f = 0;                           // filter blocks
   int filt_u = 0;                             // 16-byte loads per lane and filter step
+  bool filt_db = true;                        // filter steps double-buffered (all but the sparse launch)
   uint32_t seg_cap = 0;                       // entries per candidate segment (= M)
   uint32_t G_fb = 0;                          // fallback blocks (at most)
   size_t off_state = 0, off_segcnt = 0, off_union = 0, off_blk_max = 0;
